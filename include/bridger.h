@@ -1,0 +1,188 @@
+/*
+ * bridger.h -- C ABI of the MI355X tree-ensemble prediction library.
+ *
+ * The library evaluates classical-ML tree ensembles (a single decision tree, a
+ * random forest, gradient-boosted trees; binary or multiclass) over a batch of
+ * rows.  In the paper's terms a tree model is a combination of comparison,
+ * conditional, assignment and aggregation operators (Sec. 4.2, the classical
+ * operator representation) lowered to the primitive operators of Table 4:
+ * gather/take (feature and node reads), less_equal (threshold compare),
+ * where / if_then_else (child choice), loop/while (descent), sum/mean
+ * (aggregation over trees) and exp/add/divide/max (link functions).  The frontend
+ * hands over a trained model's arrays (Sec. 4.1: the frontend converts models,
+ * the runtime reads the executable and the input data); here that is
+ * bridger_forest_create, and the runtime call is bridger_forest_predict.
+ *
+ * Semantics (the paper fixes no comparison, tie or NaN rule; these are the
+ * library's conventions):
+ *   - each tree starts at its tree-local node 0; a node is a leaf iff
+ *     left == right == -1;
+ *   - a row goes to the left child iff x[feature] <= threshold (ties go left);
+ *     comparisons are IEEE: a NaN feature value goes right, -0.0 == +0.0,
+ *     -inf goes left of every finite threshold and +inf goes right;
+ *   - tree t adds its leaf value to class tree_class[t] (or t mod n_classes);
+ *     per class the sum runs in ascending tree order, accumulated in double
+ *     precision; SUM starts from base_score[k]; MEAN is
+ *     base_score[k] + sum / (number of trees of class k);
+ *   - the transform is applied to the n_classes class values: identity,
+ *     sigmoid (n_classes == 1) or softmax (n_classes >= 2); results are
+ *     rounded once to float.
+ *
+ * Threading: calls on different handles are independent.  One handle may serve
+ * concurrent predict calls on different streams.  bridger_forest_set_kernel and
+ * bridger_forest_destroy must not overlap other calls on the same handle.
+ * Errors are reported through the return value; bridger_last_error() gives a
+ * message for the calling thread's most recent failure.  Nothing throws across
+ * this interface.
+ */
+#ifndef BRIDGER_H
+#define BRIDGER_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct bridger_forest *bridger_forest_t; /* opaque; immutable after create */
+
+typedef enum {
+  BRIDGER_OK = 0,
+  BRIDGER_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, shape, or handle/device mismatch */
+  BRIDGER_ERR_INVALID_FOREST = 2,   /* the arrays do not describe a valid forest          */
+  BRIDGER_ERR_UNSUPPORTED = 3,      /* valid, but the requested kernel cannot run it     */
+  BRIDGER_ERR_OUT_OF_MEMORY = 4,    /* host or device allocation failed                  */
+  BRIDGER_ERR_DEVICE = 5            /* no usable GPU, or a HIP call / launch failed      */
+} bridger_status;
+
+enum { BRIDGER_AGG_SUM = 0, BRIDGER_AGG_MEAN = 1 };
+enum { BRIDGER_XFORM_IDENTITY = 0, BRIDGER_XFORM_SIGMOID = 1, BRIDGER_XFORM_SOFTMAX = 2 };
+
+/* Kernel families.  AUTO picks PERFECT when every tree is a perfect binary tree of
+ * one common depth (1..10), else RAGGED when every tree fits an LDS chunk, else
+ * DIRECT.  PERFECT and RAGGED stage the trees through LDS (the data-movement
+ * model of Eq. 1 sizes the row tile and the tree chunks); DIRECT reads nodes
+ * from global memory and handles any forest. */
+enum {
+  BRIDGER_KERNEL_AUTO = 0,
+  BRIDGER_KERNEL_PERFECT = 1,
+  BRIDGER_KERNEL_RAGGED = 2,
+  BRIDGER_KERNEL_DIRECT = 3
+};
+
+/* Flags for bridger_forest_create_ex. */
+enum {
+  /* Validate and pack on the host only; no device is touched.  Predict calls on
+   * such a handle fail with BRIDGER_ERR_INVALID_ARGUMENT.  Used to inspect the
+   * packed layout and the launch plan on a machine without a GPU. */
+  BRIDGER_CREATE_HOST_ONLY = 1u
+};
+
+/*
+ * Build a forest handle from per-node arrays (all host pointers; every array is
+ * copied, so the caller may free them as soon as the call returns).
+ *   n_trees        >= 1
+ *   tree_offsets   [n_trees + 1] int64; tree t owns nodes [tree_offsets[t],
+ *                  tree_offsets[t+1]); tree_offsets[0] == 0; every tree has >= 1 node
+ *   feature        [N] int32 split feature, 0 <= f < n_features (ignored at leaves)
+ *   threshold      [N] float split threshold, not NaN (ignored at leaves)
+ *   left, right    [N] int32 tree-local child ids, or -1 and -1 for a leaf
+ *   value          [N] float leaf value (ignored at internal nodes)
+ *   n_features     >= 1, the row width every predict call must use
+ *   n_classes      K, 1 <= K <= 64, the output width
+ *   tree_class     [n_trees] int32 in [0, K), or NULL for t mod K
+ *   aggregate      BRIDGER_AGG_SUM or BRIDGER_AGG_MEAN (MEAN needs >= 1 tree per class)
+ *   transform      BRIDGER_XFORM_*; SIGMOID needs K == 1, SOFTMAX needs K >= 2
+ *   base_score     [K] float, or NULL for zeros
+ *   out            receives the handle (set to NULL on failure)
+ * Validation: every non-root node is the child of exactly one node and every
+ * node is reachable from node 0 (each tree is a tree), depth <= 64.
+ * Returns BRIDGER_ERR_INVALID_FOREST / _INVALID_ARGUMENT on bad input,
+ * BRIDGER_ERR_DEVICE when no GPU is usable, BRIDGER_ERR_OUT_OF_MEMORY.
+ * The packed forest is uploaded synchronously to the device current at the call.
+ */
+bridger_status bridger_forest_create(int32_t n_trees, const int64_t *tree_offsets,
+                                     const int32_t *feature, const float *threshold,
+                                     const int32_t *left, const int32_t *right,
+                                     const float *value, int32_t n_features, int32_t n_classes,
+                                     const int32_t *tree_class, int32_t aggregate,
+                                     int32_t transform, const float *base_score,
+                                     bridger_forest_t *out);
+
+/* As bridger_forest_create, with BRIDGER_CREATE_* flags. */
+bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_offsets,
+                                        const int32_t *feature, const float *threshold,
+                                        const int32_t *left, const int32_t *right,
+                                        const float *value, int32_t n_features,
+                                        int32_t n_classes, const int32_t *tree_class,
+                                        int32_t aggregate, int32_t transform,
+                                        const float *base_score, uint32_t flags,
+                                        bridger_forest_t *out);
+
+/*
+ * Predict n_rows rows.
+ *   X       device pointer, row-major float [n_rows, n_features], 4-byte aligned;
+ *           read only
+ *   out     device pointer, row-major float [n_rows, n_classes]; must not overlap X
+ *   stream  a hipStream_t (NULL = the null stream); the call is asynchronous on it
+ * n_features must equal the value given at create; n_rows == 0 launches nothing.
+ * Must be called with the handle's device current.  Launch failures return
+ * BRIDGER_ERR_DEVICE; faults during execution surface at the caller's sync.
+ */
+bridger_status bridger_forest_predict(bridger_forest_t h, const float *X, int64_t n_rows,
+                                      int32_t n_features, float *out, void *stream);
+
+/*
+ * Write, for every (row, tree), the id of the leaf the row reaches, in the
+ * caller's tree-local node numbering: device int32 [n_rows, n_trees], row-major
+ * (tree index in the caller's order).  Same arguments and rules as predict.
+ */
+bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X, int64_t n_rows,
+                                             int32_t n_features, int32_t *out_leaf,
+                                             void *stream);
+
+/* Shape facts.  Any output pointer may be NULL.  all_perfect = 1 when every tree
+ * is perfect with one common depth (then max_depth is that depth). */
+bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,
+                                   int32_t *n_outputs, int32_t *max_depth, int32_t *all_perfect);
+
+/* Select the kernel family (BRIDGER_KERNEL_*).  Returns BRIDGER_ERR_UNSUPPORTED
+ * (and keeps the current choice) when that family cannot evaluate this forest. */
+bridger_status bridger_forest_set_kernel(bridger_forest_t h, int32_t kernel);
+
+/* The kernel family predict will use (AUTO resolved). */
+bridger_status bridger_forest_get_kernel(bridger_forest_t h, int32_t *kernel);
+
+/*
+ * The launch plan predict would use for n_rows rows (the Eq. 1 choice):
+ * rows per workgroup, bytes of one LDS tree-chunk buffer, trees per chunk (0 when
+ * chunks hold a varying number of trees), number of chunks, LDS bytes per
+ * workgroup, and the modelled bytes moved per level (HBM, L2->LDS staging, LDS
+ * reads).  Any output pointer may be NULL.  Works on host-only handles.
+ */
+bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *rows_per_wg,
+                                   int32_t *chunk_bytes, int32_t *trees_per_chunk,
+                                   int32_t *n_chunks, int32_t *lds_bytes, double *hbm_bytes,
+                                   double *stage_bytes, double *lds_read_bytes);
+
+/*
+ * Read-only view of a host copy of the packed layout, for inspection and tests:
+ * which = 0 node records of the active kernel family, 1 per-tree start offsets,
+ * 2 leaf-id map (kernel leaf slot -> caller node id), 3 kernel tree order
+ * (kernel position -> caller tree index), 4 chunk table.  *ptr stays valid until
+ * destroy or set_kernel.
+ */
+bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
+                                     int64_t *bytes);
+
+/* Free the handle and its device memory (device-synchronizing).  NULL is a no-op. */
+void bridger_forest_destroy(bridger_forest_t h);
+
+/* Message for the calling thread's most recent failed call ("" if none). */
+const char *bridger_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BRIDGER_H */

@@ -1,0 +1,247 @@
+"""MI355X tree-ensemble prediction: Python binding of the C ABI in include/bridger.h.
+
+The functions named ``bridger_*`` marshal arguments to the entry points of the same
+name in ``libbridger.so`` (built by ``paper_2405_12491_amd.build``); every step of
+prediction runs in the library's HIP kernels.  ``Forest`` is a small convenience
+wrapper that takes numpy arrays for the model and torch CUDA tensors for the rows,
+using torch only for device memory and the current stream.  There is no CPU
+fallback: if the library is missing, importing the binding's functions raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbridger.so")
+
+BRIDGER_OK = 0
+BRIDGER_ERR_INVALID_ARGUMENT = 1
+BRIDGER_ERR_INVALID_FOREST = 2
+BRIDGER_ERR_UNSUPPORTED = 3
+BRIDGER_ERR_OUT_OF_MEMORY = 4
+BRIDGER_ERR_DEVICE = 5
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "INVALID_FOREST", 3: "UNSUPPORTED",
+                4: "OUT_OF_MEMORY", 5: "DEVICE"}
+
+BRIDGER_AGG_SUM, BRIDGER_AGG_MEAN = 0, 1
+BRIDGER_XFORM_IDENTITY, BRIDGER_XFORM_SIGMOID, BRIDGER_XFORM_SOFTMAX = 0, 1, 2
+BRIDGER_KERNEL_AUTO, BRIDGER_KERNEL_PERFECT, BRIDGER_KERNEL_RAGGED, BRIDGER_KERNEL_DIRECT = 0, 1, 2, 3
+KERNEL_NAMES = {0: "auto", 1: "perfect", 2: "ragged", 3: "direct"}
+BRIDGER_CREATE_HOST_ONLY = 1
+
+_lib = None
+
+
+class BridgerError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+def load_library(path: Optional[str] = None):
+    """Load libbridger.so (raises OSError if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise OSError(f"{p} not found: build it with `python -m paper_2405_12491_amd.build`")
+    lib = ctypes.CDLL(p)
+    P, I32, I64, U32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+    create_args = [I32, P, P, P, P, P, P, I32, I32, P, I32, I32, P]
+    lib.bridger_forest_create.argtypes = create_args + [P]
+    lib.bridger_forest_create_ex.argtypes = create_args + [U32, P]
+    lib.bridger_forest_predict.argtypes = [P, P, I64, I32, P, P]
+    lib.bridger_forest_predict_leaves.argtypes = [P, P, I64, I32, P, P]
+    lib.bridger_forest_info.argtypes = [P, P, P, P, P, P]
+    lib.bridger_forest_set_kernel.argtypes = [P, I32]
+    lib.bridger_forest_get_kernel.argtypes = [P, P]
+    lib.bridger_forest_plan.argtypes = [P, I64, P, P, P, P, P, P, P, P]
+    lib.bridger_forest_packed.argtypes = [P, I32, P, P]
+    lib.bridger_forest_destroy.argtypes = [P]
+    lib.bridger_forest_destroy.restype = None
+    lib.bridger_last_error.argtypes = []
+    lib.bridger_last_error.restype = ctypes.c_char_p
+    for name in ("bridger_forest_create", "bridger_forest_create_ex", "bridger_forest_predict",
+                 "bridger_forest_predict_leaves", "bridger_forest_info", "bridger_forest_set_kernel",
+                 "bridger_forest_get_kernel", "bridger_forest_plan", "bridger_forest_packed"):
+        getattr(lib, name).restype = ctypes.c_int
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != BRIDGER_OK:
+        msg = load_library().bridger_last_error().decode(errors="replace")
+        raise BridgerError(status, where, msg)
+
+
+def _vp(a):
+    if a is None:
+        return None
+    if isinstance(a, int):
+        return ctypes.c_void_p(a)
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ------------------------------------------------------------- raw entry points
+def bridger_forest_create(n_trees, tree_offsets, feature, threshold, left, right, value,
+                          n_features, n_classes, tree_class, aggregate, transform, base_score,
+                          flags: int = 0) -> ctypes.c_void_p:
+    """Returns the opaque handle; arrays are numpy arrays of the documented dtypes."""
+    lib = load_library()
+    h = ctypes.c_void_p()
+    arrs = [np.ascontiguousarray(tree_offsets, np.int64), np.ascontiguousarray(feature, np.int32),
+            np.ascontiguousarray(threshold, np.float32), np.ascontiguousarray(left, np.int32),
+            np.ascontiguousarray(right, np.int32), np.ascontiguousarray(value, np.float32)]
+    tc = None if tree_class is None else np.ascontiguousarray(tree_class, np.int32)
+    bs = None if base_score is None else np.ascontiguousarray(base_score, np.float32)
+    st = lib.bridger_forest_create_ex(int(n_trees), *[_vp(a) for a in arrs], int(n_features),
+                                      int(n_classes), _vp(tc), int(aggregate), int(transform),
+                                      _vp(bs), int(flags), ctypes.byref(h))
+    _check(st, "bridger_forest_create")
+    return h
+
+
+def bridger_forest_predict(h, X_ptr: int, n_rows: int, n_features: int, out_ptr: int, stream: int = 0):
+    _check(load_library().bridger_forest_predict(h, ctypes.c_void_p(X_ptr), int(n_rows),
+                                                 int(n_features), ctypes.c_void_p(out_ptr),
+                                                 ctypes.c_void_p(stream)), "bridger_forest_predict")
+
+
+def bridger_forest_predict_leaves(h, X_ptr: int, n_rows: int, n_features: int, out_ptr: int,
+                                  stream: int = 0):
+    _check(load_library().bridger_forest_predict_leaves(h, ctypes.c_void_p(X_ptr), int(n_rows),
+                                                        int(n_features), ctypes.c_void_p(out_ptr),
+                                                        ctypes.c_void_p(stream)),
+           "bridger_forest_predict_leaves")
+
+
+def bridger_forest_info(h) -> dict:
+    v = [ctypes.c_int32() for _ in range(5)]
+    _check(load_library().bridger_forest_info(h, *[ctypes.byref(x) for x in v]), "bridger_forest_info")
+    return dict(zip(("n_trees", "n_features", "n_outputs", "max_depth", "all_perfect"),
+                    (x.value for x in v)))
+
+
+def bridger_forest_set_kernel(h, kernel: int):
+    _check(load_library().bridger_forest_set_kernel(h, int(kernel)), "bridger_forest_set_kernel")
+
+
+def bridger_forest_get_kernel(h) -> int:
+    k = ctypes.c_int32()
+    _check(load_library().bridger_forest_get_kernel(h, ctypes.byref(k)), "bridger_forest_get_kernel")
+    return k.value
+
+
+def bridger_forest_plan(h, n_rows: int) -> dict:
+    i = [ctypes.c_int32() for _ in range(5)]
+    d = [ctypes.c_double() for _ in range(3)]
+    _check(load_library().bridger_forest_plan(h, int(n_rows), *[ctypes.byref(x) for x in i + d]),
+           "bridger_forest_plan")
+    keys = ("rows_per_wg", "chunk_bytes", "trees_per_chunk", "n_chunks", "lds_bytes",
+            "hbm_bytes", "stage_bytes", "lds_read_bytes")
+    return dict(zip(keys, [x.value for x in i + d]))
+
+
+def bridger_forest_packed(h, which: int, dtype) -> np.ndarray:
+    p = ctypes.c_void_p()
+    n = ctypes.c_int64()
+    _check(load_library().bridger_forest_packed(h, int(which), ctypes.byref(p), ctypes.byref(n)),
+           "bridger_forest_packed")
+    if n.value == 0:
+        return np.zeros(0, dtype)
+    buf = (ctypes.c_uint8 * n.value).from_address(p.value)
+    return np.frombuffer(bytes(buf), dtype=dtype).copy()
+
+
+def bridger_forest_destroy(h):
+    if h:
+        load_library().bridger_forest_destroy(h)
+
+
+def bridger_last_error() -> str:
+    return load_library().bridger_last_error().decode(errors="replace")
+
+
+# ---------------------------------------------------------------- convenience
+class Forest:
+    """Owns a forest handle.  ``model`` is any object with the fields of ``synth.Forest``."""
+
+    def __init__(self, model, kernel: int = BRIDGER_KERNEL_AUTO, host_only: bool = False):
+        self.n_features = int(model.n_features)
+        self.n_classes = int(model.n_classes)
+        self.n_trees = int(model.tree_offsets.shape[0] - 1)
+        self._h = bridger_forest_create(
+            self.n_trees, model.tree_offsets, model.feature, model.threshold, model.left, model.right,
+            model.value, self.n_features, self.n_classes, model.tree_class, model.aggregate,
+            model.transform, model.base_score, BRIDGER_CREATE_HOST_ONLY if host_only else 0)
+        if kernel != BRIDGER_KERNEL_AUTO:
+            bridger_forest_set_kernel(self._h, kernel)
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def kernel(self) -> int:
+        return bridger_forest_get_kernel(self._h)
+
+    @kernel.setter
+    def kernel(self, k: int):
+        bridger_forest_set_kernel(self._h, k)
+
+    def info(self) -> dict:
+        return bridger_forest_info(self._h)
+
+    def plan(self, n_rows: int) -> dict:
+        return bridger_forest_plan(self._h, n_rows)
+
+    def _check_x(self, X):
+        import torch
+        if not (isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == torch.float32):
+            raise TypeError("X must be a float32 CUDA tensor")
+        if X.dim() != 2 or X.shape[1] != self.n_features or not X.is_contiguous():
+            raise ValueError("X must be contiguous [n_rows, n_features]")
+
+    def predict(self, X, out=None):
+        import torch
+        self._check_x(X)
+        if out is None:
+            out = torch.empty((X.shape[0], self.n_classes), dtype=torch.float32, device=X.device)
+        stream = torch.cuda.current_stream(X.device).cuda_stream
+        bridger_forest_predict(self._h, X.data_ptr(), X.shape[0], self.n_features, out.data_ptr(),
+                               stream)
+        return out
+
+    def predict_leaves(self, X, out=None):
+        import torch
+        self._check_x(X)
+        if out is None:
+            out = torch.empty((X.shape[0], self.n_trees), dtype=torch.int32, device=X.device)
+        stream = torch.cuda.current_stream(X.device).cuda_stream
+        bridger_forest_predict_leaves(self._h, X.data_ptr(), X.shape[0], self.n_features,
+                                      out.data_ptr(), stream)
+        return out
+
+    def close(self):
+        if self._h:
+            bridger_forest_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

@@ -1,0 +1,879 @@
+// bridger_host.cpp -- C ABI, forest validation, packing and launch planning.
+//
+// create: validate the caller's node arrays, order trees by class (stable, so the per-class
+// sum keeps ascending tree order), detect perfect trees, pack the layouts of internal.h
+// ("data type rewriting" and "redundant operator elimination" of Table 2: narrow node
+// records, no stored child indices for perfect trees, no values at internal nodes), plan the
+// launch with the data-movement model of Eq. 1, and upload.  predict: check arguments and
+// launch on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <deque>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "bridger.h"
+#include "internal.h"
+
+using namespace bridger;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+bridger_status fail(bridger_status s, const std::string &msg) {
+  g_last_error = msg;
+  return s;
+}
+
+// ---------------------------------------------------------------- machine model
+// Constants of the Eq. 1 model (bytes/s per level).  HBM and LDS figures are measured on
+// MI355X by the calibration microbenchmarks; L2 is the per-XCD L2 request bandwidth summed
+// over the 8 XCDs.  The LDS level is counted in wave-wide instructions: a conflict-free
+// 32- or 64-bit per-lane gather costs one slot either way.
+constexpr double kHbmBytesPerSec = 5.0e12;
+constexpr double kL2BytesPerSec = 30.0e12;
+constexpr double kLdsInstrPerSec = 0.44 * 256 * 2.4e9;
+constexpr int kMaxWavesPerCU = 32;
+constexpr int kMinWavesPerCU = 8;
+constexpr int kPerfectTreesMultiple = 4;  // trees are traversed four at a time per lane
+
+int env_int(const char *name, int dflt) {
+  const char *v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::atoi(v);
+}
+
+int ilog2(int64_t v) {
+  int r = 0;
+  while ((int64_t(1) << (r + 1)) <= v) ++r;
+  return r;
+}
+
+struct DevArrays {
+  void *nodes = nullptr;
+  void *tree_start = nullptr;
+  void *chunk_first = nullptr;
+  void *chunk_rec = nullptr;
+  void *leaf_map = nullptr;
+};
+
+}  // namespace
+
+struct bridger_forest {
+  int32_t n_trees = 0, F = 0, K = 1, aggregate = 0, transform = 0;
+  int64_t n_nodes = 0;
+  int32_t max_depth = 0, all_perfect = 0, perfect_depth = -1;
+  bool host_only = false;
+  int device = -1;
+  int32_t kernel_active = kDirect;
+
+  std::vector<int32_t> tree_order;   // kernel position -> caller tree
+  std::vector<int32_t> class_begin;  // [K+1]
+  std::vector<int32_t> class_count;  // [K]
+  std::vector<float> base;           // [K]
+
+  // PERFECT
+  bool perfect_ok = false;
+  int32_t perfect_tree_bytes = 0;
+  std::vector<uint8_t> perfect_blob;
+  std::vector<int32_t> perfect_leaf_map;
+  Plan perfect_plan{};
+
+  // RAGGED
+  bool ragged_ok = false;
+  std::vector<uint64_t> ragged_rec;
+  std::vector<int32_t> ragged_tree_start;  // [T+1]
+  std::vector<int32_t> ragged_rec_node;
+  std::vector<int32_t> ragged_chunk_first, ragged_chunk_rec;
+  int64_t ragged_max_tree_bytes = 0;
+  Plan ragged_plan{};
+
+  // DIRECT
+  std::vector<int32_t> direct_rec;  // 4 ints per record
+  std::vector<int32_t> direct_root;
+  std::vector<int32_t> direct_rec_node;
+
+  // device copies
+  void *d_class_begin = nullptr, *d_class_count = nullptr, *d_base = nullptr,
+       *d_tree_order = nullptr;
+  DevArrays d_perfect, d_ragged, d_direct;
+  double visits_per_row_est = 0;  // for the model: mean internal visits per row (all trees)
+};
+
+namespace {
+
+// ------------------------------------------------------------------ validation
+struct TreeShape {
+  int32_t depth;    // max leaf depth
+  bool perfect;     // all leaves at depth `depth` and 2^(depth+1)-1 nodes
+  double mean_path; // mean leaf depth weighted uniformly (for the cost model only)
+};
+
+bridger_status validate_tree(int32_t t, int64_t n, const int32_t *feat, const float *thr,
+                             const int32_t *left, const int32_t *right, int32_t F,
+                             std::vector<int32_t> &depth_scratch, TreeShape &shape) {
+  if (n < 1)
+    return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " has no nodes");
+  std::vector<int32_t> parents(n, 0);
+  for (int64_t i = 0; i < n; ++i) {
+    const bool l_leaf = left[i] == -1, r_leaf = right[i] == -1;
+    if (l_leaf != r_leaf)
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " node " +
+                                                  std::to_string(i) + " has exactly one child");
+    if (l_leaf) continue;
+    if (left[i] < 0 || left[i] >= n || right[i] < 0 || right[i] >= n)
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " node " +
+                                                  std::to_string(i) + " child out of range");
+    if (left[i] == right[i])
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " node " +
+                                                  std::to_string(i) + " has identical children");
+    if (feat[i] < 0 || feat[i] >= F)
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " node " +
+                                                  std::to_string(i) + " feature out of range");
+    if (std::isnan(thr[i]))
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " node " +
+                                                  std::to_string(i) + " has a NaN threshold");
+    parents[left[i]]++;
+    parents[right[i]]++;
+  }
+  if (parents[0] != 0)
+    return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + ": root is a child");
+  for (int64_t i = 1; i < n; ++i)
+    if (parents[i] != 1)
+      return fail(BRIDGER_ERR_INVALID_FOREST,
+                  "tree " + std::to_string(t) + " node " + std::to_string(i) +
+                      (parents[i] ? " has several parents" : " is unreachable"));
+  // breadth-first from the root: depths, reachability (parents==1 everywhere + reached all)
+  depth_scratch.assign(n, -1);
+  std::vector<int64_t> q;
+  q.reserve(n);
+  q.push_back(0);
+  depth_scratch[0] = 0;
+  int32_t maxd = 0;
+  int64_t leaves = 0;
+  double path_sum = 0;
+  for (size_t qi = 0; qi < q.size(); ++qi) {
+    int64_t i = q[qi];
+    int32_t d = depth_scratch[i];
+    if (left[i] == -1) {
+      maxd = std::max(maxd, d);
+      ++leaves;
+      path_sum += d;
+      continue;
+    }
+    if (d + 1 > 64)
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " deeper than 64");
+    for (int32_t c : {left[i], right[i]}) {
+      if (depth_scratch[c] != -1)
+        return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " has a cycle");
+      depth_scratch[c] = d + 1;
+      q.push_back(c);
+    }
+  }
+  if ((int64_t)q.size() != n)
+    return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " has unreachable nodes");
+  shape.depth = maxd;
+  shape.perfect = (maxd <= 30) && (n == (int64_t(2) << maxd) - 1);
+  if (shape.perfect)
+    for (int64_t i = 0; i < n; ++i)
+      if (left[i] == -1 && depth_scratch[i] != maxd) shape.perfect = false;
+  shape.mean_path = leaves ? path_sum / leaves : 0;
+  return BRIDGER_OK;
+}
+
+// -------------------------------------------------------------------- packing
+void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *feat,
+                  const float *thr, const int32_t *left, const int32_t *right,
+                  const float *value) {
+  const int n_int = (1 << D) - 1, n_leaf = 1 << D;
+  int tb = 8 * n_int + 4 * n_leaf;
+  tb = (tb + 15) & ~15;
+  h->perfect_tree_bytes = tb;
+  h->perfect_blob.assign((size_t)tb * h->n_trees, 0);
+  h->perfect_leaf_map.assign((size_t)n_leaf * h->n_trees, -1);
+  std::vector<int32_t> heap_to_node((size_t)2 * n_leaf - 1);
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int32_t t = h->tree_order[k];
+    const int64_t a = offs[t];
+    // heap slot -> caller node
+    heap_to_node[0] = 0;
+    for (int s = 0; s < n_int; ++s) {
+      const int32_t nd = heap_to_node[s];
+      heap_to_node[2 * s + 1] = left[a + nd];
+      heap_to_node[2 * s + 2] = right[a + nd];
+    }
+    uint8_t *blk = h->perfect_blob.data() + (size_t)k * tb;
+    for (int s = 0; s < n_int; ++s) {
+      const int32_t nd = heap_to_node[s];
+      const float th = thr[a + nd];
+      const uint32_t f = (uint32_t)feat[a + nd];
+      std::memcpy(blk + 8 * s, &th, 4);
+      std::memcpy(blk + 8 * s + 4, &f, 4);
+    }
+    for (int j = 0; j < n_leaf; ++j) {
+      const int32_t nd = heap_to_node[n_int + j];
+      const float v = value[a + nd];
+      std::memcpy(blk + 8 * n_int + 4 * j, &v, 4);
+      h->perfect_leaf_map[(size_t)k * n_leaf + j] = nd;
+    }
+  }
+}
+
+// Breadth-first record order with adjacent children; returns false if a tree cannot be
+// encoded (child offset or feature index too large).
+bool pack_ragged(bridger_forest *h, const int64_t *offs, const int32_t *feat, const float *thr,
+                 const int32_t *left, const int32_t *right, const float *value) {
+  if (h->F > kMaxRaggedFeatures) return false;
+  h->ragged_rec.clear();
+  h->ragged_rec.reserve(h->n_nodes);
+  h->ragged_rec_node.clear();
+  h->ragged_rec_node.reserve(h->n_nodes);
+  h->ragged_tree_start.assign(h->n_trees + 1, 0);
+  h->ragged_max_tree_bytes = 0;
+  std::vector<int32_t> order;
+  std::vector<int32_t> slot;
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int32_t t = h->tree_order[k];
+    const int64_t a = offs[t], n = offs[t + 1] - offs[t];
+    const int64_t base = (int64_t)h->ragged_rec.size();
+    if (base + n + 1 > INT32_MAX) return false;
+    h->ragged_tree_start[k] = (int32_t)base;
+    order.assign(1, 0);
+    slot.assign(n, -1);
+    slot[0] = 0;
+    for (size_t qi = 0; qi < order.size(); ++qi) {
+      const int32_t nd = order[qi];
+      if (left[a + nd] == -1) continue;
+      slot[left[a + nd]] = (int32_t)order.size();
+      order.push_back(left[a + nd]);
+      slot[right[a + nd]] = (int32_t)order.size();
+      order.push_back(right[a + nd]);
+    }
+    const int64_t n_padded = n + (n & 1);  // even record count: trees start 16-byte aligned
+    for (int64_t s = 0; s < n; ++s) {
+      const int32_t nd = order[s];
+      uint32_t w, meta;
+      if (left[a + nd] == -1) {
+        const int64_t next_rel = n_padded - s;
+        if (next_rel > kMaxRel) return false;
+        std::memcpy(&w, &value[a + nd], 4);
+        meta = (uint32_t)kLeafFlag | (uint32_t)next_rel;
+      } else {
+        const int64_t rel = slot[left[a + nd]] - s;
+        if (rel < 1 || rel > kMaxRel) return false;
+        std::memcpy(&w, &thr[a + nd], 4);
+        meta = ((uint32_t)feat[a + nd] << 16) | (uint32_t)rel;
+      }
+      h->ragged_rec.push_back((uint64_t)w | ((uint64_t)meta << 32));
+      h->ragged_rec_node.push_back(nd);
+    }
+    if (n_padded != n) {  // filler record, never visited
+      h->ragged_rec.push_back((uint64_t)kLeafFlag << 32);
+      h->ragged_rec_node.push_back(-1);
+    }
+    h->ragged_max_tree_bytes = std::max<int64_t>(h->ragged_max_tree_bytes, 8 * n_padded);
+  }
+  h->ragged_tree_start[h->n_trees] = (int32_t)h->ragged_rec.size();
+  return true;
+}
+
+void pack_direct(bridger_forest *h, const int64_t *offs, const int32_t *feat, const float *thr,
+                 const int32_t *left, const int32_t *right, const float *value) {
+  h->direct_rec.assign((size_t)4 * h->n_nodes, 0);
+  h->direct_rec_node.assign(h->n_nodes, 0);
+  h->direct_root.assign(h->n_trees, 0);
+  int64_t r = 0;
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int32_t t = h->tree_order[k];
+    const int64_t a = offs[t], n = offs[t + 1] - offs[t];
+    h->direct_root[k] = (int32_t)r;
+    for (int64_t i = 0; i < n; ++i) {
+      int32_t *rec = &h->direct_rec[(size_t)4 * (r + i)];
+      float w = left[a + i] == -1 ? value[a + i] : thr[a + i];
+      std::memcpy(&rec[0], &w, 4);
+      rec[1] = left[a + i] == -1 ? -1 : feat[a + i];
+      rec[2] = left[a + i] == -1 ? -1 : (int32_t)(r + left[a + i]);
+      rec[3] = left[a + i] == -1 ? -1 : (int32_t)(r + right[a + i]);
+      h->direct_rec_node[r + i] = (int32_t)i;
+    }
+    r += n;
+  }
+}
+
+// -------------------------------------------------------------- Eq. 1 planner
+// Choose (waves per workgroup, rows per tile, chunk size) minimising the slowest level's
+// data-movement time max_l DataMove_l / BandWidth_l, subject to the LDS capacity of a CU
+// (DataOccupy_LDS < Capacity_LDS) and to keeping at least kMinWavesPerCU waves resident
+// (relaxed if nothing satisfies it).  Levels: HBM (X once, output once, forest once), L2->LDS
+// (the forest is staged once per workgroup), LDS reads (per-visit node and feature gathers,
+// plus one leaf read per tree).  Ties (the usual case: the LDS level binds) go to higher
+// occupancy, then to fewer chunks.
+struct PlanInput {
+  int64_t n_rows;
+  int32_t F, K, n_trees;
+  double forest_bytes;
+  int32_t tree_bytes;      // PERFECT: fixed block; RAGGED: largest tree
+  bool perfect;
+  double visits_per_row;
+};
+
+Plan choose_plan(const PlanInput &in) {
+  Plan best{};
+  double best_t = 1e300;
+  int best_waves_cu = -1, best_chunks = 1 << 30;
+  const int force_waves = env_int("BRIDGER_WAVES", 0);
+  const int force_rows = env_int("BRIDGER_ROWS", 0);
+  const int force_ct = env_int("BRIDGER_CHUNK_TREES", 0);
+  const int force_wg_per_cu = env_int("BRIDGER_WG_PER_CU", 0);
+  const int64_t n = std::max<int64_t>(in.n_rows, 1);
+  for (int pass = 0; pass < 2 && best_t == 1e300; ++pass) {
+    for (int W : {1, 2, 4, 8, 16}) {
+      if (force_waves && W != force_waves) continue;
+      for (int R = 32; R <= 64 * W; R *= 2) {
+        if (force_rows && R != force_rows) continue;
+        const int G = 64 * W / R;
+        if (G > 1 && !in.perfect && R < 64) continue;
+        const bool acc_lds = in.K > 1 || G > 1;
+        const int64_t x_tile = (int64_t)in.F * R * 4;
+        const int64_t acc_bytes = acc_lds ? (int64_t)in.K * G * R * 8 : 0;
+        for (int m = 1; m <= kMaxWavesPerCU / W; ++m) {  // workgroups per CU
+          if (force_wg_per_cu && m != force_wg_per_cu) continue;
+          if (pass == 0 && m * W < kMinWavesPerCU) continue;
+          const int64_t budget = kLdsBytesPerCU / m - x_tile - acc_bytes;
+          if (budget < 2 * (int64_t)in.tree_bytes) continue;
+          int64_t chunk = std::min<int64_t>(budget / 2, 65536);  // immediate-offset reach
+          int ct = 0;
+          int n_chunks;
+          if (in.perfect) {
+            ct = (int)(chunk / in.tree_bytes);
+            ct -= ct % kPerfectTreesMultiple;
+            if (ct < kPerfectTreesMultiple) {
+              if (in.n_trees < kPerfectTreesMultiple && ct >= in.n_trees) ct = in.n_trees;
+              else continue;
+            }
+            ct = std::min(ct, ((in.n_trees + kPerfectTreesMultiple - 1) / kPerfectTreesMultiple) *
+                                  kPerfectTreesMultiple);
+            if (force_ct) {
+              if (force_ct * (int64_t)in.tree_bytes > chunk) continue;
+              ct = force_ct;
+            }
+            // every lane group needs at least one quad of trees per chunk
+            if (ct < kPerfectTreesMultiple * G && in.n_trees >= kPerfectTreesMultiple * G) continue;
+            chunk = (int64_t)ct * in.tree_bytes;
+            n_chunks = (in.n_trees + ct - 1) / ct;
+          } else {
+            if (chunk < in.tree_bytes) continue;
+            chunk &= ~int64_t(1023);
+            if (chunk < in.tree_bytes) continue;
+            // lane groups split a chunk's trees: want a couple of trees per group on average
+            if (G > 1 && chunk < 2.0 * G * in.forest_bytes / in.n_trees) continue;
+            n_chunks = (int)std::ceil(in.forest_bytes / (0.9 * chunk));
+          }
+          const int64_t lds = 2 * chunk + x_tile + acc_bytes;
+          if (lds > kLdsBytesPerCU) continue;
+          const double n_wg = std::ceil((double)n / R);
+          const double hbm = (double)n * in.F * 4 + (double)n * in.K * 4 + in.forest_bytes;
+          const double stage = n_wg * in.forest_bytes + (double)n * in.F * 4;
+          const double lds_instr =
+              (double)n / 64.0 * (2.0 * in.visits_per_row + in.n_trees) +
+              n_wg * (in.forest_bytes / 1024.0);
+          const double t = std::max({hbm / kHbmBytesPerSec, stage / kL2BytesPerSec,
+                                     lds_instr / kLdsInstrPerSec});
+          const int waves_cu = m * W;
+          const bool better =
+              t < best_t * 0.999 ||
+              (t <= best_t * 1.001 &&
+               (waves_cu > best_waves_cu || (waves_cu == best_waves_cu && n_chunks < best_chunks)));
+          if (better) {
+            best_t = t;
+            best_waves_cu = waves_cu;
+            best_chunks = n_chunks;
+            best.waves = W;
+            best.rows_per_wg = R;
+            best.groups = G;
+            best.chunk_bytes = (int32_t)chunk;
+            best.trees_per_chunk = ct;
+            best.n_chunks = n_chunks;
+            best.lds_bytes = (int32_t)lds;
+            best.acc_in_lds = acc_lds;
+            best.hbm_bytes = hbm;
+            best.stage_bytes = stage;
+            best.lds_read_bytes = lds_instr * 256.0;
+            best.est_seconds = t;
+          }
+        }
+      }
+    }
+  }
+  if (best_t == 1e300) best.waves = 0;  // infeasible
+  return best;
+}
+
+void ragged_chunks(bridger_forest *h, int64_t chunk_bytes) {
+  h->ragged_chunk_first.assign(1, 0);
+  h->ragged_chunk_rec.assign(1, 0);
+  int64_t cur = 0;
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int64_t tbytes = 8 * (int64_t)(h->ragged_tree_start[k + 1] - h->ragged_tree_start[k]);
+    if (cur > 0 && cur + tbytes > chunk_bytes) {
+      h->ragged_chunk_first.push_back(k);
+      h->ragged_chunk_rec.push_back(h->ragged_tree_start[k]);
+      cur = 0;
+    }
+    cur += tbytes;
+  }
+  h->ragged_chunk_first.push_back(h->n_trees);
+  h->ragged_chunk_rec.push_back(h->ragged_tree_start[h->n_trees]);
+  h->ragged_plan.n_chunks = (int32_t)h->ragged_chunk_first.size() - 1;
+}
+
+// ------------------------------------------------------------------- device io
+template <class T>
+bridger_status upload(void **dst, const std::vector<T> &src, size_t pad = 0) {
+  const size_t bytes = src.size() * sizeof(T);
+  if (hipMalloc(dst, bytes + pad + 16) != hipSuccess) {
+    *dst = nullptr;
+    (void)hipGetLastError();
+    return fail(BRIDGER_ERR_OUT_OF_MEMORY, "device allocation failed");
+  }
+  if (pad && hipMemset(*dst, 0, bytes + pad + 16) != hipSuccess)
+    return fail(BRIDGER_ERR_DEVICE, "hipMemset failed");
+  if (bytes && hipMemcpy(*dst, src.data(), bytes, hipMemcpyHostToDevice) != hipSuccess)
+    return fail(BRIDGER_ERR_DEVICE, "hipMemcpy to device failed");
+  return BRIDGER_OK;
+}
+
+void free_dev(void *&p) {
+  if (p) (void)hipFree(p);
+  p = nullptr;
+}
+
+void free_all(bridger_forest *h) {
+  free_dev(h->d_class_begin);
+  free_dev(h->d_class_count);
+  free_dev(h->d_base);
+  free_dev(h->d_tree_order);
+  for (DevArrays *d : {&h->d_perfect, &h->d_ragged, &h->d_direct}) {
+    free_dev(d->nodes);
+    free_dev(d->tree_start);
+    free_dev(d->chunk_first);
+    free_dev(d->chunk_rec);
+    free_dev(d->leaf_map);
+  }
+}
+
+bridger_status upload_all(bridger_forest *h) {
+  bridger_status s;
+  if ((s = upload(&h->d_class_begin, h->class_begin)) != BRIDGER_OK) return s;
+  if ((s = upload(&h->d_class_count, h->class_count)) != BRIDGER_OK) return s;
+  if ((s = upload(&h->d_base, h->base)) != BRIDGER_OK) return s;
+  if ((s = upload(&h->d_tree_order, h->tree_order)) != BRIDGER_OK) return s;
+  if (h->perfect_ok) {
+    if ((s = upload(&h->d_perfect.nodes, h->perfect_blob, 1024)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_perfect.leaf_map, h->perfect_leaf_map)) != BRIDGER_OK) return s;
+  }
+  if (h->ragged_ok) {
+    if ((s = upload(&h->d_ragged.nodes, h->ragged_rec, 1024)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_ragged.tree_start, h->ragged_tree_start)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_ragged.chunk_first, h->ragged_chunk_first)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_ragged.chunk_rec, h->ragged_chunk_rec)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_ragged.leaf_map, h->ragged_rec_node)) != BRIDGER_OK) return s;
+  }
+  if ((s = upload(&h->d_direct.nodes, h->direct_rec)) != BRIDGER_OK) return s;
+  if ((s = upload(&h->d_direct.tree_start, h->direct_root)) != BRIDGER_OK) return s;
+  if ((s = upload(&h->d_direct.leaf_map, h->direct_rec_node)) != BRIDGER_OK) return s;
+  return BRIDGER_OK;
+}
+
+int32_t resolve_auto(const bridger_forest *h) {
+  if (h->perfect_ok) return kPerfect;
+  if (h->ragged_ok) return kRagged;
+  return kDirect;
+}
+
+bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_rows,
+                             int32_t n_features, const void *out) {
+  if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
+  if (h->host_only) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "handle was created host-only");
+  if (n_rows < 0) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_rows < 0");
+  if (n_features != h->F)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT,
+                "n_features " + std::to_string(n_features) + " != forest's " + std::to_string(h->F));
+  if (n_rows == 0) return BRIDGER_OK;
+  if (!X || !out) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null X or output pointer");
+  if (((uintptr_t)X & 3) || ((uintptr_t)out & 3))
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "X and output must be 4-byte aligned");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != h->device)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "the handle's device is not current");
+  if (n_rows > (int64_t)INT32_MAX * 64)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_rows too large");
+  return BRIDGER_OK;
+}
+
+bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int32_t n_features,
+                          float *out, int32_t *out_leaf, void *stream) {
+  g_last_error.clear();
+  bridger_status s = check_predict(h, X, n_rows, n_features, out ? (void *)out : (void *)out_leaf);
+  if (s != BRIDGER_OK || n_rows == 0) return s;
+  const uint8_t *xb = (const uint8_t *)X;
+  const uint8_t *ob = out ? (const uint8_t *)out : (const uint8_t *)out_leaf;
+  const size_t xbytes = (size_t)n_rows * h->F * 4;
+  const size_t obytes = (size_t)n_rows * (out ? h->K : h->n_trees) * 4;
+  if (xb < ob + obytes && ob < xb + xbytes)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
+
+  LaunchArgs a{};
+  a.X = X;
+  a.n_rows = n_rows;
+  a.F = h->F;
+  a.x_vec4 = ((uintptr_t)X % 16 == 0) && (h->F % 4 == 0);
+  a.out = out;
+  a.out_leaf = out_leaf;
+  a.class_begin = (const int32_t *)h->d_class_begin;
+  a.class_count = (const int32_t *)h->d_class_count;
+  a.base = (const float *)h->d_base;
+  a.tree_order = (const int32_t *)h->d_tree_order;
+  a.n_trees = h->n_trees;
+  a.K = h->K;
+  a.aggregate = h->aggregate;
+  a.transform = h->transform;
+  int err = 0;
+  if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
+    const Plan &p = h->kernel_active == kPerfect ? h->perfect_plan : h->ragged_plan;
+    const DevArrays &d = h->kernel_active == kPerfect ? h->d_perfect : h->d_ragged;
+    a.nodes = (const uint8_t *)d.nodes;
+    a.tree_start = (const int32_t *)d.tree_start;
+    a.chunk_first = (const int32_t *)d.chunk_first;
+    a.chunk_rec = (const int32_t *)d.chunk_rec;
+    a.leaf_map = (const int32_t *)d.leaf_map;
+    a.tree_bytes = h->perfect_tree_bytes;
+    a.trees_per_chunk = p.trees_per_chunk;
+    a.n_chunks = p.n_chunks;
+    a.rows_per_wg = p.rows_per_wg;
+    a.log2_row_bytes = ilog2(4 * (int64_t)p.rows_per_wg);
+    a.groups = p.groups;
+    a.chunk_bytes = p.chunk_bytes;
+    a.lds_x_off = 2 * p.chunk_bytes;
+    a.lds_acc_off = a.lds_x_off + h->F * p.rows_per_wg * 4;
+    a.acc_in_lds = p.acc_in_lds;
+    const int64_t n_wg = (n_rows + p.rows_per_wg - 1) / p.rows_per_wg;
+    if (h->kernel_active == kPerfect)
+      err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
+    else
+      err = launch_ragged(a, p.waves, n_wg, p.lds_bytes, stream);
+  } else {
+    a.nodes = (const uint8_t *)h->d_direct.nodes;
+    a.tree_start = (const int32_t *)h->d_direct.tree_start;
+    a.leaf_map = (const int32_t *)h->d_direct.leaf_map;
+    const int64_t n_wg = (n_rows + 255) / 256;
+    err = launch_direct(a, n_wg, stream);
+  }
+  if (err != 0)
+    return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
+                                        hipGetErrorString((hipError_t)err));
+  return BRIDGER_OK;
+}
+
+}  // namespace
+
+// ========================================================================== ABI
+extern "C" {
+
+const char *bridger_last_error(void) { return g_last_error.c_str(); }
+
+bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_offsets,
+                                        const int32_t *feature, const float *threshold,
+                                        const int32_t *left, const int32_t *right,
+                                        const float *value, int32_t n_features,
+                                        int32_t n_classes, const int32_t *tree_class,
+                                        int32_t aggregate, int32_t transform,
+                                        const float *base_score, uint32_t flags,
+                                        bridger_forest_t *out) {
+  g_last_error.clear();
+  if (!out) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null output handle pointer");
+  *out = nullptr;
+  if (n_trees < 1) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_trees must be >= 1");
+  if (!tree_offsets || !feature || !threshold || !left || !right || !value)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null forest array");
+  if (n_features < 1) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_features must be >= 1");
+  if (n_classes < 1) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_classes must be >= 1");
+  if (n_classes > kMaxClasses)
+    return fail(BRIDGER_ERR_UNSUPPORTED, "n_classes above " + std::to_string(kMaxClasses));
+  if (aggregate != BRIDGER_AGG_SUM && aggregate != BRIDGER_AGG_MEAN)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown aggregate");
+  if (transform < BRIDGER_XFORM_IDENTITY || transform > BRIDGER_XFORM_SOFTMAX)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown transform");
+  if (transform == BRIDGER_XFORM_SIGMOID && n_classes != 1)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "sigmoid needs n_classes == 1");
+  if (transform == BRIDGER_XFORM_SOFTMAX && n_classes < 2)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "softmax needs n_classes >= 2");
+  if (flags & ~(uint32_t)BRIDGER_CREATE_HOST_ONLY)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown flags");
+  if (tree_offsets[0] != 0) return fail(BRIDGER_ERR_INVALID_FOREST, "tree_offsets[0] != 0");
+  for (int32_t t = 0; t < n_trees; ++t)
+    if (tree_offsets[t + 1] <= tree_offsets[t])
+      return fail(BRIDGER_ERR_INVALID_FOREST, "tree " + std::to_string(t) + " has no nodes");
+  if (tree_offsets[n_trees] > (int64_t)INT32_MAX / 4)
+    return fail(BRIDGER_ERR_UNSUPPORTED, "too many nodes");
+  std::vector<int32_t> klass(n_trees);
+  for (int32_t t = 0; t < n_trees; ++t) {
+    klass[t] = tree_class ? tree_class[t] : t % n_classes;
+    if (klass[t] < 0 || klass[t] >= n_classes)
+      return fail(BRIDGER_ERR_INVALID_ARGUMENT, "tree_class out of range");
+  }
+
+  bridger_forest *h = new (std::nothrow) bridger_forest();
+  if (!h) return fail(BRIDGER_ERR_OUT_OF_MEMORY, "host allocation failed");
+  try {
+    h->n_trees = n_trees;
+    h->F = n_features;
+    h->K = n_classes;
+    h->aggregate = aggregate;
+    h->transform = transform;
+    h->n_nodes = tree_offsets[n_trees];
+    h->host_only = (flags & BRIDGER_CREATE_HOST_ONLY) != 0;
+
+    // validation and shape
+    std::vector<int32_t> scratch;
+    int32_t common_depth = -2;
+    bool all_perfect = true;
+    double visits = 0;
+    for (int32_t t = 0; t < n_trees; ++t) {
+      const int64_t a = tree_offsets[t], n = tree_offsets[t + 1] - a;
+      TreeShape sh;
+      bridger_status s = validate_tree(t, n, feature + a, threshold + a, left + a, right + a,
+                                       n_features, scratch, sh);
+      if (s != BRIDGER_OK) {
+        delete h;
+        return s;
+      }
+      h->max_depth = std::max(h->max_depth, sh.depth);
+      if (!sh.perfect) all_perfect = false;
+      if (common_depth == -2) common_depth = sh.depth;
+      else if (common_depth != sh.depth) all_perfect = false;
+      visits += sh.perfect ? sh.depth : sh.mean_path;
+    }
+    h->visits_per_row_est = visits;
+    h->all_perfect = all_perfect ? 1 : 0;
+    h->perfect_depth = all_perfect ? common_depth : -1;
+
+    // class-major stable tree order
+    h->class_count.assign(n_classes, 0);
+    for (int32_t t = 0; t < n_trees; ++t) h->class_count[klass[t]]++;
+    if (aggregate == BRIDGER_AGG_MEAN)
+      for (int32_t k = 0; k < n_classes; ++k)
+        if (h->class_count[k] == 0) {
+          delete h;
+          return fail(BRIDGER_ERR_INVALID_ARGUMENT,
+                      "mean needs at least one tree in class " + std::to_string(k));
+        }
+    h->class_begin.assign(n_classes + 1, 0);
+    for (int32_t k = 0; k < n_classes; ++k)
+      h->class_begin[k + 1] = h->class_begin[k] + h->class_count[k];
+    h->tree_order.resize(n_trees);
+    {
+      std::vector<int32_t> fill(h->class_begin.begin(), h->class_begin.end() - 1);
+      for (int32_t t = 0; t < n_trees; ++t) h->tree_order[fill[klass[t]]++] = t;
+    }
+    h->base.assign(n_classes, 0.0f);
+    if (base_score)
+      for (int32_t k = 0; k < n_classes; ++k) h->base[k] = base_score[k];
+
+    // packing
+    pack_direct(h, tree_offsets, feature, threshold, left, right, value);
+    const int D = h->perfect_depth;
+    if (all_perfect && D >= 1 && D <= kMaxPerfectDepth) {
+      pack_perfect(h, D, tree_offsets, feature, threshold, left, right, value);
+      PlanInput pin{1 << 20, n_features, n_classes, n_trees,
+                    (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
+      h->perfect_plan = choose_plan(pin);
+      h->perfect_ok = h->perfect_plan.waves > 0;
+    }
+    if (pack_ragged(h, tree_offsets, feature, threshold, left, right, value)) {
+      PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
+                    (int32_t)std::min<int64_t>(h->ragged_max_tree_bytes, INT32_MAX), false, visits};
+      h->ragged_plan = choose_plan(pin);
+      h->ragged_ok = h->ragged_plan.waves > 0;
+      if (h->ragged_ok) ragged_chunks(h, h->ragged_plan.chunk_bytes);
+    }
+    h->kernel_active = resolve_auto(h);
+    const int forced = env_int("BRIDGER_KERNEL", 0);
+    if (forced == kPerfect && h->perfect_ok) h->kernel_active = kPerfect;
+    if (forced == kRagged && h->ragged_ok) h->kernel_active = kRagged;
+    if (forced == kDirect) h->kernel_active = kDirect;
+
+    if (!h->host_only) {
+      int ndev = 0;
+      if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
+        (void)hipGetLastError();
+        delete h;
+        return fail(BRIDGER_ERR_DEVICE, "no HIP device available");
+      }
+      if (hipGetDevice(&h->device) != hipSuccess) {
+        delete h;
+        return fail(BRIDGER_ERR_DEVICE, "hipGetDevice failed");
+      }
+      bridger_status s = upload_all(h);
+      if (s != BRIDGER_OK) {
+        std::string msg = g_last_error;
+        free_all(h);
+        delete h;
+        return fail(s, msg);
+      }
+    }
+  } catch (const std::bad_alloc &) {
+    free_all(h);
+    delete h;
+    return fail(BRIDGER_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  *out = h;
+  return BRIDGER_OK;
+}
+
+bridger_status bridger_forest_create(int32_t n_trees, const int64_t *tree_offsets,
+                                     const int32_t *feature, const float *threshold,
+                                     const int32_t *left, const int32_t *right,
+                                     const float *value, int32_t n_features, int32_t n_classes,
+                                     const int32_t *tree_class, int32_t aggregate,
+                                     int32_t transform, const float *base_score,
+                                     bridger_forest_t *out) {
+  return bridger_forest_create_ex(n_trees, tree_offsets, feature, threshold, left, right, value,
+                                  n_features, n_classes, tree_class, aggregate, transform,
+                                  base_score, 0u, out);
+}
+
+bridger_status bridger_forest_predict(bridger_forest_t h, const float *X, int64_t n_rows,
+                                      int32_t n_features, float *out, void *stream) {
+  return do_predict(h, X, n_rows, n_features, out, nullptr, stream);
+}
+
+bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X, int64_t n_rows,
+                                             int32_t n_features, int32_t *out_leaf,
+                                             void *stream) {
+  return do_predict(h, X, n_rows, n_features, nullptr, out_leaf, stream);
+}
+
+bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,
+                                   int32_t *n_outputs, int32_t *max_depth, int32_t *all_perfect) {
+  g_last_error.clear();
+  if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
+  if (n_trees) *n_trees = h->n_trees;
+  if (n_features) *n_features = h->F;
+  if (n_outputs) *n_outputs = h->K;
+  if (max_depth) *max_depth = h->max_depth;
+  if (all_perfect) *all_perfect = h->all_perfect;
+  return BRIDGER_OK;
+}
+
+bridger_status bridger_forest_set_kernel(bridger_forest_t h, int32_t kernel) {
+  g_last_error.clear();
+  if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
+  switch (kernel) {
+    case BRIDGER_KERNEL_AUTO: h->kernel_active = resolve_auto(h); return BRIDGER_OK;
+    case BRIDGER_KERNEL_PERFECT:
+      if (!h->perfect_ok)
+        return fail(BRIDGER_ERR_UNSUPPORTED, "forest is not all perfect trees of one depth 1..10");
+      h->kernel_active = kPerfect;
+      return BRIDGER_OK;
+    case BRIDGER_KERNEL_RAGGED:
+      if (!h->ragged_ok)
+        return fail(BRIDGER_ERR_UNSUPPORTED, "a tree does not fit the LDS-chunked layout");
+      h->kernel_active = kRagged;
+      return BRIDGER_OK;
+    case BRIDGER_KERNEL_DIRECT: h->kernel_active = kDirect; return BRIDGER_OK;
+    default: return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown kernel");
+  }
+}
+
+bridger_status bridger_forest_get_kernel(bridger_forest_t h, int32_t *kernel) {
+  g_last_error.clear();
+  if (!h || !kernel) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null argument");
+  *kernel = h->kernel_active;
+  return BRIDGER_OK;
+}
+
+bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *rows_per_wg,
+                                   int32_t *chunk_bytes, int32_t *trees_per_chunk,
+                                   int32_t *n_chunks, int32_t *lds_bytes, double *hbm_bytes,
+                                   double *stage_bytes, double *lds_read_bytes) {
+  g_last_error.clear();
+  if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
+  if (n_rows < 0) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_rows < 0");
+  Plan p{};
+  double forest_bytes = 0;
+  if (h->kernel_active == kPerfect) {
+    p = h->perfect_plan;
+    forest_bytes = (double)h->perfect_blob.size();
+  } else if (h->kernel_active == kRagged) {
+    p = h->ragged_plan;
+    forest_bytes = 8.0 * h->ragged_rec.size();
+  } else {
+    p.rows_per_wg = 256;
+    p.waves = 4;
+    forest_bytes = 16.0 * h->n_nodes;
+  }
+  const double n = (double)n_rows;
+  const double n_wg = std::ceil(n / std::max(p.rows_per_wg, 1));
+  if (rows_per_wg) *rows_per_wg = p.rows_per_wg;
+  if (chunk_bytes) *chunk_bytes = p.chunk_bytes;
+  if (trees_per_chunk) *trees_per_chunk = p.trees_per_chunk;
+  if (n_chunks) *n_chunks = p.n_chunks;
+  if (lds_bytes) *lds_bytes = p.lds_bytes;
+  if (hbm_bytes) *hbm_bytes = n * h->F * 4 + n * h->K * 4 + forest_bytes;
+  if (stage_bytes)
+    *stage_bytes = (h->kernel_active == kDirect) ? 0.0 : n_wg * forest_bytes + n * h->F * 4;
+  if (lds_read_bytes)
+    *lds_read_bytes = (h->kernel_active == kDirect)
+                          ? 0.0
+                          : 256.0 * (n / 64.0 * (2.0 * h->visits_per_row_est + h->n_trees) +
+                                     n_wg * forest_bytes / 1024.0);
+  return BRIDGER_OK;
+}
+
+bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
+                                     int64_t *bytes) {
+  g_last_error.clear();
+  if (!h || !ptr || !bytes) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null argument");
+  *ptr = nullptr;
+  *bytes = 0;
+  auto give = [&](const void *p, size_t b) {
+    *ptr = p;
+    *bytes = (int64_t)b;
+    return BRIDGER_OK;
+  };
+  if (which == 3) return give(h->tree_order.data(), h->tree_order.size() * 4);
+  switch (h->kernel_active) {
+    case kPerfect:
+      if (which == 0) return give(h->perfect_blob.data(), h->perfect_blob.size());
+      if (which == 2) return give(h->perfect_leaf_map.data(), h->perfect_leaf_map.size() * 4);
+      break;
+    case kRagged:
+      if (which == 0) return give(h->ragged_rec.data(), h->ragged_rec.size() * 8);
+      if (which == 1) return give(h->ragged_tree_start.data(), h->ragged_tree_start.size() * 4);
+      if (which == 2) return give(h->ragged_rec_node.data(), h->ragged_rec_node.size() * 4);
+      if (which == 4) return give(h->ragged_chunk_first.data(), h->ragged_chunk_first.size() * 4);
+      break;
+    default:
+      if (which == 0) return give(h->direct_rec.data(), h->direct_rec.size() * 4);
+      if (which == 1) return give(h->direct_root.data(), h->direct_root.size() * 4);
+      if (which == 2) return give(h->direct_rec_node.data(), h->direct_rec_node.size() * 4);
+      break;
+  }
+  return fail(BRIDGER_ERR_INVALID_ARGUMENT, "no such packed array for the active kernel");
+}
+
+void bridger_forest_destroy(bridger_forest_t h) {
+  if (!h) return;
+  if (!h->host_only) free_all(h);
+  delete h;
+}
+
+}  // extern "C"

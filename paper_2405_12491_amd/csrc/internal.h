@@ -1,0 +1,90 @@
+// internal.h -- layouts and launch descriptors shared by the host code and the HIP kernels.
+//
+// Packed layouts (all little-endian, built once by bridger_forest_create):
+//
+// PERFECT (every tree perfect with one depth D, 1 <= D <= kMaxPerfectDepth):
+//   one block of tree_bytes per tree, in kernel tree order (trees stably sorted by class):
+//     [0, 8*(2^D - 1))        internal records {float threshold; uint32 feature}, breadth-first
+//                             heap order (children of slot n are 2n+1 and 2n+2)
+//     [8*(2^D - 1), +4*2^D)   leaf values, leaf slot j = heap slot 2^D - 1 + j
+//     padding up to a multiple of 16 bytes
+//
+// RAGGED (any tree whose records fit one LDS chunk):
+//   8-byte records {uint32 w; uint32 meta}, trees contiguous in kernel order, each tree
+//   breadth-first with the two children of a node adjacent (right = left + 1):
+//     internal: w = threshold bits, meta = feature << 16 | left_rel   (1 <= left_rel <= 0x7FFF,
+//               left child = this record + left_rel)
+//     leaf    : w = value bits,     meta = 0x8000 | next_rel           (next_rel = records to the
+//               next tree's root, i.e. to the end of this tree)
+//   Trees are grouped into chunks of at most chunk_bytes; a chunk is staged to LDS whole.
+//
+// DIRECT (any forest): 16-byte records {float w; int32 feature (-1 at a leaf); int32 left;
+//   int32 right} with absolute record indices; kernel tree t starts at record root[t].
+#pragma once
+#include <stdint.h>
+
+namespace bridger {
+
+constexpr int kMaxPerfectDepth = 10;
+constexpr int kLdsBytesPerCU = 163840;
+constexpr int kLeafFlag = 0x8000;
+constexpr int kMaxRel = 0x7FFF;
+constexpr int kMaxRaggedFeatures = 0xFFFF;
+constexpr int kMaxClasses = 64;  // class sums of one 256-row block fit LDS in every kernel
+
+enum Kernel { kAuto = 0, kPerfect = 1, kRagged = 2, kDirect = 3 };
+
+// Launch plan (host side), chosen by the data-movement model of Eq. 1.
+struct Plan {
+  int32_t waves;           // waves per workgroup
+  int32_t rows_per_wg;     // R: rows held in the LDS feature tile (power of two, >= 32)
+  int32_t groups;          // G = 64*waves / R: tree groups sharing the row tile
+  int32_t chunk_bytes;     // bytes of one LDS chunk buffer (two are used, double-buffered)
+  int32_t trees_per_chunk; // PERFECT: fixed trees per chunk; RAGGED: 0 (variable)
+  int32_t n_chunks;
+  int32_t lds_bytes;       // dynamic LDS per workgroup
+  int32_t acc_in_lds;      // class/group partial sums kept in LDS
+  double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
+};
+
+// Everything a kernel needs; passed by value (lands in SGPRs / the kernarg segment).
+struct LaunchArgs {
+  const float *X;
+  int64_t n_rows;
+  int32_t F;
+  int32_t x_vec4;          // rows are 16-byte aligned and F % 4 == 0
+  float *out;              // [n_rows, K] (scores) or nullptr
+  int32_t *out_leaf;       // [n_rows, n_trees] (leaf ids) or nullptr
+  const uint8_t *nodes;    // packed records of the kernel family
+  const int32_t *tree_start;   // RAGGED: record index of each kernel tree's root; DIRECT: same
+  const int32_t *chunk_first;  // RAGGED: first kernel tree of each chunk [n_chunks + 1]
+  const int32_t *chunk_rec;    // RAGGED: first record of each chunk [n_chunks + 1]
+  const int32_t *class_begin;  // [K + 1] first kernel tree of each class
+  const int32_t *class_count;  // [K] trees per class
+  const float *base;           // [K]
+  const int32_t *tree_order;   // kernel tree -> caller tree
+  const int32_t *leaf_map;     // PERFECT: kernel tree * 2^D + slot -> caller node id;
+                               // RAGGED/DIRECT: record -> caller node id
+  int32_t n_trees;
+  int32_t K;
+  int32_t aggregate;
+  int32_t transform;
+  int32_t tree_bytes;          // PERFECT
+  int32_t trees_per_chunk;     // PERFECT
+  int32_t n_chunks;
+  int32_t rows_per_wg;         // R
+  int32_t log2_row_bytes;      // log2(4 * R): feature f's row of the LDS tile starts at f << this
+  int32_t groups;              // G
+  int32_t chunk_bytes;
+  int32_t lds_x_off;           // byte offset of the feature tile in dynamic LDS
+  int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
+  int32_t acc_in_lds;
+};
+
+// Kernel launchers (defined in the .hip files).  Return a hipError_t as int.
+int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                   void *stream);
+int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
+int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream);
+
+}  // namespace bridger

@@ -1,0 +1,497 @@
+// kernels.hip -- gfx950 kernels for batched tree-ensemble prediction.
+//
+// One fused kernel per launch runs the whole lowered pipeline of a tree model (Sec. 4.2 and
+// Table 4): gather the split feature of the current node (take/gather), compare it with the
+// threshold (less_equal), pick the child (where), descend (loop/while), fetch the leaf and
+// aggregate over trees (sum/mean), then apply the link function (exp/add/divide/max).  No
+// intermediate tensor leaves the chip (the cross-domain fusion idea of Sec. 4.3 applied to
+// one model).
+//
+// Work decomposition (the "tile", "split" and "parallel" schedules of Table 5, sized by the
+// Eq. 1 planner on the host):
+//   * a workgroup owns R consecutive rows; their features are copied once from HBM into an
+//     LDS tile stored feature-major (x of feature f, row r at byte 4*(f*R + r)).  Lane r of
+//     every 32-lane half-wave then reads a different LDS bank whatever feature it needs, so
+//     the per-lane feature gather is conflict-free;
+//   * the trees stream through two LDS chunk buffers: while the waves traverse chunk c, the
+//     direct global->LDS loads for chunk c+1 are in flight (one barrier per chunk);
+//   * with 64*waves == R every lane owns one row and adds its leaves in ascending tree order
+//     (bit-identical to a sequential sum); with 64*waves > R the G = 64*waves/R lane groups
+//     split the trees and their per-class partial sums are added in group order at the end.
+// Sums are kept in double precision; the output is rounded once to float.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <map>
+#include <mutex>
+
+#include "internal.h"
+
+namespace bridger {
+
+typedef __attribute__((address_space(3))) uint8_t lds_byte;
+
+// The kernels declare no static LDS, so dynamic LDS starts at LDS address 0 and a byte
+// offset into it is directly an LDS address (no base add on every access).
+__device__ __forceinline__ float lds_f32(const uint8_t *, uint32_t addr) {
+  return *(const __attribute__((address_space(3))) float *)(uintptr_t)addr;
+}
+__device__ __forceinline__ uint2 lds_u64(const uint8_t *, uint32_t addr) {
+  const uint64_t v = *(const __attribute__((address_space(3))) uint64_t *)(uintptr_t)addr;
+  return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+// Hide a value from the optimiser so a select between two precomputed offsets stays one
+// v_cndmask instead of being re-derived (select of constants, then a subtract) per level.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// Stage `bytes` (multiple of 16) from global memory into LDS at byte offset `dst` with
+// direct global->LDS loads: each wave instruction moves 1 KB (64 lanes x 16 bytes).
+__device__ __forceinline__ void stage_async(uint8_t *smem, uint32_t dst, const uint8_t *src,
+                                            int bytes, int wave, int lane, int waves) {
+  for (int off = wave * 1024; off < bytes; off += waves * 1024) {
+    if (off + lane * 16 < bytes) {
+      __builtin_amdgcn_global_load_lds(
+          (const void *)(src + off + lane * 16),
+          (__attribute__((address_space(3))) void *)((lds_byte *)smem + dst + off), 16, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void wait_stage() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Load this lane's row into the feature-major LDS tile (zeros past the last row).
+__device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a, int r,
+                                              int64_t row, bool row_ok) {
+  float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
+  const int R = a.rows_per_wg;
+  if (!row_ok) {
+    for (int f = 0; f < a.F; ++f) xt[f * R + r] = 0.0f;
+    return;
+  }
+  const float *xr = a.X + row * (int64_t)a.F;
+  if (a.x_vec4) {
+    const float4 *x4 = reinterpret_cast<const float4 *>(xr);
+    const int n4 = a.F >> 2;
+    int i = 0;
+    for (; i + 2 <= n4; i += 2) {
+      float4 v0 = x4[i], v1 = x4[i + 1];
+      xt[(4 * i + 0) * R + r] = v0.x;
+      xt[(4 * i + 1) * R + r] = v0.y;
+      xt[(4 * i + 2) * R + r] = v0.z;
+      xt[(4 * i + 3) * R + r] = v0.w;
+      xt[(4 * i + 4) * R + r] = v1.x;
+      xt[(4 * i + 5) * R + r] = v1.y;
+      xt[(4 * i + 6) * R + r] = v1.z;
+      xt[(4 * i + 7) * R + r] = v1.w;
+    }
+    for (; i < n4; ++i) {
+      float4 v = x4[i];
+      xt[(4 * i + 0) * R + r] = v.x;
+      xt[(4 * i + 1) * R + r] = v.y;
+      xt[(4 * i + 2) * R + r] = v.z;
+      xt[(4 * i + 3) * R + r] = v.w;
+    }
+  } else {
+    for (int f = 0; f < a.F; ++f) xt[f * R + r] = xr[f];
+  }
+}
+
+__device__ __forceinline__ double sigmoid_d(double z) {
+  if (z >= 0.0) return 1.0 / (1.0 + exp(-z));
+  const double e = exp(z);
+  return e / (1.0 + e);
+}
+
+// Finish class values z[0..K) held in LDS (stride `stride` doubles) and store the row.
+__device__ void finalize_store(const LaunchArgs &a, double *z, int stride, int64_t row) {
+  const int K = a.K;
+  for (int k = 0; k < K; ++k) {
+    double v = z[k * stride];
+    if (a.aggregate == 1) v = (double)a.base[k] + v / (double)a.class_count[k];
+    z[k * stride] = v;
+  }
+  float *o = a.out + row * (int64_t)K;
+  if (a.transform == 1) {
+    o[0] = (float)sigmoid_d(z[0]);
+  } else if (a.transform == 2) {
+    double m = z[0];
+    for (int k = 1; k < K; ++k) m = z[k * stride] > m ? z[k * stride] : m;
+    double s = 0.0;
+    for (int k = 0; k < K; ++k) {
+      const double e = exp(z[k * stride] - m);
+      z[k * stride] = e;
+      s += e;
+    }
+    for (int k = 0; k < K; ++k) o[k] = (float)(z[k * stride] / s);
+  } else {
+    for (int k = 0; k < K; ++k) o[k] = (float)z[k * stride];
+  }
+}
+
+// Per-lane class bookkeeping for forests with several classes or several tree groups.
+struct ClassAcc {
+  double acc;
+  int k;       // class being accumulated
+  int next_b;  // first kernel tree of class k+1
+};
+
+__device__ __forceinline__ double class_init(const LaunchArgs &a, int k, bool first_group) {
+  return (a.aggregate == 0 && first_group) ? (double)a.base[k] : 0.0;
+}
+
+__device__ __forceinline__ void class_advance(const LaunchArgs &a, ClassAcc &c, int t,
+                                              double *acc_lds, int slot_stride, bool first_group) {
+  while (t >= c.next_b) {
+    acc_lds[c.k * slot_stride] = c.acc;
+    c.k += 1;
+    c.acc = class_init(a, c.k, first_group);
+    c.next_b = a.class_begin[c.k + 1];
+  }
+}
+
+__device__ __forceinline__ void class_flush_all(const LaunchArgs &a, ClassAcc &c,
+                                                double *acc_lds, int slot_stride,
+                                                bool first_group) {
+  while (c.k < a.K) {
+    acc_lds[c.k * slot_stride] = c.acc;
+    c.k += 1;
+    if (c.k < a.K) c.acc = class_init(a, c.k, first_group);
+  }
+}
+
+// ======================================================================= PERFECT
+// Trees are perfect of depth D, stored as breadth-first heaps (internal.h).  Each lane walks
+// four trees at once (independent dependency chains); per level and tree: one 64-bit LDS read
+// {threshold, feature}, one 32-bit LDS read of the feature value, a compare and a select.
+template <int D, bool LEAVES, bool SIMPLE>
+__global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, waves = blockDim.x >> 6;
+  const int R = a.rows_per_wg, G = a.groups;
+  const int r = tid & (R - 1);
+  const int g = tid / R;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const uint32_t tb = (uint32_t)a.tree_bytes;
+  const int T = a.n_trees, CT = a.trees_per_chunk;
+  const int shift = a.log2_row_bytes;
+  constexpr uint32_t kLeafOff = 4u << D;  // leaf slot 0 sits 4*2^D past the last-level record
+
+  {
+    const int t1 = CT < T ? CT : T;
+    stage_async(smem, 0, a.nodes, t1 * (int)tb, wave, lane, waves);
+  }
+  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  wait_stage();
+  __syncthreads();
+
+  double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
+  const int slot_stride = G * R;
+  ClassAcc ca;
+  ca.k = 0;
+  ca.acc = SIMPLE ? (a.aggregate == 0 ? (double)a.base[0] : 0.0) : class_init(a, 0, g == 0);
+  ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+
+  for (int c = 0; c < a.n_chunks; ++c) {
+    const int t0 = c * CT;
+    const int t1 = (t0 + CT < T) ? t0 + CT : T;
+    if (c + 1 < a.n_chunks) {
+      const int n0 = t1, n1 = (n0 + CT < T) ? n0 + CT : T;
+      stage_async(smem, ((c + 1) & 1) ? (uint32_t)a.chunk_bytes : 0u, a.nodes + (size_t)n0 * tb,
+                  (n1 - n0) * (int)tb, wave, lane, waves);
+    }
+    const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
+    for (int q = t0 + 4 * g; q < t1; q += 4 * G) {
+      const int nq = (t1 - q) < 4 ? (t1 - q) : 4;  // valid trees in this quad
+      uint32_t base[4], addr[4], kl[4], kr[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        base[u] = buf + (uint32_t)(q - t0 + u) * tb;
+        addr[u] = base[u];
+        // heap slot n at base + 8n; children at base + 8(2n+1) = 2*addr + (8 - base) and
+        // base + 8(2n+2) = 2*addr + (16 - base)
+        kl[u] = opaque(8u - base[u]);
+        kr[u] = opaque(16u - base[u]);
+      }
+      if (nq == 4) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+          uint2 rec[4];
+          float xv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) rec[u] = lds_u64(smem, addr[u]);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) xv[u] = lds_f32(smem, (rec[u].y << shift) + lane_off);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const bool left = xv[u] <= __uint_as_float(rec[u].x);
+            if (d < D - 1)
+              addr[u] = 2u * addr[u] + (left ? kl[u] : kr[u]);
+            else
+              addr[u] = addr[u] + (left ? 0u : 4u);
+          }
+        }
+      } else {
+        for (int u = 0; u < nq; ++u) {
+#pragma unroll
+          for (int d = 0; d < D; ++d) {
+            const uint2 rec = lds_u64(smem, addr[u]);
+            const float xv = lds_f32(smem, (rec.y << shift) + lane_off);
+            const bool left = xv <= __uint_as_float(rec.x);
+            if (d < D - 1)
+              addr[u] = 2u * addr[u] + (left ? kl[u] : kr[u]);
+            else
+              addr[u] = addr[u] + (left ? 0u : 4u);
+          }
+        }
+      }
+      if (LEAVES) {
+        for (int u = 0; u < nq; ++u) {
+          const int t = q + u;
+          const uint32_t slot = (addr[u] + kLeafOff - base[u] - 8u * ((1u << D) - 1u)) >> 2;
+          if (row_ok)
+            a.out_leaf[row * (int64_t)T + a.tree_order[t]] = a.leaf_map[(int64_t)t * (1 << D) + slot];
+        }
+      } else {
+        float lv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) lv[u] = (u < nq) ? lds_f32(smem, addr[u] + kLeafOff) : 0.0f;
+        for (int u = 0; u < nq; ++u) {
+          if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+          ca.acc += (double)lv[u];
+        }
+      }
+    }
+    wait_stage();
+    __syncthreads();
+  }
+  if (LEAVES) return;
+  if (SIMPLE) {
+    if (row_ok) {
+      double z = ca.acc;
+      if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
+      a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
+    }
+    return;
+  }
+  class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  __syncthreads();
+  if (g == 0) {
+    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
+    for (int k = 0; k < a.K; ++k) {
+      double s = z[k * slot_stride];
+      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
+      z[k * slot_stride] = s;
+    }
+    if (row_ok) finalize_store(a, z, slot_stride, row);
+  }
+}
+
+// ======================================================================== RAGGED
+// Any tree shape.  Each lane runs a state machine over its group's trees of the chunk: at an
+// internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
+// adds the value and jumps to the next tree's root.  Lanes never wait for each other inside
+// a chunk, so a short path in one tree is not padded to the wave's longest path.
+template <bool LEAVES, bool SIMPLE>
+__global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, waves = blockDim.x >> 6;
+  const int R = a.rows_per_wg, G = a.groups;
+  const int r = tid & (R - 1);
+  const int g = tid / R;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const int shift = a.log2_row_bytes;
+  const int T = a.n_trees;
+
+  stage_async(smem, 0, a.nodes + 8 * (size_t)a.chunk_rec[0],
+              8 * (a.chunk_rec[1] - a.chunk_rec[0]), wave, lane, waves);
+  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  wait_stage();
+  __syncthreads();
+
+  double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
+  const int slot_stride = G * R;
+  ClassAcc ca;
+  ca.k = 0;
+  ca.acc = class_init(a, 0, g == 0);
+  ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+
+  for (int c = 0; c < a.n_chunks; ++c) {
+    if (c + 1 < a.n_chunks)
+      stage_async(smem, ((c + 1) & 1) ? (uint32_t)a.chunk_bytes : 0u,
+                  a.nodes + 8 * (size_t)a.chunk_rec[c + 1],
+                  8 * (a.chunk_rec[c + 2] - a.chunk_rec[c + 1]), wave, lane, waves);
+    const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
+    const int ct0 = a.chunk_first[c], ct1 = a.chunk_first[c + 1];
+    const int nt = ct1 - ct0;
+    const int ga = ct0 + (int)(((int64_t)nt * g) / G);
+    const int gb = ct0 + (int)(((int64_t)nt * (g + 1)) / G);
+    const int rec0 = a.chunk_rec[c];
+    uint32_t addr = buf + 8u * (uint32_t)(a.tree_start[ga] - rec0);
+    const uint32_t end = buf + 8u * (uint32_t)(a.tree_start[gb] - rec0);
+    int t = ga;
+    while (addr < end) {
+      const uint2 rec = lds_u64(smem, addr);
+      const uint32_t meta = rec.y;
+      const float xv = lds_f32(smem, ((meta >> 16) << shift) + lane_off);
+      const bool leaf = (meta & (uint32_t)kLeafFlag) != 0;
+      const uint32_t rel = meta & (uint32_t)kMaxRel;
+      const bool right = !(xv <= __uint_as_float(rec.x)) && !leaf;
+      if (leaf) {
+        if (LEAVES) {
+          if (row_ok)
+            a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
+                a.leaf_map[rec0 + (int)((addr - buf) >> 3)];
+        } else {
+          if (!SIMPLE) class_advance(a, ca, t, acc_lds, slot_stride, g == 0);
+          ca.acc += (double)__uint_as_float(rec.x);
+        }
+        ++t;
+      }
+      // a valid record always moves forward (left_rel >= 1, next_rel >= 1); the max keeps the
+      // loop finite even on a corrupted record
+      const uint32_t step = rel + (right ? 1u : 0u);
+      addr += 8u * (step > 1u ? step : 1u);
+    }
+    wait_stage();
+    __syncthreads();
+  }
+  if (LEAVES) return;
+  if (SIMPLE && G == 1) {
+    if (row_ok) {
+      double z = ca.acc;
+      if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
+      a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
+    }
+    return;
+  }
+  if (SIMPLE) {
+    acc_lds[0] = ca.acc;
+  } else {
+    class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  }
+  __syncthreads();
+  if (g == 0) {
+    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
+    for (int k = 0; k < a.K; ++k) {
+      double s = z[k * slot_stride];
+      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
+      z[k * slot_stride] = s;
+    }
+    if (row_ok) finalize_store(a, z, slot_stride, row);
+  }
+}
+
+// ======================================================================== DIRECT
+// Fallback for any forest: one row per lane, nodes and features read from global memory.
+template <bool LEAVES>
+__global__ __launch_bounds__(256) void direct_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool row_ok = row < a.n_rows;
+  const int64_t rr = row_ok ? row : 0;
+  const float *xr = a.X + rr * (int64_t)a.F;
+  const int4 *recs = reinterpret_cast<const int4 *>(a.nodes);
+  const int T = a.n_trees;
+  double *acc_lds = reinterpret_cast<double *>(smem) + threadIdx.x;
+  const int slot_stride = blockDim.x;
+  ClassAcc ca;
+  ca.k = 0;
+  ca.acc = class_init(a, 0, true);
+  ca.next_b = a.class_begin[1];
+  for (int t = 0; t < T; ++t) {
+    int n = a.tree_start[t];
+    int4 rc = recs[n];
+    while (rc.y >= 0) {
+      const float xv = xr[rc.y];
+      n = (xv <= __int_as_float(rc.x)) ? rc.z : rc.w;
+      rc = recs[n];
+    }
+    if (LEAVES) {
+      if (row_ok) a.out_leaf[row * (int64_t)T + a.tree_order[t]] = a.leaf_map[n];
+    } else {
+      class_advance(a, ca, t, acc_lds, slot_stride, true);
+      ca.acc += (double)__int_as_float(rc.x);
+    }
+  }
+  if (LEAVES) return;
+  class_flush_all(a, ca, acc_lds, slot_stride, true);
+  if (row_ok) finalize_store(a, reinterpret_cast<double *>(smem) + threadIdx.x, slot_stride, row);
+}
+
+// ====================================================================== launchers
+// Raise a kernel's dynamic-LDS limit once per (kernel, device) to the largest size used.
+static int ensure_lds_limit(const void *kernel, int lds_bytes) {
+  static std::mutex mu;
+  static std::map<std::pair<const void *, int>, int> limits;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  int &cur = limits[{kernel, dev}];
+  if (lds_bytes <= cur) return 0;
+  hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+  if (e != hipSuccess) return (int)e;
+  cur = lds_bytes;
+  return 0;
+}
+
+template <class K>
+static int launch_common(K kernel, int threads, int64_t n_wg, int lds_bytes, void *stream,
+                         const LaunchArgs &a) {
+  const int e = ensure_lds_limit((const void *)kernel, lds_bytes);
+  if (e != 0) return e;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)n_wg), dim3(threads), lds_bytes,
+                     (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+template <int D>
+static int launch_perfect_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                            void *stream) {
+  const bool simple = a.K == 1 && a.groups == 1;
+  const int threads = 64 * waves;
+  if (a.out_leaf) return launch_common(perfect_kernel<D, true, false>, threads, n_wg, lds_bytes, stream, a);
+  if (simple) return launch_common(perfect_kernel<D, false, true>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(perfect_kernel<D, false, false>, threads, n_wg, lds_bytes, stream, a);
+}
+
+int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                   void *stream) {
+  switch (depth) {
+    case 1: return launch_perfect_d<1>(a, waves, n_wg, lds_bytes, stream);
+    case 2: return launch_perfect_d<2>(a, waves, n_wg, lds_bytes, stream);
+    case 3: return launch_perfect_d<3>(a, waves, n_wg, lds_bytes, stream);
+    case 4: return launch_perfect_d<4>(a, waves, n_wg, lds_bytes, stream);
+    case 5: return launch_perfect_d<5>(a, waves, n_wg, lds_bytes, stream);
+    case 6: return launch_perfect_d<6>(a, waves, n_wg, lds_bytes, stream);
+    case 7: return launch_perfect_d<7>(a, waves, n_wg, lds_bytes, stream);
+    case 8: return launch_perfect_d<8>(a, waves, n_wg, lds_bytes, stream);
+    case 9: return launch_perfect_d<9>(a, waves, n_wg, lds_bytes, stream);
+    case 10: return launch_perfect_d<10>(a, waves, n_wg, lds_bytes, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {
+  const bool simple = a.K == 1;
+  const int threads = 64 * waves;
+  if (a.out_leaf) return launch_common(ragged_kernel<true, false>, threads, n_wg, lds_bytes, stream, a);
+  if (simple) return launch_common(ragged_kernel<false, true>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_kernel<false, false>, threads, n_wg, lds_bytes, stream, a);
+}
+
+int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream) {
+  const int lds = a.out_leaf ? 0 : 256 * 8 * a.K;
+  if (a.out_leaf) return launch_common(direct_kernel<true>, 256, n_wg, lds, stream, a);
+  return launch_common(direct_kernel<false>, 256, n_wg, lds, stream, a);
+}
+
+}  // namespace bridger

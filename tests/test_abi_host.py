@@ -1,0 +1,277 @@
+"""Host-side checks that need no GPU: the library loads and exports every declared entry
+point; create validates forests; the packed layouts, walked by a test-only interpreter on
+the CPU, reproduce the oracle; the launch plan respects the LDS capacity."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2405_12491_amd as B
+from synth import (AGG_MEAN, XFORM_SIGMOID, XFORM_SOFTMAX, CONFIGS, concat_trees, make_workload,
+                   perfect_tree_arrays, permute_nodes, random_tiny_forest)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bridger.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bridger_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("bridger_forest_create", "bridger_forest_predict", "bridger_forest_predict_leaves",
+              "bridger_forest_destroy", "bridger_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(B.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def host(model, **kw):
+    return B.Forest(model, host_only=True, **kw)
+
+
+def _tiny():
+    return concat_trees([perfect_tree_arrays(2, np.array([0, 1, 1]), np.array([0.5, 0.25, 0.75], np.float32),
+                                             np.array([1, 2, 3, 4], np.float32))], 2)
+
+
+def _create_err(**changes):
+    f = _tiny()
+    args = dict(n_trees=f.n_trees, tree_offsets=f.tree_offsets, feature=f.feature, threshold=f.threshold,
+                left=f.left, right=f.right, value=f.value, n_features=2, n_classes=1, tree_class=None,
+                aggregate=0, transform=0, base_score=None, flags=B.BRIDGER_CREATE_HOST_ONLY)
+    args.update(changes)
+    with pytest.raises(B.BridgerError) as e:
+        B.bridger_forest_create(**args)
+    return e.value.status
+
+
+def test_validation_errors():
+    f = _tiny()
+    INV, ARG, UNS = B.BRIDGER_ERR_INVALID_FOREST, B.BRIDGER_ERR_INVALID_ARGUMENT, B.BRIDGER_ERR_UNSUPPORTED
+    l = f.left.copy(); l[1] = 0                                   # root as a child (cycle)
+    assert _create_err(left=l) == INV
+    l = f.left.copy(); l[2] = 9                                   # child out of range
+    assert _create_err(left=l) == INV
+    l = f.left.copy(); l[1] = -1                                  # exactly one child
+    assert _create_err(left=l) == INV
+    l = f.left.copy(); r = f.right.copy(); l[0] = 1; r[0] = 1     # identical children
+    assert _create_err(left=l, right=r) == INV
+    l = f.left.copy(); l[1] = 4                                   # node 4 has two parents, 3 unreachable
+    assert _create_err(left=l) == INV
+    ft = f.feature.copy(); ft[0] = 2                              # feature >= n_features
+    assert _create_err(feature=ft) == INV
+    ft = f.feature.copy(); ft[0] = -3
+    assert _create_err(feature=ft) == INV
+    th = f.threshold.copy(); th[1] = np.nan                       # NaN threshold
+    assert _create_err(threshold=th) == INV
+    assert _create_err(n_trees=0, tree_offsets=np.zeros(1, np.int64)) == ARG
+    assert _create_err(tree_offsets=np.array([1, 7], np.int64)) == INV
+    assert _create_err(n_features=0) == ARG
+    assert _create_err(n_classes=0) == ARG
+    assert _create_err(n_classes=65) == UNS
+    assert _create_err(transform=XFORM_SIGMOID, n_classes=2) == ARG
+    assert _create_err(transform=XFORM_SOFTMAX) == ARG
+    assert _create_err(tree_class=np.array([3], np.int32), n_classes=2) == ARG
+    assert _create_err(aggregate=AGG_MEAN, n_classes=2, tree_class=np.array([1], np.int32)) == ARG
+    assert _create_err(aggregate=7) == ARG
+    assert _create_err(flags=8) == ARG
+
+
+def test_null_pointer_arguments():
+    lib = B.load_library()
+    h = ctypes.c_void_p()
+    st = lib.bridger_forest_create_ex(1, None, None, None, None, None, None, 2, 1, None, 0, 0, None,
+                                      1, ctypes.byref(h))
+    assert st == B.BRIDGER_ERR_INVALID_ARGUMENT and not h.value
+    assert lib.bridger_forest_predict(None, None, 1, 2, None, None) == B.BRIDGER_ERR_INVALID_ARGUMENT
+    assert "null" in B.bridger_last_error()
+    lib.bridger_forest_destroy(None)
+
+
+def test_deep_tree_rejected():
+    # a chain of depth 65
+    n = 131
+    left = np.full(n, -1, np.int32); right = np.full(n, -1, np.int32)
+    for d in range(65):
+        left[2 * d] = 2 * d + 1 if 2 * d + 1 < n else -1
+        right[2 * d] = 2 * d + 2
+    f = concat_trees([(np.zeros(n, np.int32), np.zeros(n, np.float32), left, right, np.zeros(n, np.float32))], 1)
+    with pytest.raises(B.BridgerError) as e:
+        host(f)
+    assert e.value.status == B.BRIDGER_ERR_INVALID_FOREST
+
+
+def test_predict_on_host_only_handle_fails():
+    with host(_tiny()) as f:
+        with pytest.raises(B.BridgerError) as e:
+            B.bridger_forest_predict(f.handle, 16, 1, 2, 64, 0)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
+
+
+# ----------------------------------------------------- packed-layout interpreter
+def walk_perfect(f: B.Forest, model, X):
+    blob = B.bridger_forest_packed(f.handle, 0, np.uint8)
+    leaf_map = B.bridger_forest_packed(f.handle, 2, np.int32)
+    order = B.bridger_forest_packed(f.handle, 3, np.int32)
+    D = f.info()["max_depth"]
+    T = f.n_trees
+    tb = blob.size // T
+    n_int = (1 << D) - 1
+    leaves = np.empty((X.shape[0], T), np.int32)
+    vals = np.empty((X.shape[0], T), np.float32)
+    for k in range(T):
+        blk = blob[k * tb:(k + 1) * tb]
+        thr = blk[:8 * n_int].view(np.float32)[0::2]
+        feat = blk[:8 * n_int].view(np.uint32)[1::2]
+        lv = blk[8 * n_int:8 * n_int + 4 * (n_int + 1)].view(np.float32)
+        n = np.zeros(X.shape[0], np.int64)
+        for _ in range(D):
+            go_left = X[np.arange(X.shape[0]), feat[n]] <= thr[n]
+            n = 2 * n + np.where(go_left, 1, 2)
+        j = n - n_int
+        leaves[:, order[k]] = leaf_map[k * (n_int + 1) + j]
+        vals[:, order[k]] = lv[j]
+    return leaves, vals
+
+
+def walk_ragged(f: B.Forest, X):
+    rec = B.bridger_forest_packed(f.handle, 0, np.uint32).reshape(-1, 2)
+    start = B.bridger_forest_packed(f.handle, 1, np.int32)
+    rec_node = B.bridger_forest_packed(f.handle, 2, np.int32)
+    order = B.bridger_forest_packed(f.handle, 3, np.int32)
+    T = f.n_trees
+    leaves = np.empty((X.shape[0], T), np.int32)
+    vals = np.empty((X.shape[0], T), np.float32)
+    rows = np.arange(X.shape[0])
+    for k in range(T):
+        a = np.full(X.shape[0], start[k], np.int64)
+        for _ in range(70):
+            meta = rec[a, 1]
+            leaf = (meta & 0x8000) != 0
+            if leaf.all():
+                break
+            feat = (meta >> 16).astype(np.int64)
+            right = ~(X[rows, feat] <= rec[a, 0].view(np.float32)) & ~leaf
+            a = np.where(leaf, a, a + (meta & 0x7FFF) + right)
+        assert np.all((rec[a, 1] & 0x8000) != 0)
+        nxt = a + (rec[a, 1] & 0x7FFF)
+        assert np.all(nxt == start[k + 1])                     # a leaf points at the next root
+        leaves[:, order[k]] = rec_node[a]
+        vals[:, order[k]] = rec[a, 0].view(np.float32)
+    return leaves, vals
+
+
+def walk_direct(f: B.Forest, X):
+    rec = B.bridger_forest_packed(f.handle, 0, np.int32).reshape(-1, 4)
+    root = B.bridger_forest_packed(f.handle, 1, np.int32)
+    rec_node = B.bridger_forest_packed(f.handle, 2, np.int32)
+    order = B.bridger_forest_packed(f.handle, 3, np.int32)
+    T = f.n_trees
+    leaves = np.empty((X.shape[0], T), np.int32)
+    rows = np.arange(X.shape[0])
+    for k in range(T):
+        n = np.full(X.shape[0], root[k], np.int64)
+        while True:
+            feat = rec[n, 1]
+            act = feat >= 0
+            if not act.any():
+                break
+            go_left = X[rows, np.maximum(feat, 0)] <= rec[n, 0].view(np.float32)
+            n = np.where(act, np.where(go_left, rec[n, 2], rec[n, 3]), n)
+        leaves[:, order[k]] = rec_node[n]
+    return leaves
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_packed_layouts_reproduce_oracle_leaves(name):
+    w = make_workload(name, 200 if name != "ragged_d12" else 40)
+    X = w.X()
+    _, ref_lv, _ = oracle.predict(w.forest, X, want_leaves=True, threads=8)
+    with host(w.forest) as f:
+        for k in (B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT):
+            try:
+                f.kernel = k
+            except B.BridgerError:
+                continue
+            if k == B.BRIDGER_KERNEL_PERFECT:
+                lv, _ = walk_perfect(f, w.forest, X)
+            elif k == B.BRIDGER_KERNEL_RAGGED:
+                lv, _ = walk_ragged(f, X)
+            else:
+                lv = walk_direct(f, X)
+            assert np.array_equal(lv, ref_lv), (name, k)
+
+
+def test_packed_layouts_permuted_and_classes():
+    rng = np.random.default_rng(5)
+    trees = [perfect_tree_arrays(3, rng.integers(0, 5, 7), rng.standard_normal(7).astype(np.float32),
+                                 rng.standard_normal(8).astype(np.float32)) for _ in range(11)]
+    model = permute_nodes(concat_trees(trees, 5, 3, rng.integers(0, 3, 11)), rng)
+    X = rng.standard_normal((300, 5)).astype(np.float32)
+    _, ref_lv, _ = oracle.predict(model, X, want_leaves=True)
+    with host(model) as f:
+        order = B.bridger_forest_packed(f.handle, 3, np.int32)
+        tc = model.tree_class[order]
+        assert np.all(np.diff(tc) >= 0)                            # class-major
+        for c in range(3):                                         # stable within a class
+            assert np.all(np.diff(order[tc == c]) > 0)
+        lv, _ = walk_perfect(f, model, X)
+        assert np.array_equal(lv, ref_lv)
+        f.kernel = B.BRIDGER_KERNEL_RAGGED
+        lv, _ = walk_ragged(f, X)
+        assert np.array_equal(lv, ref_lv)
+    rf = random_tiny_forest(rng, 17, 4, max_depth=8)
+    X = rng.standard_normal((300, 4)).astype(np.float32)
+    _, ref_lv, _ = oracle.predict(rf, X, want_leaves=True)
+    with host(rf) as f:
+        assert f.kernel == B.BRIDGER_KERNEL_RAGGED
+        lv, _ = walk_ragged(f, X)
+        assert np.array_equal(lv, ref_lv)
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_plan_respects_lds_capacity(name):
+    w = make_workload(name, 1000)
+    with host(w.forest) as f:
+        for k in (B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED):
+            try:
+                f.kernel = k
+            except B.BridgerError:
+                continue
+            p = f.plan(w.n_rows)
+            R = p["rows_per_wg"]
+            assert R >= 32 and R & (R - 1) == 0
+            assert p["lds_bytes"] <= 160 * 1024
+            assert 2 * p["chunk_bytes"] + R * w.n_features * 4 <= p["lds_bytes"]
+            if k == B.BRIDGER_KERNEL_PERFECT:
+                tb = B.bridger_forest_packed(f.handle, 0, np.uint8).size // f.n_trees
+                assert p["trees_per_chunk"] * tb <= p["chunk_bytes"]
+                assert p["n_chunks"] * p["trees_per_chunk"] >= f.n_trees
+            else:
+                chunks = B.bridger_forest_packed(f.handle, 4, np.int32)
+                start = B.bridger_forest_packed(f.handle, 1, np.int32)
+                assert chunks[0] == 0 and chunks[-1] == f.n_trees
+                assert len(chunks) - 1 == p["n_chunks"]
+                for a, b in zip(chunks[:-1], chunks[1:]):
+                    assert 8 * (start[b] - start[a]) <= p["chunk_bytes"]
+                    assert start[a] % 2 == 0                    # 16-byte aligned chunk start
+
+
+def test_create_without_gpu_reports_device_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(B.BridgerError) as e:
+        B.Forest(_tiny())
+    assert e.value.status == B.BRIDGER_ERR_DEVICE

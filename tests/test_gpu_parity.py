@@ -1,0 +1,294 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Leaf ids must match bit for bit; scores within 1e-6 + 1e-5 * |oracle|.  Every kernel family
+that can run a forest is checked on it.  Sizes span several row tiles plus a ragged tail.
+"""
+import numpy as np
+import pytest
+
+import paper_2405_12491_amd as B
+from parity_util import (assert_leaves, assert_scores, check_parity, gpu_predict, oracle_predict,
+                         to_dev)
+from synth import (AGG_MEAN, AGG_SUM, CONFIGS, XFORM_IDENTITY, XFORM_SIGMOID, XFORM_SOFTMAX,
+                   concat_trees, make_workload, perfect_tree_arrays, permute_nodes,
+                   random_tiny_forest)
+
+pytestmark = pytest.mark.gpu
+
+KERNELS = [B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT]
+
+# rows per workload for the oracle-sized cases: several tiles of the largest row tile (1024)
+# plus a tail that is not a multiple of 32
+SMALL_ROWS = {"dt_d3": 10_000, "rf_d8": 3 * 1024 + 77, "gbdt_d6": 3 * 1024 + 77,
+              "mc_gbdt_d8": 2 * 32 * 3 + 45, "ragged_d12": 3 * 64 + 29}
+
+
+def supported(f: B.Forest, k: int) -> bool:
+    try:
+        f.kernel = k
+        return True
+    except B.BridgerError as e:
+        assert e.status == B.BRIDGER_ERR_UNSUPPORTED
+        return False
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+    yield
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_workload_small(name):
+    w = make_workload(name, SMALL_ROWS[name])
+    X = w.X()
+    Xd = to_dev(X)
+    ran = 0
+    with B.Forest(w.forest) as f:
+        for k in KERNELS:
+            if not supported(f, k):
+                continue
+            print(f"[parity] {name} rows={X.shape[0]} kernel={B.KERNEL_NAMES[k]}", flush=True)
+            check_parity(w.forest, X, k, f"{name}/{B.KERNEL_NAMES[k]}", Xd=Xd, forest=f)
+            ran += 1
+    assert ran >= 2
+
+
+def test_direct_sums_bit_identical():
+    """One row per lane, trees in ascending order: the double-precision sum is the oracle's."""
+    for name in ("dt_d3", "rf_d8", "ragged_d12"):
+        w = make_workload(name, 500)
+        X = w.X()
+        check_parity(w.forest, X, B.BRIDGER_KERNEL_DIRECT, name + "/direct", exact_sum=True)
+
+
+def test_perfect_single_group_sums_bit_identical():
+    w = make_workload("rf_d8", 2048 + 5)
+    X = w.X()
+    check_parity(w.forest, X, B.BRIDGER_KERNEL_PERFECT, "rf_d8/perfect", exact_sum=True)
+
+
+@pytest.mark.parametrize("n", [1, 2, 31, 32, 33, 63, 64, 65, 255, 257, 1023, 1025])
+def test_row_counts(n):
+    w = make_workload("gbdt_d6", n)
+    X = w.X()
+    with B.Forest(w.forest) as f:
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(w.forest, X, k, f"gbdt_d6 n={n} {B.KERNEL_NAMES[k]}", forest=f)
+
+
+def test_zero_rows_launches_nothing():
+    import torch
+    w = make_workload("gbdt_d6", 4)
+    with B.Forest(w.forest) as f:
+        X = torch.zeros((0, 28), device="cuda")
+        out = torch.full((0, 1), 7.0, device="cuda")
+        f.predict(X, out)
+        torch.cuda.synchronize()
+
+
+def _adversarial_rows(F, thr_values, rng, n=600):
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    specials = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 1.17549435e-38],
+                        np.float32)
+    m = rng.random(X.shape) < 0.15
+    X[m] = specials[rng.integers(0, len(specials), m.sum())]
+    t = np.asarray(thr_values, np.float32)
+    m = rng.random(X.shape) < 0.25
+    pick = t[rng.integers(0, len(t), m.sum())]
+    nudge = rng.integers(-1, 2, m.sum())
+    vals = np.where(nudge == 0, pick, np.where(nudge > 0, np.nextafter(pick, np.float32(np.inf)),
+                                               np.nextafter(pick, np.float32(-np.inf))))
+    X[m] = vals.astype(np.float32)
+    return X
+
+
+@pytest.mark.parametrize("F", [3, 7, 28])
+def test_adversarial_values(F):
+    """NaN, +-inf, +-0, denormals, values on a threshold and one ulp either side."""
+    rng = np.random.default_rng(100 + F)
+    grid = np.array([-1.0, -1e-45, 0.0, 1e-45, 0.5, 2.0], np.float32)
+    trees = []
+    for D in (2, 3, 4, 5):
+        for _ in range(3):
+            n_int = (1 << D) - 1
+            trees.append(perfect_tree_arrays(D, rng.integers(0, F, n_int), grid[rng.integers(0, 6, n_int)],
+                                             rng.standard_normal(1 << D).astype(np.float32)))
+    ragged = concat_trees(trees, F)
+    perfect = concat_trees([perfect_tree_arrays(4, rng.integers(0, F, 15), grid[rng.integers(0, 6, 15)],
+                                                rng.standard_normal(16).astype(np.float32))
+                            for _ in range(9)], F)
+    X = _adversarial_rows(F, grid, rng)
+    for model in (ragged, perfect):
+        with B.Forest(model) as f:
+            for k in KERNELS:
+                if supported(f, k):
+                    check_parity(model, X, k, f"adversarial F={F} {B.KERNEL_NAMES[k]}", forest=f)
+
+
+def test_unaligned_rows():
+    """X starting 4 bytes past a 16-byte boundary takes the scalar row-load path."""
+    import torch
+    w = make_workload("gbdt_d6", 700)
+    X = w.X()
+    big = torch.zeros(X.size + 1, dtype=torch.float32, device="cuda")
+    big[1:] = torch.from_numpy(X.reshape(-1)).cuda()
+    Xd = big[1:].view(X.shape)
+    assert Xd.data_ptr() % 16 == 4
+    with B.Forest(w.forest) as f:
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(w.forest, X, k, f"unaligned {B.KERNEL_NAMES[k]}", Xd=Xd, forest=f)
+
+
+def test_permuted_numbering_and_leaf_map():
+    """Caller node ids in random order: leaf ids come back in the caller's numbering."""
+    rng = np.random.default_rng(7)
+    w = make_workload("rf_d8", 900)
+    model = permute_nodes(w.forest, rng)
+    X = w.X()
+    with B.Forest(model) as f:
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(model, X, k, f"permuted {B.KERNEL_NAMES[k]}", forest=f)
+
+
+@pytest.mark.parametrize("n_trees", [1, 2, 3, 5, 33])
+def test_tree_counts_and_shapes(n_trees):
+    rng = np.random.default_rng(n_trees)
+    model = random_tiny_forest(rng, n_trees, 9, max_depth=9, p_split=0.75)
+    X = rng.standard_normal((333, 9)).astype(np.float32)
+    with B.Forest(model) as f:
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(model, X, k, f"T={n_trees} {B.KERNEL_NAMES[k]}", forest=f)
+    # perfect trees too
+    trees = [perfect_tree_arrays(3, rng.integers(0, 9, 7), rng.standard_normal(7).astype(np.float32),
+                                 rng.standard_normal(8).astype(np.float32)) for _ in range(n_trees)]
+    model = concat_trees(trees, 9)
+    with B.Forest(model) as f:
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(model, X, k, f"perfect T={n_trees} {B.KERNEL_NAMES[k]}", forest=f)
+
+
+def test_depth_zero_trees():
+    rng = np.random.default_rng(3)
+    stump = perfect_tree_arrays(1, np.array([2]), np.array([0.0], np.float32), np.array([-1.0, 1.0], np.float32))
+    leaf = (np.array([-1], np.int32), np.zeros(1, np.float32), np.array([-1], np.int32),
+            np.array([-1], np.int32), np.array([2.5], np.float32))
+    model = concat_trees([leaf, stump, leaf, leaf, stump], 4)
+    X = rng.standard_normal((200, 4)).astype(np.float32)
+    with B.Forest(model) as f:
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(model, X, k, f"depth0 {B.KERNEL_NAMES[k]}", forest=f)
+
+
+@pytest.mark.parametrize("agg,xform,K", [(AGG_SUM, XFORM_SOFTMAX, 3), (AGG_MEAN, XFORM_IDENTITY, 4),
+                                         (AGG_MEAN, XFORM_SOFTMAX, 5), (AGG_SUM, XFORM_SIGMOID, 1),
+                                         (AGG_MEAN, XFORM_SIGMOID, 1)])
+def test_classes_aggregates_transforms(agg, xform, K):
+    rng = np.random.default_rng(K * 10 + agg)
+    T = 23
+    trees = [perfect_tree_arrays(4, rng.integers(0, 6, 15), rng.standard_normal(15).astype(np.float32),
+                                 rng.standard_normal(16).astype(np.float32)) for _ in range(T)]
+    tc = rng.integers(0, K, T)
+    tc[:K] = np.arange(K)  # every class has a tree
+    base = rng.standard_normal(K).astype(np.float32)
+    X = rng.standard_normal((1100, 6)).astype(np.float32)
+    for model in (concat_trees(trees, 6, K, tc, agg, xform, base),
+                  permute_nodes(concat_trees(trees, 6, K, None, agg, xform, base), rng)):
+        with B.Forest(model) as f:
+            for k in KERNELS:
+                if supported(f, k):
+                    check_parity(model, X, k, f"K={K} agg={agg} x={xform} {B.KERNEL_NAMES[k]}", forest=f)
+
+
+def test_determinism_and_streams():
+    import torch
+    w = make_workload("gbdt_d6", 5000)
+    Xd = to_dev(w.X())
+    with B.Forest(w.forest) as f:
+        a = gpu_predict(f, Xd)
+        b = gpu_predict(f, Xd)
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            out = f.predict(Xd)
+        s.synchronize()
+        c = out.cpu().numpy()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert np.array_equal(a.view(np.uint32), c.view(np.uint32))
+
+
+def test_argument_errors():
+    import torch
+    w = make_workload("gbdt_d6", 64)
+    Xd = to_dev(w.X())
+    with B.Forest(w.forest) as f:
+        out = torch.empty((64, 1), device="cuda")
+        with pytest.raises(B.BridgerError) as e:
+            B.bridger_forest_predict(f.handle, Xd.data_ptr(), 64, 27, out.data_ptr(), 0)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
+        with pytest.raises(B.BridgerError) as e:
+            B.bridger_forest_predict(f.handle, Xd.data_ptr(), 64, 28, Xd.data_ptr() + 64, 0)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
+        with pytest.raises(B.BridgerError) as e:
+            B.bridger_forest_predict(f.handle, Xd.data_ptr(), -1, 28, out.data_ptr(), 0)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
+
+
+# ------------------------------------------------------------- full-size workloads
+def _full_X_device(w):
+    """The full feature matrix on the device, built block by block."""
+    import torch
+    from synth import BLOCK_ROWS, x_rows
+    Xd = torch.empty((w.n_rows, w.n_features), dtype=torch.float32, device="cuda")
+    step = BLOCK_ROWS * 4
+    for r in range(0, w.n_rows, step):
+        blk = x_rows(w.seed, w.x_kind, w.n_features, r, min(r + step, w.n_rows), **w.x_params)
+        Xd[r:r + blk.shape[0]].copy_(torch.from_numpy(blk))
+    return Xd
+
+
+def _sample_rows(n, R, rng, k=1500):
+    idx = set(range(min(n, R + 3)))                 # the first tile and a bit
+    idx |= set(range(max(0, n - R - 3), n))          # the last (ragged) tile
+    idx |= set(rng.integers(0, n, k).tolist())
+    return np.array(sorted(idx))
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_workload_full_size_sampled(name):
+    """Full-size inputs in the benchmark's launch configuration; sampled rows against the
+    oracle, plus leaf ids on windows at the start, middle and end."""
+    import torch
+    from synth import x_rows
+    w = make_workload(name)
+    print(f"[full] {name}: building X {w.n_rows}x{w.n_features}", flush=True)
+    Xd = _full_X_device(w)
+    rng = np.random.default_rng(1234)
+    with B.Forest(w.forest) as f:
+        plan = f.plan(w.n_rows)
+        print(f"[full] {name}: kernel={B.KERNEL_NAMES[f.kernel]} plan={plan}", flush=True)
+        out = f.predict(Xd)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        idx = _sample_rows(w.n_rows, plan["rows_per_wg"] or 256, rng)
+        Xs = np.concatenate([x_rows(w.seed, w.x_kind, w.n_features, int(i), int(i) + 1, **w.x_params)
+                             for i in idx])
+        ref, _ = oracle_predict(w.forest, Xs)
+        assert_scores(got[idx], ref, f"{name} full-size sampled scores")
+        assert np.all(np.isfinite(got))
+        win = 256 if w.forest.n_trees * w.n_features < 300_000 else 64
+        for a in (0, w.n_rows // 2 + 13, w.n_rows - win):
+            lv = gpu_predict(f, Xd[a:a + win], leaves=True)
+            _, ref_lv = oracle_predict(w.forest, x_rows(w.seed, w.x_kind, w.n_features, a, a + win, **w.x_params),
+                                       leaves=True)
+            assert_leaves(lv, ref_lv, f"{name} full-size leaves @{a}")
+    del Xd
+    torch.cuda.empty_cache()
