@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark: batched tree-ensemble prediction on one MI355X.
+
+A step is one fused prediction over the whole batch: feature gather, threshold compare,
+child select, leaf reduce and the final transform for every (row, tree), i.e. one
+bridger_forest_predict launch.  The default workload is the binary GBDT of 500 perfect
+depth-6 trees over 1,000,000 rows x 28 fp32 features (sigmoid output).  Inputs are
+synthetic and seeded, resident in HBM before the timed region starts.
+
+Prints one JSON line.  ``roofline`` rates the dominant (only) kernel against the bound
+that binds it: every internal-node visit needs two data-dependent per-lane gathers from LDS
+(the node's {threshold, feature} and the row's feature value), and an MI355X CU's LDS
+serves 32 lanes per clock, so peak visits/s = 256 CUs * 2.4 GHz * 32 / 2.  HBM bandwidth is
+reported too (algorithmic bytes: X once, the output once, the forest once).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+N_CU, CLOCK_HZ, LDS_LANES_PER_CLK = 256, 2.4e9, 32
+GATHERS_PER_VISIT = 2
+PEAK_VISITS_PER_S = N_CU * CLOCK_HZ * LDS_LANES_PER_CLK / GATHERS_PER_VISIT
+HBM_PEAK_BYTES_PER_S = 8.0e12
+
+# HBM bytes per launch of the default workload's kernel from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE runs (KiB per dispatch), each scaled by what the same counter reads for a plain
+# copy of known size (profiles/perfect_kernel_gbdt_d6_1Mx28_500trees.md).  Valid only for the
+# kernel source they were measured on; any other source reports traffic as null.
+MEASURED_TRAFFIC = {
+    "kernel_sha256_prefix": "74a4eb672ce875d2",
+    "workload": "gbdt_d6",
+    "fetch_kib": 57307.5, "write_kib": 3906.25,
+    "copy_bytes": 112_000_000, "copy_fetch_kib": 54701.9375, "copy_write_kib": 109375.0,
+}
+
+
+def measured_traffic(workload: str, n_rows: int):
+    import hashlib
+    src = os.path.join(ROOT, "paper_2405_12491_amd", "csrc", "kernels.hip")
+    m = MEASURED_TRAFFIC
+    if workload != m["workload"] or n_rows != 1_000_000:
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != m["kernel_sha256_prefix"]:
+        return None
+    true_kib = m["copy_bytes"] / 1024.0
+    fetch = m["fetch_kib"] * (true_kib / m["copy_fetch_kib"]) * 1024.0
+    write = m["write_kib"] * (true_kib / m["copy_write_kib"]) * 1024.0
+    return fetch + write
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="gbdt_d6")
+    p.add_argument("--rows", type=int, default=None, help="override the workload's row count")
+    p.add_argument("--kernel", default="auto", choices=["auto", "perfect", "ragged", "direct"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-rows", type=int, default=200_000)
+    p.add_argument("--calib-copy", action="store_true",
+                   help="time a plain device copy of X instead (counter calibration)")
+    return p.parse_args()
+
+
+def build_x(w, device):
+    import torch
+    from synth import BLOCK_ROWS, x_rows
+    Xd = torch.empty((w.n_rows, w.n_features), dtype=torch.float32, device=device)
+    step = BLOCK_ROWS * 4
+    for r in range(0, w.n_rows, step):
+        blk = x_rows(w.seed, w.x_kind, w.n_features, r, min(r + step, w.n_rows), **w.x_params)
+        Xd[r:r + blk.shape[0]].copy_(torch.from_numpy(blk))
+    return Xd
+
+
+def node_depths(f):
+    """Depth of every node (root = 0), per tree, from the child arrays."""
+    depth = np.zeros(f.n_nodes, np.int64)
+    for t in range(f.n_trees):
+        a, b = int(f.tree_offsets[t]), int(f.tree_offsets[t + 1])
+        l, r = f.left[a:b], f.right[a:b]
+        d = depth[a:b]
+        stack = [0]
+        while stack:
+            i = stack.pop()
+            if l[i] >= 0:
+                d[l[i]] = d[r[i]] = d[i] + 1
+                stack += [int(l[i]), int(r[i])]
+    return depth
+
+
+def cpu_baseline(w, out_dev, sample_rows):
+    """The CPU oracle timed on the host's cores over the first `sample_rows` rows; its
+    outputs are also compared with the GPU's for those rows."""
+    import oracle
+    from synth import x_rows
+    n = min(sample_rows, w.n_rows)
+    X = x_rows(w.seed, w.x_kind, w.n_features, 0, n, **w.x_params)
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    t0 = time.perf_counter()
+    ref, _, visits = oracle.predict(w.forest, X, threads=threads)
+    dt = time.perf_counter() - t0
+    got = out_dev[:n].cpu().numpy().astype(np.float64)
+    ok = bool(np.all(np.abs(got - ref) <= 1e-6 + 1e-5 * np.abs(ref)))
+    return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n:,} rows of the {w.n_rows:,}-row workload ({visits:,} node visits), "
+                      f"{dt:.2f} s wall on {threads} threads",
+            "visits_per_s": visits / dt, "agrees_with_gpu": ok}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}); "
+              "the forest is replicated and rows are independent, so N GPUs would each run this "
+              "same kernel on n/N rows. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2405_12491_amd as B
+    from synth import make_workload
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = make_workload(args.workload, args.rows)
+    Xd = build_x(w, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    if args.calib_copy:
+        dst = torch.empty_like(Xd)
+        for _ in range(args.warmup):
+            dst.copy_(Xd)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            dst.copy_(Xd)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        nbytes = Xd.numel() * 4
+        print(json.dumps({"calib_copy_bytes_read": nbytes, "calib_copy_bytes_written": nbytes,
+                          "ms_per_copy": ms, "GBps": 2 * nbytes / ms / 1e6}))
+        return
+
+    forest = B.Forest(w.forest)
+    if args.kernel != "auto":
+        forest.kernel = {"perfect": 1, "ragged": 2, "direct": 3}[args.kernel]
+    out = torch.empty((w.n_rows, w.forest.n_classes), dtype=torch.float32, device=dev)
+    plan = forest.plan(w.n_rows)
+    for _ in range(args.warmup):
+        forest.predict(Xd, out)
+    torch.cuda.synchronize()
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        forest.predict(Xd, out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1) / args.steps
+
+    f = w.forest
+    n = w.n_rows
+    # visits per row: exact for perfect trees; otherwise the depth of the leaf each row
+    # reaches, summed over trees (leaf ids from the GPU on a 4096-row sample)
+    info = B.bridger_forest_info(forest.handle)
+    if info["all_perfect"]:
+        visits_per_row = float(f.n_trees * info["max_depth"])
+    else:
+        m = min(4096, n)
+        lv = forest.predict_leaves(Xd[:m]).cpu().numpy()
+        depth = node_depths(f)
+        offs = f.tree_offsets[:-1].astype(np.int64)
+        visits_per_row = float(depth[lv.astype(np.int64) + offs[None, :]].sum()) / m
+    visits = visits_per_row * n
+    forest_bytes = B.bridger_forest_packed(forest.handle, 0, np.uint8).size
+    alg_bytes = n * w.n_features * 4 + n * f.n_classes * 4 + forest_bytes
+    s = ms / 1e3
+    visits_per_s = visits / s
+    line = {
+        "metric": "rows/sec and achieved HBM GB/s fraction, tree-ensemble predict (1 MI355X)",
+        "value": n / s,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded; stands in for the paper's tabular regression set)",
+        "config": {
+            "workload": f"{w.name}: {w.description}",
+            "n_rows": n, "n_features": w.n_features, "n_trees": f.n_trees,
+            "n_classes": f.n_classes,
+            "kernel": B.KERNEL_NAMES[forest.kernel],
+            "plan": {k: v for k, v in plan.items() if not isinstance(v, float)},
+        },
+        "roofline": {
+            "bound": "lds",
+            "achieved": visits_per_s / 1e9,
+            "peak": PEAK_VISITS_PER_S / 1e9,
+            "unit": "Gvisit/s",
+            "frac": visits_per_s / PEAK_VISITS_PER_S,
+            "traffic": measured_traffic(w.name, n),
+            "what": "internal-node visits per second against the on-chip gather bound: each "
+                    "visit needs 2 data-dependent per-lane LDS gathers (node, feature value); a "
+                    "CU's 32-bank LDS serves 32 lanes/clk; 256 CUs x 2.4 GHz. HBM is not the "
+                    "binding level (see hbm).",
+        },
+        "node_visits_per_s": visits_per_s,
+        "visits_per_row": visits_per_row,
+        "hbm": {"algorithmic_bytes": alg_bytes, "achieved_GBps": alg_bytes / s / 1e9,
+                "peak_GBps": HBM_PEAK_BYTES_PER_S / 1e9,
+                "frac": alg_bytes / s / HBM_PEAK_BYTES_PER_S},
+        "wall_s_timed_region": t_wall,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, out, args.cpu_sample_rows)
+    print(json.dumps(line), flush=True)
+    forest.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -11,11 +11,13 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <deque>
 #include <new>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "bridger.h"
@@ -42,7 +44,6 @@ constexpr double kL2BytesPerSec = 30.0e12;
 constexpr double kLdsInstrPerSec = 0.44 * 256 * 2.4e9;
 constexpr int kMaxWavesPerCU = 32;
 constexpr int kMinWavesPerCU = 8;
-constexpr int kPerfectTreesMultiple = 4;  // trees are traversed four at a time per lane
 
 int env_int(const char *name, int dflt) {
   const char *v = std::getenv(name);
@@ -193,34 +194,34 @@ void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *
                   const float *thr, const int32_t *left, const int32_t *right,
                   const float *value) {
   const int n_int = (1 << D) - 1, n_leaf = 1 << D;
-  int tb = 8 * n_int + 4 * n_leaf;
-  tb = (tb + 15) & ~15;
+  const int leaf_off = 8 * (n_int + 1);   // 1-based heap: slots 1 .. 2^D - 1, slot 0 unused
+  const int tb = (leaf_off + 4 * n_leaf + 15) & ~15;
   h->perfect_tree_bytes = tb;
   h->perfect_blob.assign((size_t)tb * h->n_trees, 0);
   h->perfect_leaf_map.assign((size_t)n_leaf * h->n_trees, -1);
-  std::vector<int32_t> heap_to_node((size_t)2 * n_leaf - 1);
+  std::vector<int32_t> heap_to_node((size_t)2 * n_leaf);
   for (int32_t k = 0; k < h->n_trees; ++k) {
     const int32_t t = h->tree_order[k];
     const int64_t a = offs[t];
-    // heap slot -> caller node
-    heap_to_node[0] = 0;
-    for (int s = 0; s < n_int; ++s) {
-      const int32_t nd = heap_to_node[s];
-      heap_to_node[2 * s + 1] = left[a + nd];
-      heap_to_node[2 * s + 2] = right[a + nd];
+    // 1-based heap slot -> caller node
+    heap_to_node[1] = 0;
+    for (int m = 1; m <= n_int; ++m) {
+      const int32_t nd = heap_to_node[m];
+      heap_to_node[2 * m] = left[a + nd];
+      heap_to_node[2 * m + 1] = right[a + nd];
     }
     uint8_t *blk = h->perfect_blob.data() + (size_t)k * tb;
-    for (int s = 0; s < n_int; ++s) {
-      const int32_t nd = heap_to_node[s];
+    for (int m = 1; m <= n_int; ++m) {
+      const int32_t nd = heap_to_node[m];
       const float th = thr[a + nd];
       const uint32_t f = (uint32_t)feat[a + nd];
-      std::memcpy(blk + 8 * s, &th, 4);
-      std::memcpy(blk + 8 * s + 4, &f, 4);
+      std::memcpy(blk + 8 * m, &th, 4);
+      std::memcpy(blk + 8 * m + 4, &f, 4);
     }
     for (int j = 0; j < n_leaf; ++j) {
-      const int32_t nd = heap_to_node[n_int + j];
+      const int32_t nd = heap_to_node[n_leaf + j];
       const float v = value[a + nd];
-      std::memcpy(blk + 8 * n_int + 4 * j, &v, 4);
+      std::memcpy(blk + leaf_off + 4 * j, &v, 4);
       h->perfect_leaf_map[(size_t)k * n_leaf + j] = nd;
     }
   }
@@ -325,15 +326,19 @@ struct PlanInput {
 };
 
 Plan choose_plan(const PlanInput &in) {
-  Plan best{};
-  double best_t = 1e300;
-  int best_waves_cu = -1, best_chunks = 1 << 30;
+  const int ilp = env_int("BRIDGER_ILP", 4) == 8 ? 8 : 4;  // trees walked at once per lane
+  const int kTreesMultiple = ilp;
   const int force_waves = env_int("BRIDGER_WAVES", 0);
   const int force_rows = env_int("BRIDGER_ROWS", 0);
   const int force_ct = env_int("BRIDGER_CHUNK_TREES", 0);
   const int force_wg_per_cu = env_int("BRIDGER_WG_PER_CU", 0);
   const int64_t n = std::max<int64_t>(in.n_rows, 1);
-  for (int pass = 0; pass < 2 && best_t == 1e300; ++pass) {
+  struct Cand {
+    Plan p;
+    int waves_cu, single, overlap;
+  };
+  std::vector<Cand> cands;
+  for (int pass = 0; pass < 2 && cands.empty(); ++pass) {
     for (int W : {1, 2, 4, 8, 16}) {
       if (force_waves && W != force_waves) continue;
       for (int R = 32; R <= 64 * W; R *= 2) {
@@ -348,24 +353,23 @@ Plan choose_plan(const PlanInput &in) {
           if (pass == 0 && m * W < kMinWavesPerCU) continue;
           const int64_t budget = kLdsBytesPerCU / m - x_tile - acc_bytes;
           if (budget < 2 * (int64_t)in.tree_bytes) continue;
-          int64_t chunk = std::min<int64_t>(budget / 2, 65536);  // immediate-offset reach
+          int64_t chunk = std::min<int64_t>(budget / 2, 65536);
           int ct = 0;
           int n_chunks;
           if (in.perfect) {
             ct = (int)(chunk / in.tree_bytes);
-            ct -= ct % kPerfectTreesMultiple;
-            if (ct < kPerfectTreesMultiple) {
-              if (in.n_trees < kPerfectTreesMultiple && ct >= in.n_trees) ct = in.n_trees;
+            ct -= ct % kTreesMultiple;
+            if (ct < kTreesMultiple) {
+              if (in.n_trees < kTreesMultiple && ct >= in.n_trees) ct = in.n_trees;
               else continue;
             }
-            ct = std::min(ct, ((in.n_trees + kPerfectTreesMultiple - 1) / kPerfectTreesMultiple) *
-                                  kPerfectTreesMultiple);
+            ct = std::min(ct, ((in.n_trees + kTreesMultiple - 1) / kTreesMultiple) * kTreesMultiple);
             if (force_ct) {
               if (force_ct * (int64_t)in.tree_bytes > chunk) continue;
               ct = force_ct;
             }
-            // every lane group needs at least one quad of trees per chunk
-            if (ct < kPerfectTreesMultiple * G && in.n_trees >= kPerfectTreesMultiple * G) continue;
+            // every lane group needs at least one group of trees per chunk
+            if (ct < kTreesMultiple * G && in.n_trees >= kTreesMultiple * G) continue;
             chunk = (int64_t)ct * in.tree_bytes;
             n_chunks = (in.n_trees + ct - 1) / ct;
           } else {
@@ -384,36 +388,53 @@ Plan choose_plan(const PlanInput &in) {
           const double lds_instr =
               (double)n / 64.0 * (2.0 * in.visits_per_row + in.n_trees) +
               n_wg * (in.forest_bytes / 1024.0);
-          const double t = std::max({hbm / kHbmBytesPerSec, stage / kL2BytesPerSec,
-                                     lds_instr / kLdsInstrPerSec});
-          const int waves_cu = m * W;
-          const bool better =
-              t < best_t * 0.999 ||
-              (t <= best_t * 1.001 &&
-               (waves_cu > best_waves_cu || (waves_cu == best_waves_cu && n_chunks < best_chunks)));
-          if (better) {
-            best_t = t;
-            best_waves_cu = waves_cu;
-            best_chunks = n_chunks;
-            best.waves = W;
-            best.rows_per_wg = R;
-            best.groups = G;
-            best.chunk_bytes = (int32_t)chunk;
-            best.trees_per_chunk = ct;
-            best.n_chunks = n_chunks;
-            best.lds_bytes = (int32_t)lds;
-            best.acc_in_lds = acc_lds;
-            best.hbm_bytes = hbm;
-            best.stage_bytes = stage;
-            best.lds_read_bytes = lds_instr * 256.0;
-            best.est_seconds = t;
-          }
+          Cand c;
+          c.p.waves = W;
+          c.p.rows_per_wg = R;
+          c.p.groups = G;
+          c.p.chunk_bytes = (int32_t)chunk;
+          c.p.trees_per_chunk = ct;
+          c.p.n_chunks = n_chunks;
+          c.p.lds_bytes = (int32_t)lds;
+          c.p.acc_in_lds = acc_lds;
+          c.p.ilp = ilp;
+          c.p.hbm_bytes = hbm;
+          c.p.stage_bytes = stage;
+          c.p.lds_read_bytes = lds_instr * 256.0;
+          c.p.est_seconds = std::max({hbm / kHbmBytesPerSec, stage / kL2BytesPerSec,
+                                      lds_instr / kLdsInstrPerSec});
+          c.waves_cu = m * W;
+          c.single = G == 1;
+          c.overlap = m >= 2;
+          cands.push_back(c);
         }
       }
     }
   }
-  if (best_t == 1e300) best.waves = 0;  // infeasible
-  return best;
+  Plan best{};
+  if (cands.empty()) return best;  // infeasible: waves == 0
+  double t_min = 1e300;
+  for (const Cand &c : cands) t_min = std::min(t_min, c.p.est_seconds);
+  // The model resolves a few percent; among plans within 2% of the fastest prefer one lane
+  // group (each lane walks every tree of its row: no split of a chunk's trees and no partial
+  // sums), then more resident waves (latency hiding), then two or more workgroups per CU
+  // (one workgroup's barrier and tail overlap another's work), then fewer chunks.
+  const Cand *pick = nullptr;
+  const bool log = env_int("BRIDGER_LOG", 0) != 0;
+  for (const Cand &c : cands) {
+    if (log)
+      std::fprintf(stderr, "[bridger plan] W=%d R=%d G=%d waves/CU=%d chunk=%d ct=%d chunks=%d lds=%d est=%.1fus%s\n",
+                   c.p.waves, c.p.rows_per_wg, c.p.groups, c.waves_cu, c.p.chunk_bytes,
+                   c.p.trees_per_chunk, c.p.n_chunks, c.p.lds_bytes, c.p.est_seconds * 1e6,
+                   c.p.est_seconds > 1.02 * t_min ? "" : "  (tie)");
+    if (c.p.est_seconds > 1.02 * t_min) continue;
+    if (!pick) { pick = &c; continue; }
+    auto key = [](const Cand &x) {
+      return std::make_tuple(x.single, x.waves_cu, x.overlap, -x.p.n_chunks);
+    };
+    if (key(c) > key(*pick)) pick = &c;
+  }
+  return pick->p;
 }
 
 void ragged_chunks(bridger_forest *h, int64_t chunk_bytes) {
@@ -564,6 +585,7 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
     a.lds_x_off = 2 * p.chunk_bytes;
     a.lds_acc_off = a.lds_x_off + h->F * p.rows_per_wg * 4;
     a.acc_in_lds = p.acc_in_lds;
+    a.ilp = p.ilp;
     const int64_t n_wg = (n_rows + p.rows_per_wg - 1) / p.rows_per_wg;
     if (h->kernel_active == kPerfect)
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);

@@ -3,11 +3,15 @@
 // Packed layouts (all little-endian, built once by bridger_forest_create):
 //
 // PERFECT (every tree perfect with one depth D, 1 <= D <= kMaxPerfectDepth):
-//   one block of tree_bytes per tree, in kernel tree order (trees stably sorted by class):
-//     [0, 8*(2^D - 1))        internal records {float threshold; uint32 feature}, breadth-first
-//                             heap order (children of slot n are 2n+1 and 2n+2)
-//     [8*(2^D - 1), +4*2^D)   leaf values, leaf slot j = heap slot 2^D - 1 + j
-//     padding up to a multiple of 16 bytes
+//   one block of tree_bytes = 12 * 2^D per tree, in kernel tree order (trees stably sorted
+//   by class):
+//     [0, 8)                  unused
+//     [8, 8*2^D)              internal records {float threshold; uint32 feature} in a 1-based
+//                             breadth-first heap: slot m at byte 8m, children 2m and 2m+1
+//     [8*2^D, 12*2^D)         leaf values: leaf j is heap slot 2^D + j; the two leaves of
+//                             last-level slot m form an 8-byte pair 4*2^D bytes past that
+//                             slot's record
+//   Every level's records and the leaf block start 16-byte aligned.
 //
 // RAGGED (any tree whose records fit one LDS chunk):
 //   8-byte records {uint32 w; uint32 meta}, trees contiguous in kernel order, each tree
@@ -44,6 +48,7 @@ struct Plan {
   int32_t n_chunks;
   int32_t lds_bytes;       // dynamic LDS per workgroup
   int32_t acc_in_lds;      // class/group partial sums kept in LDS
+  int32_t ilp;             // PERFECT: trees walked at once per lane (4 or 8)
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
 };
 
@@ -79,6 +84,7 @@ struct LaunchArgs {
   int32_t lds_x_off;           // byte offset of the feature tile in dynamic LDS
   int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
   int32_t acc_in_lds;
+  int32_t ilp;                 // PERFECT: trees walked at once per lane (4 or 8)
 };
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.

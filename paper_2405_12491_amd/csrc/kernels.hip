@@ -163,24 +163,33 @@ __device__ __forceinline__ void class_flush_all(const LaunchArgs &a, ClassAcc &c
 }
 
 // ======================================================================= PERFECT
-// Trees are perfect of depth D, stored as breadth-first heaps (internal.h).  Each lane walks
-// four trees at once (independent dependency chains); per level and tree: one 64-bit LDS read
-// {threshold, feature}, one 32-bit LDS read of the feature value, a compare and a select.
-template <int D, bool LEAVES, bool SIMPLE>
+// Trees are perfect of depth D (layout in internal.h): internal nodes are 8-byte records
+// {threshold, feature} in a 1-based breadth-first heap (slot m at byte 8m, children 2m and
+// 2m+1), followed by the leaf values; every level's records and the leaf block start 16-byte
+// aligned, which keeps the per-lane 64-bit gathers free of LDS bank conflicts.  Each lane
+// walks U trees at once (independent dependency chains, so U LDS reads are in flight per
+// lane); per level and tree: one 64-bit LDS read {threshold, feature}, one 32-bit LDS read of
+// the feature value, a compare and a select; after the last compare one 32-bit read of the
+// chosen leaf.
+template <int D, int U, bool LEAVES, bool SIMPLE>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, waves = blockDim.x >> 6;
   const int R = a.rows_per_wg, G = a.groups;
   const int r = tid & (R - 1);
-  const int g = tid / R;
+  // with R >= 64 a wave lies inside one lane group, so the group index (and every tree
+  // address derived from it) is wave-uniform and lives in scalar registers
+  const int g = SIMPLE ? 0 : (R >= 64 ? __builtin_amdgcn_readfirstlane(tid / R) : tid / R);
   const int64_t row = (int64_t)blockIdx.x * R + r;
   const bool row_ok = row < a.n_rows;
   const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
   const uint32_t tb = (uint32_t)a.tree_bytes;
   const int T = a.n_trees, CT = a.trees_per_chunk;
   const int shift = a.log2_row_bytes;
-  constexpr uint32_t kLeafOff = 4u << D;  // leaf slot 0 sits 4*2^D past the last-level record
+  // leaf pair of last-level heap slot m (record at base + 8m): base + 8*2^D + 8(m - 2^(D-1))
+  // = record + 4*2^D
+  constexpr uint32_t kPairOff = 4u << D;
 
   {
     const int t1 = CT < T ? CT : T;
@@ -206,64 +215,60 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
                   (n1 - n0) * (int)tb, wave, lane, waves);
     }
     const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
-    for (int q = t0 + 4 * g; q < t1; q += 4 * G) {
-      const int nq = (t1 - q) < 4 ? (t1 - q) : 4;  // valid trees in this quad
-      uint32_t base[4], addr[4], kl[4], kr[4];
+    for (int q = t0 + U * g; q < t1; q += U * G) {
+      const int nq = (t1 - q) < U ? (t1 - q) : U;  // valid trees in this group of U
+      uint32_t base[U], addr[U], kl[U], kr[U];
+      bool left[U];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        base[u] = buf + (uint32_t)(q - t0 + u) * tb;
-        addr[u] = base[u];
-        // heap slot n at base + 8n; children at base + 8(2n+1) = 2*addr + (8 - base) and
-        // base + 8(2n+2) = 2*addr + (16 - base)
-        kl[u] = opaque(8u - base[u]);
-        kr[u] = opaque(16u - base[u]);
+      for (int u = 0; u < U; ++u) {
+        // a slot past the chunk's last tree re-walks the group's first tree (in bounds; its
+        // result is discarded below)
+        const int uu = (u < nq) ? u : 0;
+        base[u] = buf + (uint32_t)(q - t0 + uu) * tb;
+        addr[u] = base[u] + 8u;  // the root, slot 1
+        // slot m at base + 8m; children at base + 16m = 2*addr - base and base + 16m + 8
+        kl[u] = opaque(0u - base[u]);
+        kr[u] = opaque(8u - base[u]);
       }
-      if (nq == 4) {
 #pragma unroll
-        for (int d = 0; d < D; ++d) {
-          uint2 rec[4];
-          float xv[4];
+      for (int d = 0; d < D; ++d) {
+        uint2 rec[U];
+        float xv[U];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) rec[u] = lds_u64(smem, addr[u]);
+        for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, addr[u]);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) xv[u] = lds_f32(smem, (rec[u].y << shift) + lane_off);
+        for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, (rec[u].y << shift) + lane_off);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const bool left = xv[u] <= __uint_as_float(rec[u].x);
-            if (d < D - 1)
-              addr[u] = 2u * addr[u] + (left ? kl[u] : kr[u]);
-            else
-              addr[u] = addr[u] + (left ? 0u : 4u);
-          }
-        }
-      } else {
-        for (int u = 0; u < nq; ++u) {
-#pragma unroll
-          for (int d = 0; d < D; ++d) {
-            const uint2 rec = lds_u64(smem, addr[u]);
-            const float xv = lds_f32(smem, (rec.y << shift) + lane_off);
-            const bool left = xv <= __uint_as_float(rec.x);
-            if (d < D - 1)
-              addr[u] = 2u * addr[u] + (left ? kl[u] : kr[u]);
-            else
-              addr[u] = addr[u] + (left ? 0u : 4u);
-          }
+        for (int u = 0; u < U; ++u) {
+          const bool lft = xv[u] <= __uint_as_float(rec[u].x);
+          if (d < D - 1)
+            addr[u] = 2u * addr[u] + (lft ? kl[u] : kr[u]);
+          else
+            left[u] = lft;
         }
       }
       if (LEAVES) {
-        for (int u = 0; u < nq; ++u) {
-          const int t = q + u;
-          const uint32_t slot = (addr[u] + kLeafOff - base[u] - 8u * ((1u << D) - 1u)) >> 2;
-          if (row_ok)
-            a.out_leaf[row * (int64_t)T + a.tree_order[t]] = a.leaf_map[(int64_t)t * (1 << D) + slot];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (u < nq && row_ok) {
+            const int t = q + u;
+            // last-level slot m owns leaf slots 2(m - 2^(D-1)) + {0, 1}
+            const uint32_t m = (addr[u] - base[u]) >> 3;
+            const uint32_t slot = 2u * (m - (1u << (D - 1))) + (left[u] ? 0u : 1u);
+            a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
+                a.leaf_map[(int64_t)t * (1 << D) + slot];
+          }
         }
       } else {
-        float lv[4];
+        float lv[U];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) lv[u] = (u < nq) ? lds_f32(smem, addr[u] + kLeafOff) : 0.0f;
-        for (int u = 0; u < nq; ++u) {
-          if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
-          ca.acc += (double)lv[u];
+        for (int u = 0; u < U; ++u) lv[u] = lds_f32(smem, addr[u] + kPairOff + (left[u] ? 0u : 4u));
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (u < nq) {
+            if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+            ca.acc += (double)lv[u];
+          }
         }
       }
     }
@@ -458,9 +463,16 @@ static int launch_perfect_d(const LaunchArgs &a, int waves, int64_t n_wg, int ld
                             void *stream) {
   const bool simple = a.K == 1 && a.groups == 1;
   const int threads = 64 * waves;
-  if (a.out_leaf) return launch_common(perfect_kernel<D, true, false>, threads, n_wg, lds_bytes, stream, a);
-  if (simple) return launch_common(perfect_kernel<D, false, true>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(perfect_kernel<D, false, false>, threads, n_wg, lds_bytes, stream, a);
+  if (a.out_leaf)
+    return launch_common(perfect_kernel<D, 4, true, false>, threads, n_wg, lds_bytes, stream, a);
+  if (a.ilp == 8) {
+    if (simple)
+      return launch_common(perfect_kernel<D, 8, false, true>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_kernel<D, 8, false, false>, threads, n_wg, lds_bytes, stream, a);
+  }
+  if (simple)
+    return launch_common(perfect_kernel<D, 4, false, true>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(perfect_kernel<D, 4, false, false>, threads, n_wg, lds_bytes, stream, a);
 }
 
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

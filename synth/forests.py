@@ -101,6 +101,17 @@ def x_rows(seed: int, kind: str, n_features: int, r0: int, r1: int, **kw) -> np.
     return out
 
 
+def x_take(seed: int, kind: str, n_features: int, rows, **kw) -> np.ndarray:
+    """The given rows (any order) of the feature matrix, generating each needed block once."""
+    rows = np.asarray(rows, np.int64)
+    out = np.empty((rows.shape[0], n_features), dtype=np.float32)
+    blocks = rows // BLOCK_ROWS
+    for b in np.unique(blocks):
+        sel = np.nonzero(blocks == b)[0]
+        out[sel] = x_block(seed, kind, n_features, int(b), **kw)[rows[sel] - b * BLOCK_ROWS]
+    return out
+
+
 # ------------------------------------------------------------------------- trees
 def perfect_tree_arrays(depth: int, feats: np.ndarray, thrs: np.ndarray, leaves: np.ndarray):
     """Arrays of one perfect tree in breadth-first numbering.

@@ -121,26 +121,28 @@ def test_predict_on_host_only_handle_fails():
 
 # ----------------------------------------------------- packed-layout interpreter
 def walk_perfect(f: B.Forest, model, X):
+    """1-based heap: slot m at byte 8m (children 2m, 2m+1), leaves from byte 8*2^D."""
     blob = B.bridger_forest_packed(f.handle, 0, np.uint8)
     leaf_map = B.bridger_forest_packed(f.handle, 2, np.int32)
     order = B.bridger_forest_packed(f.handle, 3, np.int32)
     D = f.info()["max_depth"]
     T = f.n_trees
     tb = blob.size // T
-    n_int = (1 << D) - 1
+    assert tb == 12 << D
+    n_leaf = 1 << D
     leaves = np.empty((X.shape[0], T), np.int32)
     vals = np.empty((X.shape[0], T), np.float32)
+    rows = np.arange(X.shape[0])
     for k in range(T):
         blk = blob[k * tb:(k + 1) * tb]
-        thr = blk[:8 * n_int].view(np.float32)[0::2]
-        feat = blk[:8 * n_int].view(np.uint32)[1::2]
-        lv = blk[8 * n_int:8 * n_int + 4 * (n_int + 1)].view(np.float32)
-        n = np.zeros(X.shape[0], np.int64)
+        thr = blk[:8 * n_leaf].view(np.float32)[0::2]
+        feat = blk[:8 * n_leaf].view(np.uint32)[1::2]
+        lv = blk[8 * n_leaf:12 * n_leaf].view(np.float32)
+        m = np.ones(X.shape[0], np.int64)
         for _ in range(D):
-            go_left = X[np.arange(X.shape[0]), feat[n]] <= thr[n]
-            n = 2 * n + np.where(go_left, 1, 2)
-        j = n - n_int
-        leaves[:, order[k]] = leaf_map[k * (n_int + 1) + j]
+            m = 2 * m + np.where(X[rows, feat[m]] <= thr[m], 0, 1)
+        j = m - n_leaf
+        leaves[:, order[k]] = leaf_map[k * n_leaf + j]
         vals[:, order[k]] = lv[j]
     return leaves, vals
 

@@ -252,6 +252,8 @@ def _full_X_device(w):
     for r in range(0, w.n_rows, step):
         blk = x_rows(w.seed, w.x_kind, w.n_features, r, min(r + step, w.n_rows), **w.x_params)
         Xd[r:r + blk.shape[0]].copy_(torch.from_numpy(blk))
+        if (r // step) % 8 == 0:
+            print(f"[full] X rows {r}..{r + blk.shape[0]}", flush=True)
     return Xd
 
 
@@ -267,7 +269,7 @@ def test_workload_full_size_sampled(name):
     """Full-size inputs in the benchmark's launch configuration; sampled rows against the
     oracle, plus leaf ids on windows at the start, middle and end."""
     import torch
-    from synth import x_rows
+    from synth import x_rows, x_take
     w = make_workload(name)
     print(f"[full] {name}: building X {w.n_rows}x{w.n_features}", flush=True)
     Xd = _full_X_device(w)
@@ -279,13 +281,14 @@ def test_workload_full_size_sampled(name):
         torch.cuda.synchronize()
         got = out.cpu().numpy()
         idx = _sample_rows(w.n_rows, plan["rows_per_wg"] or 256, rng)
-        Xs = np.concatenate([x_rows(w.seed, w.x_kind, w.n_features, int(i), int(i) + 1, **w.x_params)
-                             for i in idx])
+        print(f"[full] {name}: oracle on {len(idx)} sampled rows", flush=True)
+        Xs = x_take(w.seed, w.x_kind, w.n_features, idx, **w.x_params)
         ref, _ = oracle_predict(w.forest, Xs)
         assert_scores(got[idx], ref, f"{name} full-size sampled scores")
         assert np.all(np.isfinite(got))
         win = 256 if w.forest.n_trees * w.n_features < 300_000 else 64
         for a in (0, w.n_rows // 2 + 13, w.n_rows - win):
+            print(f"[full] {name}: leaf ids for rows [{a}, {a + win})", flush=True)
             lv = gpu_predict(f, Xd[a:a + win], leaves=True)
             _, ref_lv = oracle_predict(w.forest, x_rows(w.seed, w.x_kind, w.n_features, a, a + win, **w.x_params),
                                        leaves=True)
