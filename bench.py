@@ -65,7 +65,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="gbdt_d6")
     p.add_argument("--rows", type=int, default=None, help="override the workload's row count")
-    p.add_argument("--kernel", default="auto", choices=["auto", "perfect", "ragged", "direct"])
+    p.add_argument("--kernel", default="auto", choices=["auto", "perfect", "ragged", "direct", "gemm"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-rows", type=int, default=200_000)
     p.add_argument("--calib-copy", action="store_true",
@@ -155,7 +155,7 @@ def main():
 
     forest = B.Forest(w.forest)
     if args.kernel != "auto":
-        forest.kernel = {"perfect": 1, "ragged": 2, "direct": 3}[args.kernel]
+        forest.kernel = {"perfect": 1, "ragged": 2, "direct": 3, "gemm": 4}[args.kernel]
     out = torch.empty((w.n_rows, w.forest.n_classes), dtype=torch.float32, device=dev)
     plan = forest.plan(w.n_rows)
     for _ in range(args.warmup):

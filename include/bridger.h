@@ -62,12 +62,16 @@ enum { BRIDGER_XFORM_IDENTITY = 0, BRIDGER_XFORM_SIGMOID = 1, BRIDGER_XFORM_SOFT
  * one common depth (1..10), else RAGGED when every tree fits an LDS chunk, else
  * DIRECT.  PERFECT and RAGGED stage the trees through LDS (the data-movement
  * model of Eq. 1 sizes the row tile and the tree chunks); DIRECT reads nodes
- * from global memory and handles any forest. */
+ * from global memory and handles any forest.  GEMM is the matrix-multiply
+ * lowering (Table 4's matmul and one_hot on the matrix cores) for perfect trees
+ * of depth 1..4 with one output class and at most 64 features; it is never
+ * chosen by AUTO and exists to be measured against the traversal kernels. */
 enum {
   BRIDGER_KERNEL_AUTO = 0,
   BRIDGER_KERNEL_PERFECT = 1,
   BRIDGER_KERNEL_RAGGED = 2,
-  BRIDGER_KERNEL_DIRECT = 3
+  BRIDGER_KERNEL_DIRECT = 3,
+  BRIDGER_KERNEL_GEMM = 4
 };
 
 /* Flags for bridger_forest_create_ex. */

@@ -30,7 +30,8 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "INVALID_FOREST", 3: "UNSUPPO
 BRIDGER_AGG_SUM, BRIDGER_AGG_MEAN = 0, 1
 BRIDGER_XFORM_IDENTITY, BRIDGER_XFORM_SIGMOID, BRIDGER_XFORM_SOFTMAX = 0, 1, 2
 BRIDGER_KERNEL_AUTO, BRIDGER_KERNEL_PERFECT, BRIDGER_KERNEL_RAGGED, BRIDGER_KERNEL_DIRECT = 0, 1, 2, 3
-KERNEL_NAMES = {0: "auto", 1: "perfect", 2: "ragged", 3: "direct"}
+BRIDGER_KERNEL_GEMM = 4
+KERNEL_NAMES = {0: "auto", 1: "perfect", 2: "ragged", 3: "direct", 4: "gemm"}
 BRIDGER_CREATE_HOST_ONLY = 1
 
 _lib = None

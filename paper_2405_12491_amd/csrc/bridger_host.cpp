@@ -513,6 +513,11 @@ bridger_status upload_all(bridger_forest *h) {
   return BRIDGER_OK;
 }
 
+bool gemm_ok(const bridger_forest *h) {
+  return h->perfect_ok && h->perfect_depth >= 1 && h->perfect_depth <= kMaxGemmDepth &&
+         h->K == 1 && h->F <= kMaxGemmFeatures;
+}
+
 int32_t resolve_auto(const bridger_forest *h) {
   if (h->perfect_ok) return kPerfect;
   if (h->ragged_ok) return kRagged;
@@ -591,6 +596,12 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else
       err = launch_ragged(a, p.waves, n_wg, p.lds_bytes, stream);
+  } else if (h->kernel_active == kGemm) {
+    a.nodes = (const uint8_t *)h->d_perfect.nodes;
+    a.leaf_map = (const int32_t *)h->d_perfect.leaf_map;
+    a.tree_bytes = h->perfect_tree_bytes;
+    const int64_t n_wg = (n_rows + 63) / 64;  // 4 waves x 16 rows
+    err = launch_gemm(h->perfect_depth, a, n_wg, stream);
   } else {
     a.nodes = (const uint8_t *)h->d_direct.nodes;
     a.tree_start = (const int32_t *)h->d_direct.tree_start;
@@ -731,6 +742,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     if (forced == kPerfect && h->perfect_ok) h->kernel_active = kPerfect;
     if (forced == kRagged && h->ragged_ok) h->kernel_active = kRagged;
     if (forced == kDirect) h->kernel_active = kDirect;
+    if (forced == kGemm && gemm_ok(h)) h->kernel_active = kGemm;
 
     if (!h->host_only) {
       int ndev = 0;
@@ -811,6 +823,13 @@ bridger_status bridger_forest_set_kernel(bridger_forest_t h, int32_t kernel) {
       h->kernel_active = kRagged;
       return BRIDGER_OK;
     case BRIDGER_KERNEL_DIRECT: h->kernel_active = kDirect; return BRIDGER_OK;
+    case BRIDGER_KERNEL_GEMM:
+      if (!gemm_ok(h))
+        return fail(BRIDGER_ERR_UNSUPPORTED,
+                    "the matrix lowering needs perfect trees of depth 1..4, one class and at "
+                    "most 64 features");
+      h->kernel_active = kGemm;
+      return BRIDGER_OK;
     default: return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown kernel");
   }
 }
@@ -837,6 +856,10 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
   } else if (h->kernel_active == kRagged) {
     p = h->ragged_plan;
     forest_bytes = 8.0 * h->ragged_rec.size();
+  } else if (h->kernel_active == kGemm) {
+    p.rows_per_wg = 64;
+    p.waves = 4;
+    forest_bytes = (double)h->perfect_blob.size();
   } else {
     p.rows_per_wg = 256;
     p.waves = 4;
@@ -850,10 +873,10 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
   if (n_chunks) *n_chunks = p.n_chunks;
   if (lds_bytes) *lds_bytes = p.lds_bytes;
   if (hbm_bytes) *hbm_bytes = n * h->F * 4 + n * h->K * 4 + forest_bytes;
-  if (stage_bytes)
-    *stage_bytes = (h->kernel_active == kDirect) ? 0.0 : n_wg * forest_bytes + n * h->F * 4;
+  const bool no_lds = h->kernel_active == kDirect || h->kernel_active == kGemm;
+  if (stage_bytes) *stage_bytes = no_lds ? 0.0 : n_wg * forest_bytes + n * h->F * 4;
   if (lds_read_bytes)
-    *lds_read_bytes = (h->kernel_active == kDirect)
+    *lds_read_bytes = no_lds
                           ? 0.0
                           : 256.0 * (n / 64.0 * (2.0 * h->visits_per_row_est + h->n_trees) +
                                      n_wg * forest_bytes / 1024.0);
@@ -874,6 +897,7 @@ bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const vo
   if (which == 3) return give(h->tree_order.data(), h->tree_order.size() * 4);
   switch (h->kernel_active) {
     case kPerfect:
+    case kGemm:
       if (which == 0) return give(h->perfect_blob.data(), h->perfect_blob.size());
       if (which == 2) return give(h->perfect_leaf_map.data(), h->perfect_leaf_map.size() * 4);
       break;

@@ -36,7 +36,9 @@ constexpr int kMaxRel = 0x7FFF;
 constexpr int kMaxRaggedFeatures = 0xFFFF;
 constexpr int kMaxClasses = 64;  // class sums of one 256-row block fit LDS in every kernel
 
-enum Kernel { kAuto = 0, kPerfect = 1, kRagged = 2, kDirect = 3 };
+enum Kernel { kAuto = 0, kPerfect = 1, kRagged = 2, kDirect = 3, kGemm = 4 };
+constexpr int kMaxGemmDepth = 4;
+constexpr int kMaxGemmFeatures = 64;
 
 // Launch plan (host side), chosen by the data-movement model of Eq. 1.
 struct Plan {
@@ -92,5 +94,6 @@ int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int 
                    void *stream);
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
 int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream);
+int launch_gemm(int depth, const LaunchArgs &a, int64_t n_wg, void *stream);
 
 }  // namespace bridger

@@ -291,11 +291,24 @@ CONFIGS = {
         description="1000 ragged trees (split prob 0.85, max depth 12), 4M x 256 N(0,1) rows; sum"),
 }
 
+# Extra shallow-forest workloads used only to compare the matrix-multiply lowering with the
+# traversal kernels (not part of the five benchmark configurations).
+EXTRA_CONFIGS = {
+    "shallow_d3": dict(
+        seed=11, n_rows=1_000_000, n_features=28, x="normal", shape="perfect", depth=3, n_trees=100,
+        thr="column", leaf_sigma=0.1, agg=AGG_SUM, xform=XFORM_SIGMOID, base=0.0,
+        description="binary GBDT, 100 perfect depth-3 trees, 1M x 28 N(0,1) rows; sigmoid"),
+    "shallow_d4": dict(
+        seed=12, n_rows=1_000_000, n_features=28, x="normal", shape="perfect", depth=4, n_trees=50,
+        thr="column", leaf_sigma=0.1, agg=AGG_SUM, xform=XFORM_SIGMOID, base=0.0,
+        description="binary GBDT, 50 perfect depth-4 trees, 1M x 28 N(0,1) rows; sigmoid"),
+}
+
 _FOREST_CACHE: dict = {}
 
 
 def make_workload(name: str, n_rows: Optional[int] = None) -> Workload:
-    spec = CONFIGS[name]
+    spec = CONFIGS[name] if name in CONFIGS else EXTRA_CONFIGS[name]
     if name not in _FOREST_CACHE:
         _FOREST_CACHE[name] = make_forest(spec)
     return Workload(name=name, seed=spec["seed"], n_rows=spec["n_rows"] if n_rows is None else n_rows,

@@ -15,7 +15,8 @@ from synth import (AGG_MEAN, AGG_SUM, CONFIGS, XFORM_IDENTITY, XFORM_SIGMOID, XF
 
 pytestmark = pytest.mark.gpu
 
-KERNELS = [B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT]
+KERNELS = [B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT,
+           B.BRIDGER_KERNEL_GEMM]
 
 # rows per workload for the oracle-sized cases: several tiles of the largest row tile (1024)
 # plus a tail that is not a multiple of 32
@@ -55,6 +56,22 @@ def test_workload_small(name):
             check_parity(w.forest, X, k, f"{name}/{B.KERNEL_NAMES[k]}", Xd=Xd, forest=f)
             ran += 1
     assert ran >= 2
+
+
+@pytest.mark.parametrize("name", ["shallow_d3", "shallow_d4"])
+def test_shallow_workloads_all_kernels(name):
+    """The matrix-multiply lowering and the traversal kernels on shallow forests."""
+    w = make_workload(name, 3 * 1024 + 77)
+    X = w.X()
+    X[5, 3] = np.nan                     # rows with non-finite features take the walk fallback
+    X[17, 0] = np.inf
+    X[700, 27] = -np.inf
+    Xd = to_dev(X)
+    with B.Forest(w.forest) as f:
+        assert supported(f, B.BRIDGER_KERNEL_GEMM)
+        for k in KERNELS:
+            if supported(f, k):
+                check_parity(w.forest, X, k, f"{name}/{B.KERNEL_NAMES[k]}", Xd=Xd, forest=f)
 
 
 def test_direct_sums_bit_identical():
