@@ -84,7 +84,9 @@ struct bridger_forest {
   bool perfect_ok = false;
   int32_t perfect_tree_bytes = 0;
   std::vector<uint8_t> perfect_blob;
+  std::vector<uint8_t> perfect_trav;  // traversal copy: {threshold, feature * 4R}
   std::vector<int32_t> perfect_leaf_map;
+  bool finite_thresholds = false;
   Plan perfect_plan{};
 
   // RAGGED
@@ -105,6 +107,7 @@ struct bridger_forest {
   void *d_class_begin = nullptr, *d_class_count = nullptr, *d_base = nullptr,
        *d_tree_order = nullptr;
   DevArrays d_perfect, d_ragged, d_direct;
+  void *d_perfect_trav = nullptr;
   double visits_per_row_est = 0;  // for the model: mean internal visits per row (all trees)
 };
 
@@ -223,6 +226,29 @@ void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *
       const float v = value[a + nd];
       std::memcpy(blk + leaf_off + 4 * j, &v, 4);
       h->perfect_leaf_map[(size_t)k * n_leaf + j] = nd;
+    }
+  }
+}
+
+// Records of the PERFECT kernel: the feature index becomes the byte offset of the feature's
+// row in the LDS tile of the chosen plan (row stride 4R bytes), and a threshold of -0 is
+// stored as +0 (equal under <=; the sign-of-difference step needs the +0).
+void build_perfect_trav(bridger_forest *h) {
+  const int D = h->perfect_depth;
+  const int tb = h->perfect_tree_bytes;
+  const uint32_t row_bytes = 4u * (uint32_t)h->perfect_plan.rows_per_wg;
+  h->perfect_trav = h->perfect_blob;
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    uint8_t *blk = h->perfect_trav.data() + (size_t)k * tb;
+    for (int m = 1; m < (1 << D); ++m) {
+      float th;
+      uint32_t f;
+      std::memcpy(&th, blk + 8 * m, 4);
+      std::memcpy(&f, blk + 8 * m + 4, 4);
+      if (th == 0.0f) th = 0.0f;
+      f *= row_bytes;
+      std::memcpy(blk + 8 * m, &th, 4);
+      std::memcpy(blk + 8 * m + 4, &f, 4);
     }
   }
 }
@@ -481,6 +507,7 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_class_count);
   free_dev(h->d_base);
   free_dev(h->d_tree_order);
+  free_dev(h->d_perfect_trav);
   for (DevArrays *d : {&h->d_perfect, &h->d_ragged, &h->d_direct}) {
     free_dev(d->nodes);
     free_dev(d->tree_start);
@@ -498,6 +525,7 @@ bridger_status upload_all(bridger_forest *h) {
   if ((s = upload(&h->d_tree_order, h->tree_order)) != BRIDGER_OK) return s;
   if (h->perfect_ok) {
     if ((s = upload(&h->d_perfect.nodes, h->perfect_blob, 1024)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_perfect_trav, h->perfect_trav, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_perfect.leaf_map, h->perfect_leaf_map)) != BRIDGER_OK) return s;
   }
   if (h->ragged_ok) {
@@ -575,7 +603,9 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
   if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
     const Plan &p = h->kernel_active == kPerfect ? h->perfect_plan : h->ragged_plan;
     const DevArrays &d = h->kernel_active == kPerfect ? h->d_perfect : h->d_ragged;
-    a.nodes = (const uint8_t *)d.nodes;
+    a.nodes = h->kernel_active == kPerfect ? (const uint8_t *)h->d_perfect_trav
+                                           : (const uint8_t *)d.nodes;
+    a.finite_thresholds = h->finite_thresholds ? 1 : 0;
     a.tree_start = (const int32_t *)d.tree_start;
     a.chunk_first = (const int32_t *)d.chunk_first;
     a.chunk_rec = (const int32_t *)d.chunk_rec;
@@ -695,6 +725,9 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       visits += sh.perfect ? sh.depth : sh.mean_path;
     }
     h->visits_per_row_est = visits;
+    h->finite_thresholds = env_int("BRIDGER_NO_SIGN_STEP", 0) == 0;
+    for (int64_t i = 0; i < h->n_nodes && h->finite_thresholds; ++i)
+      if (left[i] != -1 && !std::isfinite(threshold[i])) h->finite_thresholds = false;
     h->all_perfect = all_perfect ? 1 : 0;
     h->perfect_depth = all_perfect ? common_depth : -1;
 
@@ -729,6 +762,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
       h->perfect_plan = choose_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
+      if (h->perfect_ok) build_perfect_trav(h);
     }
     if (pack_ragged(h, tree_offsets, feature, threshold, left, right, value)) {
       PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),

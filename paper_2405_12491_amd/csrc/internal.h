@@ -12,6 +12,9 @@
 //                             last-level slot m form an 8-byte pair 4*2^D bytes past that
 //                             slot's record
 //   Every level's records and the leaf block start 16-byte aligned.
+//   The PERFECT kernel reads a traversal copy of this layout in which each record holds
+//   {threshold with -0 stored as +0; byte offset feature * 4R of the feature's row in the
+//   LDS tile of R rows}; the copy is rebuilt whenever the launch plan (and so R) is chosen.
 //
 // RAGGED (any tree whose records fit one LDS chunk):
 //   8-byte records {uint32 w; uint32 meta}, trees contiguous in kernel order, each tree
@@ -87,6 +90,7 @@ struct LaunchArgs {
   int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
   int32_t acc_in_lds;
   int32_t ilp;                 // PERFECT: trees walked at once per lane (4 or 8)
+  int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)
 };
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.

@@ -40,13 +40,6 @@ __device__ __forceinline__ uint2 lds_u64(const uint8_t *, uint32_t addr) {
   const uint64_t v = *(const __attribute__((address_space(3))) uint64_t *)(uintptr_t)addr;
   return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
 }
-// Hide a value from the optimiser so a select between two precomputed offsets stays one
-// v_cndmask instead of being re-derived (select of constants, then a subtract) per level.
-__device__ __forceinline__ uint32_t opaque(uint32_t v) {
-  asm volatile("" : "+v"(v));
-  return v;
-}
-
 // Stage `bytes` (multiple of 16) from global memory into LDS at byte offset `dst` with
 // direct global->LDS loads: each wave instruction moves 1 KB (64 lanes x 16 bytes).
 __device__ __forceinline__ void stage_async(uint8_t *smem, uint32_t dst, const uint8_t *src,
@@ -62,11 +55,18 @@ __device__ __forceinline__ void stage_async(uint8_t *smem, uint32_t dst, const u
 
 __device__ __forceinline__ void wait_stage() { __builtin_amdgcn_s_waitcnt(0); }
 
-// Load this lane's row into the feature-major LDS tile (zeros past the last row).
+// Load this lane's row into the feature-major LDS tile (zeros past the last row).  With
+// NAN_TO_INF a NaN feature is stored as +inf: against finite thresholds both compare false
+// (x <= t), so every split sends them the same way.
+template <bool NAN_TO_INF = false>
 __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a, int r,
                                               int64_t row, bool row_ok) {
   float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
   const int R = a.rows_per_wg;
+  auto put = [&](int f, float v) {
+    if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
+    xt[f * R + r] = v;
+  };
   if (!row_ok) {
     for (int f = 0; f < a.F; ++f) xt[f * R + r] = 0.0f;
     return;
@@ -78,24 +78,24 @@ __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a
     int i = 0;
     for (; i + 2 <= n4; i += 2) {
       float4 v0 = x4[i], v1 = x4[i + 1];
-      xt[(4 * i + 0) * R + r] = v0.x;
-      xt[(4 * i + 1) * R + r] = v0.y;
-      xt[(4 * i + 2) * R + r] = v0.z;
-      xt[(4 * i + 3) * R + r] = v0.w;
-      xt[(4 * i + 4) * R + r] = v1.x;
-      xt[(4 * i + 5) * R + r] = v1.y;
-      xt[(4 * i + 6) * R + r] = v1.z;
-      xt[(4 * i + 7) * R + r] = v1.w;
+      put(4 * i + 0, v0.x);
+      put(4 * i + 1, v0.y);
+      put(4 * i + 2, v0.z);
+      put(4 * i + 3, v0.w);
+      put(4 * i + 4, v1.x);
+      put(4 * i + 5, v1.y);
+      put(4 * i + 6, v1.z);
+      put(4 * i + 7, v1.w);
     }
     for (; i < n4; ++i) {
       float4 v = x4[i];
-      xt[(4 * i + 0) * R + r] = v.x;
-      xt[(4 * i + 1) * R + r] = v.y;
-      xt[(4 * i + 2) * R + r] = v.z;
-      xt[(4 * i + 3) * R + r] = v.w;
+      put(4 * i + 0, v.x);
+      put(4 * i + 1, v.y);
+      put(4 * i + 2, v.z);
+      put(4 * i + 3, v.w);
     }
   } else {
-    for (int f = 0; f < a.F; ++f) xt[f * R + r] = xr[f];
+    for (int f = 0; f < a.F; ++f) put(f, xr[f]);
   }
 }
 
@@ -163,15 +163,45 @@ __device__ __forceinline__ void class_flush_all(const LaunchArgs &a, ClassAcc &c
 }
 
 // ======================================================================= PERFECT
-// Trees are perfect of depth D (layout in internal.h): internal nodes are 8-byte records
-// {threshold, feature} in a 1-based breadth-first heap (slot m at byte 8m, children 2m and
-// 2m+1), followed by the leaf values; every level's records and the leaf block start 16-byte
-// aligned, which keeps the per-lane 64-bit gathers free of LDS bank conflicts.  Each lane
-// walks U trees at once (independent dependency chains, so U LDS reads are in flight per
-// lane); per level and tree: one 64-bit LDS read {threshold, feature}, one 32-bit LDS read of
-// the feature value, a compare and a select; after the last compare one 32-bit read of the
-// chosen leaf.
-template <int D, int U, bool LEAVES, bool SIMPLE>
+// Trees are perfect of depth D (layout in internal.h).  The kernel reads the traversal copy
+// of the layout, whose records hold {threshold, byte offset of the feature's row in the LDS
+// tile} so that the feature gather needs one add.  A lane's state per tree is its 1-based heap
+// slot m (root 1, children 2m and 2m + 1); each lane walks U trees at once, so U independent
+// LDS reads are in flight per lane.  One level of one tree:
+//   rec = LDS[base + 8m]  (64-bit gather),  x = LDS[rec.offset + lane's row]  (32-bit gather),
+//   m   = 2m + (x <= rec.threshold ? 0 : 1).
+// With only finite thresholds (FIN) the step is computed as the sign bit of threshold - x
+// shifted into m by one funnel shift, which needs no compare mask: for finite t and x != NaN
+// the IEEE difference t - x is +0 when x == t and otherwise nonzero with the sign of t - x
+// (denormals are kept; ties and -0 are handled by storing thresholds of zero as +0), it is
+// -inf for x = +inf and +inf for x = -inf, and a NaN feature is stored as +inf, which every
+// finite threshold sends right as the compare would.  After D levels m - 2^D is the leaf.
+template <int D, int U, bool FIN>
+__device__ __forceinline__ void walk_trees(const uint8_t *smem, uint32_t b0, uint32_t tb,
+                                           uint32_t lane_off, uint32_t (&m)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) m[u] = 1u;
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    uint2 rec[U];
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, (m[u] << 3) + b0 + (uint32_t)u * tb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (FIN) {
+        const float diff = __uint_as_float(rec[u].x) - xv[u];
+        m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
+      } else {
+        m[u] = 2u * m[u] + ((xv[u] <= __uint_as_float(rec[u].x)) ? 0u : 1u);
+      }
+    }
+  }
+}
+
+template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -186,16 +216,15 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
   const uint32_t tb = (uint32_t)a.tree_bytes;
   const int T = a.n_trees, CT = a.trees_per_chunk;
-  const int shift = a.log2_row_bytes;
-  // leaf pair of last-level heap slot m (record at base + 8m): base + 8*2^D + 8(m - 2^(D-1))
-  // = record + 4*2^D
-  constexpr uint32_t kPairOff = 4u << D;
+  // leaf j of a tree is at base + 8 * 2^D + 4j, i.e. base + 4m + 4 * 2^D for final slot m
+  constexpr uint32_t kLeafOff = 4u << D;
+  constexpr uint32_t kFirstLeaf = 1u << D;
 
   {
     const int t1 = CT < T ? CT : T;
     stage_async(smem, 0, a.nodes, t1 * (int)tb, wave, lane, waves);
   }
-  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  if (g == 0) load_row_tile<FIN>(smem, a, r, row, row_ok);
   wait_stage();
   __syncthreads();
 
@@ -206,6 +235,30 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   ca.acc = SIMPLE ? (a.aggregate == 0 ? (double)a.base[0] : 0.0) : class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
 
+  // leaf ids or leaf values of N walked trees, kernel trees q .. q + N - 1
+  auto finish = [&](auto &m, int q, uint32_t b0) {
+    constexpr int N = sizeof(m) / sizeof(m[0]);
+    if (LEAVES) {
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
+        if (row_ok) {
+          const int t = q + u;
+          a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
+              a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
+        }
+      }
+    } else {
+      float lv[N];
+#pragma unroll
+      for (int u = 0; u < N; ++u) lv[u] = lds_f32(smem, (m[u] << 2) + b0 + (uint32_t)u * tb + kLeafOff);
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
+        if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+        ca.acc += (double)lv[u];
+      }
+    }
+  };
+
   for (int c = 0; c < a.n_chunks; ++c) {
     const int t0 = c * CT;
     const int t1 = (t0 + CT < T) ? t0 + CT : T;
@@ -215,62 +268,20 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
                   (n1 - n0) * (int)tb, wave, lane, waves);
     }
     const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
-    for (int q = t0 + U * g; q < t1; q += U * G) {
-      const int nq = (t1 - q) < U ? (t1 - q) : U;  // valid trees in this group of U
-      uint32_t base[U], addr[U], kl[U], kr[U];
-      bool left[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        // a slot past the chunk's last tree re-walks the group's first tree (in bounds; its
-        // result is discarded below)
-        const int uu = (u < nq) ? u : 0;
-        base[u] = buf + (uint32_t)(q - t0 + uu) * tb;
-        addr[u] = base[u] + 8u;  // the root, slot 1
-        // slot m at base + 8m; children at base + 16m = 2*addr - base and base + 16m + 8
-        kl[u] = opaque(0u - base[u]);
-        kr[u] = opaque(8u - base[u]);
-      }
-#pragma unroll
-      for (int d = 0; d < D; ++d) {
-        uint2 rec[U];
-        float xv[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, addr[u]);
-#pragma unroll
-        for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, (rec[u].y << shift) + lane_off);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const bool lft = xv[u] <= __uint_as_float(rec[u].x);
-          if (d < D - 1)
-            addr[u] = 2u * addr[u] + (lft ? kl[u] : kr[u]);
-          else
-            left[u] = lft;
-        }
-      }
-      if (LEAVES) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          if (u < nq && row_ok) {
-            const int t = q + u;
-            // last-level slot m owns leaf slots 2(m - 2^(D-1)) + {0, 1}
-            const uint32_t m = (addr[u] - base[u]) >> 3;
-            const uint32_t slot = 2u * (m - (1u << (D - 1))) + (left[u] ? 0u : 1u);
-            a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
-                a.leaf_map[(int64_t)t * (1 << D) + slot];
-          }
-        }
-      } else {
-        float lv[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) lv[u] = lds_f32(smem, addr[u] + kPairOff + (left[u] ? 0u : 4u));
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          if (u < nq) {
-            if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
-            ca.acc += (double)lv[u];
-          }
-        }
-      }
+    // whole groups of U trees, then (only when the chunk's tree count leaves one) a partial
+    // group walked one tree at a time
+    int q = t0 + U * g;
+    for (; q + U <= t1; q += U * G) {
+      const uint32_t b0 = buf + (uint32_t)(q - t0) * tb;
+      uint32_t m[U];
+      walk_trees<D, U, FIN>(smem, b0, tb, lane_off, m);
+      finish(m, q, b0);
+    }
+    for (; q < t1; ++q) {
+      const uint32_t b0 = buf + (uint32_t)(q - t0) * tb;
+      uint32_t m[1];
+      walk_trees<D, 1, FIN>(smem, b0, tb, lane_off, m);
+      finish(m, q, b0);
     }
     wait_stage();
     __syncthreads();
@@ -630,21 +641,28 @@ static int launch_common(K kernel, int threads, int64_t n_wg, int lds_bytes, voi
   return (int)hipGetLastError();
 }
 
-template <int D>
-static int launch_perfect_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
-                            void *stream) {
+template <int D, bool FIN>
+static int launch_perfect_df(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                             void *stream) {
   const bool simple = a.K == 1 && a.groups == 1;
   const int threads = 64 * waves;
   if (a.out_leaf)
-    return launch_common(perfect_kernel<D, 4, true, false>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_kernel<D, 4, true, false, FIN>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 8) {
     if (simple)
-      return launch_common(perfect_kernel<D, 8, false, true>, threads, n_wg, lds_bytes, stream, a);
-    return launch_common(perfect_kernel<D, 8, false, false>, threads, n_wg, lds_bytes, stream, a);
+      return launch_common(perfect_kernel<D, 8, false, true, FIN>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_kernel<D, 8, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
   }
   if (simple)
-    return launch_common(perfect_kernel<D, 4, false, true>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(perfect_kernel<D, 4, false, false>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_kernel<D, 4, false, true, FIN>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(perfect_kernel<D, 4, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
+}
+
+template <int D>
+static int launch_perfect_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                            void *stream) {
+  return a.finite_thresholds ? launch_perfect_df<D, true>(a, waves, n_wg, lds_bytes, stream)
+                             : launch_perfect_df<D, false>(a, waves, n_wg, lds_bytes, stream);
 }
 
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

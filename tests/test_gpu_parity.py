@@ -108,10 +108,13 @@ def test_zero_rows_launches_nothing():
         torch.cuda.synchronize()
 
 
+FLT_MAX = np.float32(3.4028235e38)
+
+
 def _adversarial_rows(F, thr_values, rng, n=600):
     X = rng.standard_normal((n, F)).astype(np.float32)
-    specials = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 1.17549435e-38],
-                        np.float32)
+    specials = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 1.17549435e-38,
+                         FLT_MAX, -FLT_MAX], np.float32)
     m = rng.random(X.shape) < 0.15
     X[m] = specials[rng.integers(0, len(specials), m.sum())]
     t = np.asarray(thr_values, np.float32)
@@ -124,27 +127,45 @@ def _adversarial_rows(F, thr_values, rng, n=600):
     return X
 
 
+# thresholds on zero of either sign, denormals and the largest finite values; the second grid
+# adds infinite thresholds, which switch the perfect kernel from its sign-of-difference step
+# to the plain compare
+THRESHOLD_GRIDS = {
+    "finite": [-1.0, -1e-45, -0.0, 0.0, 1e-45, 0.5, 2.0, FLT_MAX, -FLT_MAX],
+    "with_inf": [-1.0, -0.0, 0.0, 1e-45, 0.5, np.inf, -np.inf, FLT_MAX],
+}
+
+
+@pytest.mark.parametrize("grid_name", list(THRESHOLD_GRIDS))
 @pytest.mark.parametrize("F", [3, 7, 28])
-def test_adversarial_values(F):
-    """NaN, +-inf, +-0, denormals, values on a threshold and one ulp either side."""
+def test_adversarial_values(F, grid_name, monkeypatch):
+    """NaN, +-inf, +-0, denormals, +-FLT_MAX, values on a threshold and one ulp either side."""
     rng = np.random.default_rng(100 + F)
-    grid = np.array([-1.0, -1e-45, 0.0, 1e-45, 0.5, 2.0], np.float32)
+    grid = np.array(THRESHOLD_GRIDS[grid_name], np.float32)
+    G = len(grid)
     trees = []
     for D in (2, 3, 4, 5):
         for _ in range(3):
             n_int = (1 << D) - 1
-            trees.append(perfect_tree_arrays(D, rng.integers(0, F, n_int), grid[rng.integers(0, 6, n_int)],
+            trees.append(perfect_tree_arrays(D, rng.integers(0, F, n_int), grid[rng.integers(0, G, n_int)],
                                              rng.standard_normal(1 << D).astype(np.float32)))
     ragged = concat_trees(trees, F)
-    perfect = concat_trees([perfect_tree_arrays(4, rng.integers(0, F, 15), grid[rng.integers(0, 6, 15)],
+    perfect = concat_trees([perfect_tree_arrays(4, rng.integers(0, F, 15), grid[rng.integers(0, G, 15)],
                                                 rng.standard_normal(16).astype(np.float32))
                             for _ in range(9)], F)
     X = _adversarial_rows(F, grid, rng)
     for model in (ragged, perfect):
-        with B.Forest(model) as f:
-            for k in KERNELS:
-                if supported(f, k):
-                    check_parity(model, X, k, f"adversarial F={F} {B.KERNEL_NAMES[k]}", forest=f)
+        for sign_step in ("on", "off"):
+            # the variable is read when the forest is created
+            if sign_step == "off":
+                monkeypatch.setenv("BRIDGER_NO_SIGN_STEP", "1")
+            else:
+                monkeypatch.delenv("BRIDGER_NO_SIGN_STEP", raising=False)
+            with B.Forest(model) as f:
+                for k in KERNELS:
+                    if supported(f, k):
+                        check_parity(model, X, k, f"adversarial F={F} {grid_name} sign_step={sign_step} "
+                                     f"{B.KERNEL_NAMES[k]}", forest=f)
 
 
 def test_unaligned_rows():
