@@ -85,8 +85,10 @@ struct bridger_forest {
   int32_t perfect_tree_bytes = 0;
   std::vector<uint8_t> perfect_blob;
   std::vector<uint8_t> perfect_trav;  // traversal copy: {threshold, feature * 4R}
+  std::vector<uint32_t> perfect_roots;  // per tree: the traversal copy's root record
   std::vector<int32_t> perfect_leaf_map;
   bool finite_thresholds = false;
+  bool fixed_chunks = true;           // allow the compile-time chunk kernel variants
   Plan perfect_plan{};
 
   // RAGGED
@@ -107,7 +109,7 @@ struct bridger_forest {
   void *d_class_begin = nullptr, *d_class_count = nullptr, *d_base = nullptr,
        *d_tree_order = nullptr;
   DevArrays d_perfect, d_ragged, d_direct;
-  void *d_perfect_trav = nullptr;
+  void *d_perfect_trav = nullptr, *d_perfect_roots = nullptr;
   double visits_per_row_est = 0;  // for the model: mean internal visits per row (all trees)
 };
 
@@ -198,7 +200,7 @@ void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *
                   const float *value) {
   const int n_int = (1 << D) - 1, n_leaf = 1 << D;
   const int leaf_off = 8 * (n_int + 1);   // 1-based heap: slots 1 .. 2^D - 1, slot 0 unused
-  const int tb = (leaf_off + 4 * n_leaf + 15) & ~15;
+  const int tb = perfect_tree_bytes(D);
   h->perfect_tree_bytes = tb;
   h->perfect_blob.assign((size_t)tb * h->n_trees, 0);
   h->perfect_leaf_map.assign((size_t)n_leaf * h->n_trees, -1);
@@ -251,6 +253,9 @@ void build_perfect_trav(bridger_forest *h) {
       std::memcpy(blk + 8 * m + 4, &f, 4);
     }
   }
+  h->perfect_roots.assign((size_t)2 * h->n_trees, 0);
+  for (int32_t k = 0; k < h->n_trees; ++k)
+    std::memcpy(&h->perfect_roots[2 * (size_t)k], h->perfect_trav.data() + (size_t)k * tb + 8, 8);
 }
 
 // Breadth-first record order with adjacent children; returns false if a tree cannot be
@@ -365,7 +370,7 @@ Plan choose_plan(const PlanInput &in) {
   };
   std::vector<Cand> cands;
   for (int pass = 0; pass < 2 && cands.empty(); ++pass) {
-    for (int W : {1, 2, 4, 8, 16}) {
+    for (int W : {1, 2, 4, 8}) {  // compute waves; each workgroup also has a staging wave
       if (force_waves && W != force_waves) continue;
       for (int R = 32; R <= 64 * W; R *= 2) {
         if (force_rows && R != force_rows) continue;
@@ -374,7 +379,7 @@ Plan choose_plan(const PlanInput &in) {
         const bool acc_lds = in.K > 1 || G > 1;
         const int64_t x_tile = (int64_t)in.F * R * 4;
         const int64_t acc_bytes = acc_lds ? (int64_t)in.K * G * R * 8 : 0;
-        for (int m = 1; m <= kMaxWavesPerCU / W; ++m) {  // workgroups per CU
+        for (int m = 1; m <= kMaxWavesPerCU / (W + 1); ++m) {  // workgroups per CU
           if (force_wg_per_cu && m != force_wg_per_cu) continue;
           if (pass == 0 && m * W < kMinWavesPerCU) continue;
           const int64_t budget = kLdsBytesPerCU / m - x_tile - acc_bytes;
@@ -390,6 +395,9 @@ Plan choose_plan(const PlanInput &in) {
               else continue;
             }
             ct = std::min(ct, ((in.n_trees + kTreesMultiple - 1) / kTreesMultiple) * kTreesMultiple);
+            // a power of two, so that the compile-time chunk variants of the kernel apply
+            if (ct >= kTreesMultiple)
+              while (ct & (ct - 1)) ct &= ct - 1;
             if (force_ct) {
               if (force_ct * (int64_t)in.tree_bytes > chunk) continue;
               ct = force_ct;
@@ -508,6 +516,7 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_base);
   free_dev(h->d_tree_order);
   free_dev(h->d_perfect_trav);
+  free_dev(h->d_perfect_roots);
   for (DevArrays *d : {&h->d_perfect, &h->d_ragged, &h->d_direct}) {
     free_dev(d->nodes);
     free_dev(d->tree_start);
@@ -526,6 +535,7 @@ bridger_status upload_all(bridger_forest *h) {
   if (h->perfect_ok) {
     if ((s = upload(&h->d_perfect.nodes, h->perfect_blob, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_perfect_trav, h->perfect_trav, 1024)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_perfect_roots, h->perfect_roots)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_perfect.leaf_map, h->perfect_leaf_map)) != BRIDGER_OK) return s;
   }
   if (h->ragged_ok) {
@@ -606,6 +616,7 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
     a.nodes = h->kernel_active == kPerfect ? (const uint8_t *)h->d_perfect_trav
                                            : (const uint8_t *)d.nodes;
     a.finite_thresholds = h->finite_thresholds ? 1 : 0;
+    a.roots = (const uint32_t *)h->d_perfect_roots;
     a.tree_start = (const int32_t *)d.tree_start;
     a.chunk_first = (const int32_t *)d.chunk_first;
     a.chunk_rec = (const int32_t *)d.chunk_rec;
@@ -622,7 +633,14 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
     a.acc_in_lds = p.acc_in_lds;
     a.ilp = p.ilp;
     const int64_t n_wg = (n_rows + p.rows_per_wg - 1) / p.rows_per_wg;
-    if (h->kernel_active == kPerfect)
+    const bool fixed = h->kernel_active == kPerfect && !out_leaf && h->K == 1 &&
+                       p.groups == 1 && p.waves <= 8 && h->finite_thresholds && p.ilp == 4 &&
+                       perfect_fixed_ok(h->perfect_depth, p.trees_per_chunk) &&
+                       p.chunk_bytes == p.trees_per_chunk * h->perfect_tree_bytes &&
+                       h->fixed_chunks;
+    if (fixed)
+      err = launch_perfect_fixed(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
+    else if (h->kernel_active == kPerfect)
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else
       err = launch_ragged(a, p.waves, n_wg, p.lds_bytes, stream);
@@ -726,6 +744,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     }
     h->visits_per_row_est = visits;
     h->finite_thresholds = env_int("BRIDGER_NO_SIGN_STEP", 0) == 0;
+    h->fixed_chunks = env_int("BRIDGER_NO_FIXED", 0) == 0;
     for (int64_t i = 0; i < h->n_nodes && h->finite_thresholds; ++i)
       if (left[i] != -1 && !std::isfinite(threshold[i])) h->finite_thresholds = false;
     h->all_perfect = all_perfect ? 1 : 0;

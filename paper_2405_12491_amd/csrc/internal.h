@@ -40,6 +40,17 @@ constexpr int kMaxRaggedFeatures = 0xFFFF;
 constexpr int kMaxClasses = 64;  // class sums of one 256-row block fit LDS in every kernel
 
 enum Kernel { kAuto = 0, kPerfect = 1, kRagged = 2, kDirect = 3, kGemm = 4 };
+
+// Bytes of one PERFECT tree block of depth D (records, then leaves; 16-byte multiple).
+constexpr int perfect_tree_bytes(int D) { return ((12 << D) + 15) & ~15; }
+
+// The PERFECT kernel has compile-time chunk variants (trees per chunk CT in 4..32, a power of
+// two; both chunk buffers addressable by the 16-bit offset field of an LDS instruction) for
+// one class, one lane group and finite thresholds.
+constexpr bool perfect_fixed_ok(int D, int CT) {
+  return D >= 2 && D <= 9 && (CT == 4 || CT == 8 || CT == 16 || CT == 32) &&
+         2 * CT * perfect_tree_bytes(D) <= 65536;
+}
 constexpr int kMaxGemmDepth = 4;
 constexpr int kMaxGemmFeatures = 64;
 
@@ -91,11 +102,14 @@ struct LaunchArgs {
   int32_t acc_in_lds;
   int32_t ilp;                 // PERFECT: trees walked at once per lane (4 or 8)
   int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)
+  const uint32_t *roots;       // PERFECT: per kernel tree the root's traversal record (2 words)
 };
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                    void *stream);
+int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                         void *stream);
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
 int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream);
 int launch_gemm(int depth, const LaunchArgs &a, int64_t n_wg, void *stream);

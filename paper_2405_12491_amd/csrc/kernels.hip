@@ -23,6 +23,8 @@
 #include <stdint.h>
 
 #include <map>
+#include <utility>
+#include <type_traits>
 #include <mutex>
 
 #include "internal.h"
@@ -54,6 +56,32 @@ __device__ __forceinline__ void stage_async(uint8_t *smem, uint32_t dst, const u
 }
 
 __device__ __forceinline__ void wait_stage() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Body of the staging wave that the chunked kernels add after their compute waves: it stages
+// chunk 0, then during chunk c the chunk c + 1 into the other buffer, and meets the compute
+// waves at each of their barriers (1 after the tile load, 1 per chunk, `tail` after the
+// loop).  The compute waves never issue direct global->LDS loads, so they never wait for
+// staging traffic; the barrier alone orders a chunk's arrival before its use.
+// chunk_src(c) -> {global source, bytes} of chunk c.
+template <class ChunkSrc>
+__device__ __forceinline__ void staging_wave(uint8_t *smem, int n_chunks, uint32_t chunk_bytes,
+                                             int lane, int tail, ChunkSrc chunk_src) {
+  {
+    const auto src = chunk_src(0);
+    stage_async(smem, 0, src.first, src.second, 0, lane, 1);
+    wait_stage();
+  }
+  __syncthreads();
+  for (int c = 0; c < n_chunks; ++c) {
+    if (c + 1 < n_chunks) {
+      const auto src = chunk_src(c + 1);
+      stage_async(smem, ((c + 1) & 1) ? chunk_bytes : 0u, src.first, src.second, 0, lane, 1);
+      wait_stage();
+    }
+    __syncthreads();
+  }
+  for (int i = 0; i < tail; ++i) __syncthreads();
+}
 
 // Load this lane's row into the feature-major LDS tile (zeros past the last row).  With
 // NAN_TO_INF a NaN feature is stored as +inf: against finite thresholds both compare false
@@ -201,12 +229,53 @@ __device__ __forceinline__ void walk_trees(const uint8_t *smem, uint32_t b0, uin
   }
 }
 
+// Same walk with the root records given as wave-uniform values (scalar registers): level 0
+// then needs only the feature gather.
+template <int D, int U>
+__device__ __forceinline__ void walk_trees_root(const uint8_t *smem, uint32_t b0, uint32_t tb,
+                                                uint32_t lane_off, const uint2 *root,
+                                                uint32_t (&m)[U]) {
+  {
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, root[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float diff = __uint_as_float(root[u].x) - xv[u];
+      m[u] = __builtin_amdgcn_alignbit(1u, __float_as_uint(diff), 31);
+    }
+  }
+#pragma unroll
+  for (int d = 1; d < D; ++d) {
+    uint2 rec[U];
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, (m[u] << 3) + b0 + (uint32_t)u * tb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float diff = __uint_as_float(rec[u].x) - xv[u];
+      m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
+    }
+  }
+}
+
 template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, waves = blockDim.x >> 6;
   const int R = a.rows_per_wg, G = a.groups;
+  const uint32_t tb = (uint32_t)a.tree_bytes;
+  const int T = a.n_trees, CT = a.trees_per_chunk;
+  if (tid >= G * R) {
+    staging_wave(smem, a.n_chunks, (uint32_t)a.chunk_bytes, tid & 63, (LEAVES || SIMPLE) ? 0 : 1,
+                 [&](int c) {
+                   const int n0 = c * CT, n1 = (n0 + CT < T) ? n0 + CT : T;
+                   return std::make_pair(a.nodes + (size_t)n0 * tb, (n1 - n0) * (int)tb);
+                 });
+    return;
+  }
   const int r = tid & (R - 1);
   // with R >= 64 a wave lies inside one lane group, so the group index (and every tree
   // address derived from it) is wave-uniform and lives in scalar registers
@@ -214,18 +283,11 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   const int64_t row = (int64_t)blockIdx.x * R + r;
   const bool row_ok = row < a.n_rows;
   const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
-  const uint32_t tb = (uint32_t)a.tree_bytes;
-  const int T = a.n_trees, CT = a.trees_per_chunk;
   // leaf j of a tree is at base + 8 * 2^D + 4j, i.e. base + 4m + 4 * 2^D for final slot m
   constexpr uint32_t kLeafOff = 4u << D;
   constexpr uint32_t kFirstLeaf = 1u << D;
 
-  {
-    const int t1 = CT < T ? CT : T;
-    stage_async(smem, 0, a.nodes, t1 * (int)tb, wave, lane, waves);
-  }
   if (g == 0) load_row_tile<FIN>(smem, a, r, row, row_ok);
-  wait_stage();
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -262,11 +324,6 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   for (int c = 0; c < a.n_chunks; ++c) {
     const int t0 = c * CT;
     const int t1 = (t0 + CT < T) ? t0 + CT : T;
-    if (c + 1 < a.n_chunks) {
-      const int n0 = t1, n1 = (n0 + CT < T) ? n0 + CT : T;
-      stage_async(smem, ((c + 1) & 1) ? (uint32_t)a.chunk_bytes : 0u, a.nodes + (size_t)n0 * tb,
-                  (n1 - n0) * (int)tb, wave, lane, waves);
-    }
     const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
     // whole groups of U trees, then (only when the chunk's tree count leaves one) a partial
     // group walked one tree at a time
@@ -283,7 +340,6 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
       walk_trees<D, 1, FIN>(smem, b0, tb, lane_off, m);
       finish(m, q, b0);
     }
-    wait_stage();
     __syncthreads();
   }
   if (LEAVES) return;
@@ -308,6 +364,96 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   }
 }
 
+// Compile-time chunk geometry for the common case (one class, one lane group, finite
+// thresholds): CT trees per chunk and the tree block size are constants and the chunk loop is
+// unrolled over the two buffers, so every tree's LDS base folds into the gathers' offset field
+// and a level's node address is a single shift.  A last chunk with fewer than CT trees is
+// walked with run-time bases.
+template <int D, int CT>
+__global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr int U = 4;
+  constexpr uint32_t TB = (uint32_t)perfect_tree_bytes(D);
+  constexpr uint32_t CB = (uint32_t)CT * TB;
+  constexpr uint32_t kLeafOff = 4u << D;
+  static_assert(perfect_fixed_ok(D, CT), "chunk geometry outside the offset field");
+  const int tid = threadIdx.x;
+  const int R = a.rows_per_wg;  // 64 lanes per compute wave, one row each
+  const int T = a.n_trees, n_chunks = a.n_chunks;
+
+  if (tid >= R) {
+    staging_wave(smem, n_chunks, CB, tid & 63, 0, [&](int c) {
+      const int n0 = c * CT, n1 = (n0 + CT < T) ? n0 + CT : T;
+      return std::make_pair(a.nodes + (size_t)n0 * TB, (n1 - n0) * (int)TB);
+    });
+    return;
+  }
+
+  const int64_t row = (int64_t)blockIdx.x * R + tid;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)tid;
+  load_row_tile<true>(smem, a, tid, row, row_ok);
+  __syncthreads();
+
+  double acc = a.aggregate == 0 ? (double)a.base[0] : 0.0;
+  auto chunk = [&](auto buf_tag, int c) {
+    constexpr uint32_t BUF = decltype(buf_tag)::value ? CB : 0u;
+    const int t0 = c * CT;
+    if (t0 + CT <= T) {
+      // the chunk's root records, wave-uniform: scalar loads through the constant address space
+      uint2 root[CT];
+      typedef __attribute__((address_space(4))) const uint64_t const_u64;
+      const_u64 *rt = (const_u64 *)(uintptr_t)a.roots + t0;
+#pragma unroll
+      for (int j = 0; j < CT; ++j) {
+        const uint64_t v = rt[j];
+        root[j] = make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+      }
+#pragma unroll
+      for (int j = 0; j < CT / U; ++j) {
+        uint32_t m[U];
+        walk_trees_root<D, U>(smem, BUF + (uint32_t)(j * U) * TB, TB, lane_off, root + j * U, m);
+        float lv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          lv[u] = lds_f32(smem, (m[u] << 2) + BUF + (uint32_t)(j * U + u) * TB + kLeafOff);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc += (double)lv[u];
+      }
+    } else {
+      int q = t0;
+      for (; q + U <= T; q += U) {
+        const uint32_t b0 = BUF + (uint32_t)(q - t0) * TB;
+        uint32_t m[U];
+        walk_trees<D, U, true>(smem, b0, TB, lane_off, m);
+        float lv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) lv[u] = lds_f32(smem, (m[u] << 2) + b0 + (uint32_t)u * TB + kLeafOff);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc += (double)lv[u];
+      }
+      for (; q < T; ++q) {
+        const uint32_t b0 = BUF + (uint32_t)(q - t0) * TB;
+        uint32_t m[1];
+        walk_trees<D, 1, true>(smem, b0, TB, lane_off, m);
+        acc += (double)lds_f32(smem, (m[0] << 2) + b0 + kLeafOff);
+      }
+    }
+    __syncthreads();
+  };
+  int c = 0;
+  for (; c + 2 <= n_chunks; c += 2) {
+    chunk(std::integral_constant<int, 0>{}, c);
+    chunk(std::integral_constant<int, 1>{}, c + 1);
+  }
+  if (c < n_chunks) chunk(std::integral_constant<int, 0>{}, c);
+  if (row_ok) {
+    double z = acc;
+    if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
+    a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
+  }
+}
+
 // ======================================================================== RAGGED
 // Any tree shape.  Each lane runs a state machine over its group's trees of the chunk: at an
 // internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
@@ -317,8 +463,15 @@ template <bool LEAVES, bool SIMPLE>
 __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, waves = blockDim.x >> 6;
   const int R = a.rows_per_wg, G = a.groups;
+  if (tid >= G * R) {
+    staging_wave(smem, a.n_chunks, (uint32_t)a.chunk_bytes, tid & 63,
+                 (LEAVES || (SIMPLE && G == 1)) ? 0 : 1, [&](int c) {
+                   return std::make_pair(a.nodes + 8 * (size_t)a.chunk_rec[c],
+                                         8 * (a.chunk_rec[c + 1] - a.chunk_rec[c]));
+                 });
+    return;
+  }
   const int r = tid & (R - 1);
   const int g = tid / R;
   const int64_t row = (int64_t)blockIdx.x * R + r;
@@ -327,10 +480,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   const int shift = a.log2_row_bytes;
   const int T = a.n_trees;
 
-  stage_async(smem, 0, a.nodes + 8 * (size_t)a.chunk_rec[0],
-              8 * (a.chunk_rec[1] - a.chunk_rec[0]), wave, lane, waves);
   if (g == 0) load_row_tile(smem, a, r, row, row_ok);
-  wait_stage();
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -341,10 +491,6 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
 
   for (int c = 0; c < a.n_chunks; ++c) {
-    if (c + 1 < a.n_chunks)
-      stage_async(smem, ((c + 1) & 1) ? (uint32_t)a.chunk_bytes : 0u,
-                  a.nodes + 8 * (size_t)a.chunk_rec[c + 1],
-                  8 * (a.chunk_rec[c + 2] - a.chunk_rec[c + 1]), wave, lane, waves);
     const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
     const int ct0 = a.chunk_first[c], ct1 = a.chunk_first[c + 1];
     const int nt = ct1 - ct0;
@@ -377,7 +523,6 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
       const uint32_t step = rel + (right ? 1u : 0u);
       addr += 8u * (step > 1u ? step : 1u);
     }
-    wait_stage();
     __syncthreads();
   }
   if (LEAVES) return;
@@ -645,7 +790,7 @@ template <int D, bool FIN>
 static int launch_perfect_df(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                              void *stream) {
   const bool simple = a.K == 1 && a.groups == 1;
-  const int threads = 64 * waves;
+  const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(perfect_kernel<D, 4, true, false, FIN>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 8) {
@@ -682,9 +827,45 @@ int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int 
   }
 }
 
+template <int D, int CT>
+static int launch_fixed_dc(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                           void *stream) {
+  if constexpr (perfect_fixed_ok(D, CT))
+    return launch_common(perfect_fixed_kernel<D, CT>, 64 * (waves + 1), n_wg, lds_bytes, stream, a);
+  else
+    return (int)hipErrorInvalidValue;
+}
+
+template <int D>
+static int launch_fixed_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                          void *stream) {
+  switch (a.trees_per_chunk) {
+    case 4: return launch_fixed_dc<D, 4>(a, waves, n_wg, lds_bytes, stream);
+    case 8: return launch_fixed_dc<D, 8>(a, waves, n_wg, lds_bytes, stream);
+    case 16: return launch_fixed_dc<D, 16>(a, waves, n_wg, lds_bytes, stream);
+    case 32: return launch_fixed_dc<D, 32>(a, waves, n_wg, lds_bytes, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                         void *stream) {
+  switch (depth) {
+    case 2: return launch_fixed_d<2>(a, waves, n_wg, lds_bytes, stream);
+    case 3: return launch_fixed_d<3>(a, waves, n_wg, lds_bytes, stream);
+    case 4: return launch_fixed_d<4>(a, waves, n_wg, lds_bytes, stream);
+    case 5: return launch_fixed_d<5>(a, waves, n_wg, lds_bytes, stream);
+    case 6: return launch_fixed_d<6>(a, waves, n_wg, lds_bytes, stream);
+    case 7: return launch_fixed_d<7>(a, waves, n_wg, lds_bytes, stream);
+    case 8: return launch_fixed_d<8>(a, waves, n_wg, lds_bytes, stream);
+    case 9: return launch_fixed_d<9>(a, waves, n_wg, lds_bytes, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {
   const bool simple = a.K == 1;
-  const int threads = 64 * waves;
+  const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf) return launch_common(ragged_kernel<true, false>, threads, n_wg, lds_bytes, stream, a);
   if (simple) return launch_common(ragged_kernel<false, true>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(ragged_kernel<false, false>, threads, n_wg, lds_bytes, stream, a);
