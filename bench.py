@@ -34,23 +34,32 @@ HBM_PEAK_BYTES_PER_S = 8.0e12
 
 # HBM bytes per launch of the default workload's kernel from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE runs (KiB per dispatch), each scaled by what the same counter reads for a plain
-# copy of known size (profiles/perfect_kernel_gbdt_d6_1Mx28_500trees.md).  Valid only for the
-# kernel source they were measured on; any other source reports traffic as null.
+# copy of known size (profiles/perfect_fixed_kernel_gbdt_d6_1Mx28_500trees.md).  Valid only for
+# the kernel sources they were measured on (KERNEL_SOURCES); any other source reports traffic
+# as null.
+KERNEL_SOURCES = ["perfect_fixed.hip", "perfect_walk.h", "kernel_common.h", "internal.h"]
 MEASURED_TRAFFIC = {
-    "kernel_sha256_prefix": "74a4eb672ce875d2",
+    "kernel_sha256_prefix": "68747848f95752ef",
     "workload": "gbdt_d6",
-    "fetch_kib": 57307.5, "write_kib": 3906.25,
-    "copy_bytes": 112_000_000, "copy_fetch_kib": 54701.9375, "copy_write_kib": 109375.0,
+    "fetch_kib": 57336.171875, "write_kib": 3906.25,
+    "copy_bytes": 112_000_000, "copy_fetch_kib": 54702.15625, "copy_write_kib": 109375.0,
 }
 
 
-def measured_traffic(workload: str, n_rows: int):
+def kernel_sources_sha() -> str:
     import hashlib
-    src = os.path.join(ROOT, "paper_2405_12491_amd", "csrc", "kernels.hip")
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2405_12491_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, n_rows: int):
     m = MEASURED_TRAFFIC
-    if workload != m["workload"] or n_rows != 1_000_000:
+    if workload != m["workload"] or n_rows != 1_000_000 or m["fetch_kib"] is None:
         return None
-    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != m["kernel_sha256_prefix"]:
+    if kernel_sources_sha() != m["kernel_sha256_prefix"]:
         return None
     true_kib = m["copy_bytes"] / 1024.0
     fetch = m["fetch_kib"] * (true_kib / m["copy_fetch_kib"]) * 1024.0
@@ -61,8 +70,10 @@ def measured_traffic(workload: str, n_rows: int):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
+    # the GPU clock ramps up over the first ~50 ms of back-to-back launches; the default warmup
+    # covers it so that the timed launches run at the steady clock
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--workload", default="gbdt_d6")
     p.add_argument("--rows", type=int, default=None, help="override the workload's row count")
     p.add_argument("--kernel", default="auto", choices=["auto", "perfect", "ragged", "direct", "gemm"])

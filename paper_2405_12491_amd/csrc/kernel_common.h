@@ -1,0 +1,222 @@
+// kernel_common.h -- device helpers shared by the gfx950 kernels (LDS access, chunk staging,
+// the feature tile, class bookkeeping, the link functions) and the launch helper.
+//
+// One fused kernel per launch runs the whole lowered pipeline of a tree model (Sec. 4.2 and
+// Table 4): gather the split feature of the current node (take/gather), compare it with the
+// threshold (less_equal), pick the child (where), descend (loop/while), fetch the leaf and
+// aggregate over trees (sum/mean), then apply the link function (exp/add/divide/max).  No
+// intermediate tensor leaves the chip (the cross-domain fusion idea of Sec. 4.3 applied to
+// one model).
+//
+// Work decomposition of the chunked kernels (the "tile", "split" and "parallel" schedules of
+// Table 5, sized by the Eq. 1 planner on the host):
+//   * a workgroup owns R consecutive rows; their features are copied once from HBM into an
+//     LDS tile stored feature-major (x of feature f, row r at byte 4*(f*R + r)).  Lane r of
+//     every 32-lane half-wave then reads a different LDS bank whatever feature it needs, so
+//     the per-lane feature gather is conflict-free;
+//   * the trees stream through two LDS chunk buffers.  One extra wave per workgroup does
+//     nothing but stage: while the compute waves traverse chunk c it loads chunk c + 1 into the
+//     other buffer with direct global->LDS loads; one barrier per chunk;
+//   * with 64*waves == R every lane owns one row and adds its leaves in ascending tree order
+//     (bit-identical to a sequential sum); with 64*waves > R the G = 64*waves/R lane groups
+//     split the trees and their per-class partial sums are added in group order at the end.
+// Sums are kept in double precision; the output is rounded once to float.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <map>
+#include <mutex>
+#include <type_traits>
+#include <utility>
+
+#include "internal.h"
+
+namespace bridger {
+
+typedef __attribute__((address_space(3))) uint8_t lds_byte;
+
+// The kernels declare no static LDS, so dynamic LDS starts at LDS address 0 and a byte
+// offset into it is directly an LDS address (no base add on every access).
+__device__ __forceinline__ float lds_f32(const uint8_t *, uint32_t addr) {
+  return *(const __attribute__((address_space(3))) float *)(uintptr_t)addr;
+}
+__device__ __forceinline__ uint2 lds_u64(const uint8_t *, uint32_t addr) {
+  const uint64_t v = *(const __attribute__((address_space(3))) uint64_t *)(uintptr_t)addr;
+  return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+// Stage `bytes` (multiple of 16) from global memory into LDS at byte offset `dst` with
+// direct global->LDS loads: each wave instruction moves 1 KB (64 lanes x 16 bytes).
+__device__ __forceinline__ void stage_async(uint8_t *smem, uint32_t dst, const uint8_t *src,
+                                            int bytes, int wave, int lane, int waves) {
+  for (int off = wave * 1024; off < bytes; off += waves * 1024) {
+    if (off + lane * 16 < bytes) {
+      __builtin_amdgcn_global_load_lds(
+          (const void *)(src + off + lane * 16),
+          (__attribute__((address_space(3))) void *)((lds_byte *)smem + dst + off), 16, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void wait_stage() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Body of the staging wave that the chunked kernels add after their compute waves: it stages
+// chunk 0, then during chunk c the chunk c + 1 into the other buffer, and meets the compute
+// waves at each of their barriers (1 after the tile load, 1 per chunk, `tail` after the
+// loop).  The compute waves never issue direct global->LDS loads, so they never wait for
+// staging traffic; the barrier alone orders a chunk's arrival before its use.
+// chunk_src(c) -> {global source, bytes} of chunk c.
+template <class ChunkSrc>
+__device__ __forceinline__ void staging_wave(uint8_t *smem, int n_chunks, uint32_t chunk_bytes,
+                                             int lane, int tail, ChunkSrc chunk_src) {
+  {
+    const auto src = chunk_src(0);
+    stage_async(smem, 0, src.first, src.second, 0, lane, 1);
+    wait_stage();
+  }
+  __syncthreads();
+  for (int c = 0; c < n_chunks; ++c) {
+    if (c + 1 < n_chunks) {
+      const auto src = chunk_src(c + 1);
+      stage_async(smem, ((c + 1) & 1) ? chunk_bytes : 0u, src.first, src.second, 0, lane, 1);
+      wait_stage();
+    }
+    __syncthreads();
+  }
+  for (int i = 0; i < tail; ++i) __syncthreads();
+}
+
+// Load this lane's row into the feature-major LDS tile (zeros past the last row).  With
+// NAN_TO_INF a NaN feature is stored as +inf: against finite thresholds both compare false
+// (x <= t), so every split sends them the same way.
+template <bool NAN_TO_INF = false>
+__device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a, int r,
+                                              int64_t row, bool row_ok) {
+  float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
+  const int R = a.rows_per_wg;
+  auto put = [&](int f, float v) {
+    if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
+    xt[f * R + r] = v;
+  };
+  if (!row_ok) {
+    for (int f = 0; f < a.F; ++f) xt[f * R + r] = 0.0f;
+    return;
+  }
+  const float *xr = a.X + row * (int64_t)a.F;
+  if (a.x_vec4) {
+    const float4 *x4 = reinterpret_cast<const float4 *>(xr);
+    const int n4 = a.F >> 2;
+    int i = 0;
+    for (; i + 2 <= n4; i += 2) {
+      float4 v0 = x4[i], v1 = x4[i + 1];
+      put(4 * i + 0, v0.x);
+      put(4 * i + 1, v0.y);
+      put(4 * i + 2, v0.z);
+      put(4 * i + 3, v0.w);
+      put(4 * i + 4, v1.x);
+      put(4 * i + 5, v1.y);
+      put(4 * i + 6, v1.z);
+      put(4 * i + 7, v1.w);
+    }
+    for (; i < n4; ++i) {
+      float4 v = x4[i];
+      put(4 * i + 0, v.x);
+      put(4 * i + 1, v.y);
+      put(4 * i + 2, v.z);
+      put(4 * i + 3, v.w);
+    }
+  } else {
+    for (int f = 0; f < a.F; ++f) put(f, xr[f]);
+  }
+}
+
+__device__ __forceinline__ double sigmoid_d(double z) {
+  if (z >= 0.0) return 1.0 / (1.0 + exp(-z));
+  const double e = exp(z);
+  return e / (1.0 + e);
+}
+
+// Finish class values z[0..K) held in LDS (stride `stride` doubles) and store the row.
+__device__ void finalize_store(const LaunchArgs &a, double *z, int stride, int64_t row) {
+  const int K = a.K;
+  for (int k = 0; k < K; ++k) {
+    double v = z[k * stride];
+    if (a.aggregate == 1) v = (double)a.base[k] + v / (double)a.class_count[k];
+    z[k * stride] = v;
+  }
+  float *o = a.out + row * (int64_t)K;
+  if (a.transform == 1) {
+    o[0] = (float)sigmoid_d(z[0]);
+  } else if (a.transform == 2) {
+    double m = z[0];
+    for (int k = 1; k < K; ++k) m = z[k * stride] > m ? z[k * stride] : m;
+    double s = 0.0;
+    for (int k = 0; k < K; ++k) {
+      const double e = exp(z[k * stride] - m);
+      z[k * stride] = e;
+      s += e;
+    }
+    for (int k = 0; k < K; ++k) o[k] = (float)(z[k * stride] / s);
+  } else {
+    for (int k = 0; k < K; ++k) o[k] = (float)z[k * stride];
+  }
+}
+
+// Per-lane class bookkeeping for forests with several classes or several tree groups.
+struct ClassAcc {
+  double acc;
+  int k;       // class being accumulated
+  int next_b;  // first kernel tree of class k+1
+};
+
+__device__ __forceinline__ double class_init(const LaunchArgs &a, int k, bool first_group) {
+  return (a.aggregate == 0 && first_group) ? (double)a.base[k] : 0.0;
+}
+
+__device__ __forceinline__ void class_advance(const LaunchArgs &a, ClassAcc &c, int t,
+                                              double *acc_lds, int slot_stride, bool first_group) {
+  while (t >= c.next_b) {
+    acc_lds[c.k * slot_stride] = c.acc;
+    c.k += 1;
+    c.acc = class_init(a, c.k, first_group);
+    c.next_b = a.class_begin[c.k + 1];
+  }
+}
+
+__device__ __forceinline__ void class_flush_all(const LaunchArgs &a, ClassAcc &c,
+                                                double *acc_lds, int slot_stride,
+                                                bool first_group) {
+  while (c.k < a.K) {
+    acc_lds[c.k * slot_stride] = c.acc;
+    c.k += 1;
+    if (c.k < a.K) c.acc = class_init(a, c.k, first_group);
+  }
+}
+
+// ====================================================================== launchers
+// Raise a kernel's dynamic-LDS limit once per (kernel, device) to the largest size used.
+static inline int ensure_lds_limit(const void *kernel, int lds_bytes) {
+  static std::mutex mu;
+  static std::map<std::pair<const void *, int>, int> limits;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  int &cur = limits[{kernel, dev}];
+  if (lds_bytes <= cur) return 0;
+  hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+  if (e != hipSuccess) return (int)e;
+  cur = lds_bytes;
+  return 0;
+}
+
+template <class K>
+static inline int launch_common(K kernel, int threads, int64_t n_wg, int lds_bytes, void *stream,
+                         const LaunchArgs &a) {
+  const int e = ensure_lds_limit((const void *)kernel, lds_bytes);
+  if (e != 0) return e;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)n_wg), dim3(threads), lds_bytes,
+                     (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+}  // namespace bridger

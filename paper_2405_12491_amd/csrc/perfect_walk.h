@@ -1,0 +1,78 @@
+// perfect_walk.h -- the per-lane walk of perfect trees shared by the PERFECT kernels.
+#pragma once
+#include "kernel_common.h"
+
+namespace bridger {
+
+// ======================================================================= PERFECT
+// Trees are perfect of depth D (layout in internal.h).  The kernel reads the traversal copy
+// of the layout, whose records hold {threshold, byte offset of the feature's row in the LDS
+// tile} so that the feature gather needs one add.  A lane's state per tree is its 1-based heap
+// slot m (root 1, children 2m and 2m + 1); each lane walks U trees at once, so U independent
+// LDS reads are in flight per lane.  One level of one tree:
+//   rec = LDS[base + 8m]  (64-bit gather),  x = LDS[rec.offset + lane's row]  (32-bit gather),
+//   m   = 2m + (x <= rec.threshold ? 0 : 1).
+// With only finite thresholds (FIN) the step is computed as the sign bit of threshold - x
+// shifted into m by one funnel shift, which needs no compare mask: for finite t and x != NaN
+// the IEEE difference t - x is +0 when x == t and otherwise nonzero with the sign of t - x
+// (denormals are kept; ties and -0 are handled by storing thresholds of zero as +0), it is
+// -inf for x = +inf and +inf for x = -inf, and a NaN feature is stored as +inf, which every
+// finite threshold sends right as the compare would.  After D levels m - 2^D is the leaf.
+template <int D, int U, bool FIN>
+__device__ __forceinline__ void walk_trees(const uint8_t *smem, uint32_t b0, uint32_t tb,
+                                           uint32_t lane_off, uint32_t (&m)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) m[u] = 1u;
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    uint2 rec[U];
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, (m[u] << 3) + b0 + (uint32_t)u * tb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (FIN) {
+        const float diff = __uint_as_float(rec[u].x) - xv[u];
+        m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
+      } else {
+        m[u] = 2u * m[u] + ((xv[u] <= __uint_as_float(rec[u].x)) ? 0u : 1u);
+      }
+    }
+  }
+}
+
+// Same walk with the root records given as wave-uniform values (scalar registers): level 0
+// then needs only the feature gather.
+template <int D, int U>
+__device__ __forceinline__ void walk_trees_root(const uint8_t *smem, uint32_t b0, uint32_t tb,
+                                                uint32_t lane_off, const uint2 *root,
+                                                uint32_t (&m)[U]) {
+  {
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, root[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float diff = __uint_as_float(root[u].x) - xv[u];
+      m[u] = __builtin_amdgcn_alignbit(1u, __float_as_uint(diff), 31);
+    }
+  }
+#pragma unroll
+  for (int d = 1; d < D; ++d) {
+    uint2 rec[U];
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, (m[u] << 3) + b0 + (uint32_t)u * tb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float diff = __uint_as_float(rec[u].x) - xv[u];
+      m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
+    }
+  }
+}
+
+}  // namespace bridger

@@ -1,0 +1,112 @@
+// ragged.hip -- gfx950 kernel for forests of trees of any shape, staged through LDS.
+#include "kernel_common.h"
+
+namespace bridger {
+
+// ======================================================================== RAGGED
+// Any tree shape.  Each lane runs a state machine over its group's trees of the chunk: at an
+// internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
+// adds the value and jumps to the next tree's root.  Lanes never wait for each other inside
+// a chunk, so a short path in one tree is not padded to the wave's longest path.
+template <bool LEAVES, bool SIMPLE>
+__global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x;
+  const int R = a.rows_per_wg, G = a.groups;
+  if (tid >= G * R) {
+    staging_wave(smem, a.n_chunks, (uint32_t)a.chunk_bytes, tid & 63,
+                 (LEAVES || (SIMPLE && G == 1)) ? 0 : 1, [&](int c) {
+                   return std::make_pair(a.nodes + 8 * (size_t)a.chunk_rec[c],
+                                         8 * (a.chunk_rec[c + 1] - a.chunk_rec[c]));
+                 });
+    return;
+  }
+  const int r = tid & (R - 1);
+  const int g = tid / R;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const int shift = a.log2_row_bytes;
+  const int T = a.n_trees;
+
+  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  __syncthreads();
+
+  double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
+  const int slot_stride = G * R;
+  ClassAcc ca;
+  ca.k = 0;
+  ca.acc = class_init(a, 0, g == 0);
+  ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+
+  for (int c = 0; c < a.n_chunks; ++c) {
+    const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
+    const int ct0 = a.chunk_first[c], ct1 = a.chunk_first[c + 1];
+    const int nt = ct1 - ct0;
+    const int ga = ct0 + (int)(((int64_t)nt * g) / G);
+    const int gb = ct0 + (int)(((int64_t)nt * (g + 1)) / G);
+    const int rec0 = a.chunk_rec[c];
+    uint32_t addr = buf + 8u * (uint32_t)(a.tree_start[ga] - rec0);
+    const uint32_t end = buf + 8u * (uint32_t)(a.tree_start[gb] - rec0);
+    int t = ga;
+    while (addr < end) {
+      const uint2 rec = lds_u64(smem, addr);
+      const uint32_t meta = rec.y;
+      const float xv = lds_f32(smem, ((meta >> 16) << shift) + lane_off);
+      const bool leaf = (meta & (uint32_t)kLeafFlag) != 0;
+      const uint32_t rel = meta & (uint32_t)kMaxRel;
+      const bool right = !(xv <= __uint_as_float(rec.x)) && !leaf;
+      if (leaf) {
+        if (LEAVES) {
+          if (row_ok)
+            a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
+                a.leaf_map[rec0 + (int)((addr - buf) >> 3)];
+        } else {
+          if (!SIMPLE) class_advance(a, ca, t, acc_lds, slot_stride, g == 0);
+          ca.acc += (double)__uint_as_float(rec.x);
+        }
+        ++t;
+      }
+      // a valid record always moves forward (left_rel >= 1, next_rel >= 1); the max keeps the
+      // loop finite even on a corrupted record
+      const uint32_t step = rel + (right ? 1u : 0u);
+      addr += 8u * (step > 1u ? step : 1u);
+    }
+    __syncthreads();
+  }
+  if (LEAVES) return;
+  if (SIMPLE && G == 1) {
+    if (row_ok) {
+      double z = ca.acc;
+      if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
+      a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
+    }
+    return;
+  }
+  if (SIMPLE) {
+    acc_lds[0] = ca.acc;
+  } else {
+    class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  }
+  __syncthreads();
+  if (g == 0) {
+    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
+    for (int k = 0; k < a.K; ++k) {
+      double s = z[k * slot_stride];
+      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
+      z[k * slot_stride] = s;
+    }
+    if (row_ok) finalize_store(a, z, slot_stride, row);
+  }
+}
+
+// ---------------------------------------------------------------------- launchers
+int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {
+  const bool simple = a.K == 1;
+  const int threads = 64 * (waves + 1);  // + the staging wave
+  if (a.out_leaf) return launch_common(ragged_kernel<true, false>, threads, n_wg, lds_bytes, stream, a);
+  if (simple) return launch_common(ragged_kernel<false, true>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_kernel<false, false>, threads, n_wg, lds_bytes, stream, a);
+}
+
+}  // namespace bridger
