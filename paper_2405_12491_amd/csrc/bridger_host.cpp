@@ -410,8 +410,10 @@ Plan choose_plan(const PlanInput &in) {
             if (chunk < in.tree_bytes) continue;
             chunk &= ~int64_t(1023);
             if (chunk < in.tree_bytes) continue;
-            // lane groups split a chunk's trees: want a couple of trees per group on average
-            if (G > 1 && chunk < 2.0 * G * in.forest_bytes / in.n_trees) continue;
+            // lane groups split a chunk's trees by count: want about one tree per group at
+            // least (a walk costs its path length, not the tree's size, so equal counts
+            // balance the groups)
+            if (G > 1 && chunk < 0.8 * G * in.forest_bytes / in.n_trees) continue;
             n_chunks = (int)std::ceil(in.forest_bytes / (0.9 * chunk));
           }
           const int64_t lds = 2 * chunk + x_tile + acc_bytes;
@@ -449,10 +451,11 @@ Plan choose_plan(const PlanInput &in) {
   if (cands.empty()) return best;  // infeasible: waves == 0
   double t_min = 1e300;
   for (const Cand &c : cands) t_min = std::min(t_min, c.p.est_seconds);
-  // The model resolves a few percent; among plans within 2% of the fastest prefer one lane
-  // group (each lane walks every tree of its row: no split of a chunk's trees and no partial
-  // sums), then more resident waves (latency hiding), then two or more workgroups per CU
-  // (one workgroup's barrier and tail overlap another's work), then fewer chunks.
+  // The model resolves a few percent; among plans within 2% of the fastest prefer enough
+  // resident waves to keep every SIMD issuing, then one lane group (each lane walks every
+  // tree of its row: no split of a chunk's trees and no partial sums), then more resident
+  // waves (latency hiding), then two or more workgroups per CU (one workgroup's barrier and
+  // tail overlap another's work), then fewer chunks.
   const Cand *pick = nullptr;
   const bool log = env_int("BRIDGER_LOG", 0) != 0;
   for (const Cand &c : cands) {
@@ -463,8 +466,11 @@ Plan choose_plan(const PlanInput &in) {
                    c.p.est_seconds > 1.02 * t_min ? "" : "  (tie)");
     if (c.p.est_seconds > 1.02 * t_min) continue;
     if (!pick) { pick = &c; continue; }
+    // a CU issues from its four SIMDs: below two compute waves per SIMD, more waves come
+    // before a single lane group
     auto key = [](const Cand &x) {
-      return std::make_tuple(x.single, x.waves_cu, x.overlap, -x.p.n_chunks);
+      return std::make_tuple(std::min(x.waves_cu, kMinWavesPerCU), x.single, x.waves_cu,
+                             x.overlap, -x.p.n_chunks);
     };
     if (key(c) > key(*pick)) pick = &c;
   }
