@@ -43,6 +43,7 @@ constexpr double kHbmBytesPerSec = 5.0e12;
 constexpr double kL2BytesPerSec = 30.0e12;
 constexpr double kLdsInstrPerSec = 0.44 * 256 * 2.4e9;
 constexpr int kMaxWavesPerCU = 32;
+constexpr double kL2BytesPerXcd = 4.0 * 1024 * 1024;
 constexpr int kMinWavesPerCU = 8;
 
 int env_int(const char *name, int dflt) {
@@ -357,8 +358,13 @@ struct PlanInput {
 };
 
 Plan choose_plan(const PlanInput &in) {
-  const int ilp = env_int("BRIDGER_ILP", 4) == 8 ? 8 : 4;  // trees walked at once per lane
-  const int kTreesMultiple = ilp;
+  // trees walked at once per lane (PERFECT): 4 unless the LDS only fits fewer trees per lane
+  // group; forced with BRIDGER_ILP
+  const int force_ilp = env_int("BRIDGER_ILP", 0);
+  std::vector<int> ilps;
+  if (force_ilp == 1 || force_ilp == 2 || force_ilp == 4) ilps = {force_ilp};
+  else if (in.perfect) ilps = {4, 2, 1};
+  else ilps = {4};
   const int force_waves = env_int("BRIDGER_WAVES", 0);
   const int force_rows = env_int("BRIDGER_ROWS", 0);
   const int force_ct = env_int("BRIDGER_CHUNK_TREES", 0);
@@ -370,6 +376,8 @@ Plan choose_plan(const PlanInput &in) {
   };
   std::vector<Cand> cands;
   for (int pass = 0; pass < 2 && cands.empty(); ++pass) {
+   for (const int ilp : ilps) {
+    const int kTreesMultiple = ilp;
     for (int W : {1, 2, 4, 8}) {  // compute waves; each workgroup also has a staging wave
       if (force_waves && W != force_waves) continue;
       for (int R = 32; R <= 64 * W; R *= 2) {
@@ -424,7 +432,7 @@ Plan choose_plan(const PlanInput &in) {
           const double lds_instr =
               (double)n / 64.0 * (2.0 * in.visits_per_row + in.n_trees) +
               n_wg * (in.forest_bytes / 1024.0);
-          Cand c;
+          Cand c{};
           c.p.waves = W;
           c.p.rows_per_wg = R;
           c.p.groups = G;
@@ -440,12 +448,14 @@ Plan choose_plan(const PlanInput &in) {
           c.p.est_seconds = std::max({hbm / kHbmBytesPerSec, stage / kL2BytesPerSec,
                                       lds_instr / kLdsInstrPerSec});
           c.waves_cu = m * W;
+          c.p.waves_per_cu = m * W;
           c.single = G == 1;
           c.overlap = m >= 2;
           cands.push_back(c);
         }
       }
     }
+   }
   }
   Plan best{};
   if (cands.empty()) return best;  // infeasible: waves == 0
@@ -453,15 +463,15 @@ Plan choose_plan(const PlanInput &in) {
   for (const Cand &c : cands) t_min = std::min(t_min, c.p.est_seconds);
   // The model resolves a few percent; among plans within 2% of the fastest prefer enough
   // resident waves to keep every SIMD issuing, then one lane group (each lane walks every
-  // tree of its row: no split of a chunk's trees and no partial sums), then more resident
-  // waves (latency hiding), then two or more workgroups per CU (one workgroup's barrier and
-  // tail overlap another's work), then fewer chunks.
+  // tree of its row: no split of a chunk's trees and no partial sums), then more trees per
+  // lane, then more resident waves (latency hiding), then two or more workgroups per CU (one
+  // workgroup's barrier and tail overlap another's work), then fewer chunks.
   const Cand *pick = nullptr;
   const bool log = env_int("BRIDGER_LOG", 0) != 0;
   for (const Cand &c : cands) {
     if (log)
-      std::fprintf(stderr, "[bridger plan] W=%d R=%d G=%d waves/CU=%d chunk=%d ct=%d chunks=%d lds=%d est=%.1fus%s\n",
-                   c.p.waves, c.p.rows_per_wg, c.p.groups, c.waves_cu, c.p.chunk_bytes,
+      std::fprintf(stderr, "[bridger plan] W=%d R=%d G=%d U=%d waves/CU=%d chunk=%d ct=%d chunks=%d lds=%d est=%.1fus%s\n",
+                   c.p.waves, c.p.rows_per_wg, c.p.groups, c.p.ilp, c.waves_cu, c.p.chunk_bytes,
                    c.p.trees_per_chunk, c.p.n_chunks, c.p.lds_bytes, c.p.est_seconds * 1e6,
                    c.p.est_seconds > 1.02 * t_min ? "" : "  (tie)");
     if (c.p.est_seconds > 1.02 * t_min) continue;
@@ -469,12 +479,47 @@ Plan choose_plan(const PlanInput &in) {
     // a CU issues from its four SIMDs: below two compute waves per SIMD, more waves come
     // before a single lane group
     auto key = [](const Cand &x) {
-      return std::make_tuple(std::min(x.waves_cu, kMinWavesPerCU), x.single, x.waves_cu,
-                             x.overlap, -x.p.n_chunks);
+      return std::make_tuple(std::min(x.waves_cu, kMinWavesPerCU), x.single, x.p.ilp,
+                             x.waves_cu, x.overlap, -x.p.n_chunks);
     };
     if (key(c) > key(*pick)) pick = &c;
   }
   return pick->p;
+}
+
+// Wide rows: a plan for the global-node PERFECT kernel.  The LDS holds the row tile and the
+// per-group class sums only; G lane groups split the trees; up to 16 waves per workgroup (no
+// staging wave).  Picks the most resident waves (up to 16 per CU), then fewer lane groups,
+// then more rows per tile.
+Plan choose_global_plan(const PlanInput &in) {
+  Plan best{};
+  auto key = [](const Plan &p) {
+    return std::make_tuple(std::min(p.waves_per_cu, 16), -p.groups, p.rows_per_wg);
+  };
+  for (int W : {1, 2, 4, 8, 16}) {
+    for (int R = 32; R <= 64 * W; R *= 2) {
+      const int G = 64 * W / R;
+      if (G > 1 && (int64_t)G * 4 > in.n_trees) continue;  // a few trees per lane group
+      const int64_t lds = (int64_t)in.F * R * 4 + (int64_t)in.K * G * R * 8;
+      if (lds > kLdsBytesPerCU) continue;
+      const int m = (int)std::min<int64_t>(kLdsBytesPerCU / lds, kMaxWavesPerCU / W);
+      if (m < 1) continue;
+      Plan p{};
+      p.waves = W;
+      p.rows_per_wg = R;
+      p.groups = G;
+      p.lds_bytes = (int32_t)lds;
+      p.acc_in_lds = 1;
+      p.ilp = env_int("BRIDGER_ILP", 8) == 4 ? 4 : 8;  // L2 round trips: keep 8 in flight
+      p.global_nodes = 1;
+      p.waves_per_cu = m * W;
+      const double n = (double)std::max<int64_t>(in.n_rows, 1);
+      p.hbm_bytes = n * in.F * 4 + n * in.K * 4 + in.forest_bytes;
+      p.lds_read_bytes = 256.0 * n / 64.0 * in.visits_per_row;
+      if (best.waves == 0 || key(p) > key(best)) best = p;
+    }
+  }
+  return best;
 }
 
 void ragged_chunks(bridger_forest *h, int64_t chunk_bytes) {
@@ -634,7 +679,7 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
     a.log2_row_bytes = ilog2(4 * (int64_t)p.rows_per_wg);
     a.groups = p.groups;
     a.chunk_bytes = p.chunk_bytes;
-    a.lds_x_off = 2 * p.chunk_bytes;
+    a.lds_x_off = p.global_nodes ? 0 : 2 * p.chunk_bytes;
     a.lds_acc_off = a.lds_x_off + h->F * p.rows_per_wg * 4;
     a.acc_in_lds = p.acc_in_lds;
     a.ilp = p.ilp;
@@ -644,7 +689,9 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
                        perfect_fixed_ok(h->perfect_depth, p.trees_per_chunk) &&
                        p.chunk_bytes == p.trees_per_chunk * h->perfect_tree_bytes &&
                        h->fixed_chunks;
-    if (fixed)
+    if (h->kernel_active == kPerfect && p.global_nodes)
+      err = launch_perfect_global(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
+    else if (fixed)
       err = launch_perfect_fixed(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else if (h->kernel_active == kPerfect)
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
@@ -786,6 +833,18 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       PlanInput pin{1 << 20, n_features, n_classes, n_trees,
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
       h->perfect_plan = choose_plan(pin);
+      // Wide rows: when streaming the forest through LDS chunks leaves few waves per CU and
+      // the forest fits in L2, read the records from global memory instead.
+      const int gmode = env_int("BRIDGER_GLOBAL", -1);  // tuning override: 0 off, 1 on
+      if (gmode != 0 && D <= kMaxPerfectDepth) {
+        const Plan g = choose_global_plan(pin);
+        const bool few = h->perfect_plan.waves == 0 ||
+                         h->perfect_plan.waves_per_cu < kMinWavesPerCU;
+        if (g.waves > 0 &&
+            (gmode == 1 || (few && pin.forest_bytes <= kL2BytesPerXcd &&
+                            g.waves_per_cu > h->perfect_plan.waves_per_cu)))
+          h->perfect_plan = g;
+      }
       h->perfect_ok = h->perfect_plan.waves > 0;
       if (h->perfect_ok) build_perfect_trav(h);
     }
@@ -933,7 +992,8 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
   if (lds_bytes) *lds_bytes = p.lds_bytes;
   if (hbm_bytes) *hbm_bytes = n * h->F * 4 + n * h->K * 4 + forest_bytes;
   const bool no_lds = h->kernel_active == kDirect || h->kernel_active == kGemm;
-  if (stage_bytes) *stage_bytes = no_lds ? 0.0 : n_wg * forest_bytes + n * h->F * 4;
+  const bool no_chunks = no_lds || p.global_nodes;
+  if (stage_bytes) *stage_bytes = no_lds ? 0.0 : (no_chunks ? 0.0 : n_wg * forest_bytes) + n * h->F * 4;
   if (lds_read_bytes)
     *lds_read_bytes = no_lds
                           ? 0.0

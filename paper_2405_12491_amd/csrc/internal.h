@@ -64,7 +64,9 @@ struct Plan {
   int32_t n_chunks;
   int32_t lds_bytes;       // dynamic LDS per workgroup
   int32_t acc_in_lds;      // class/group partial sums kept in LDS
-  int32_t ilp;             // PERFECT: trees walked at once per lane (4 or 8)
+  int32_t ilp;             // PERFECT: trees walked at once per lane (1, 2 or 4)
+  int32_t global_nodes;    // PERFECT: records read from global memory, LDS holds only the tile
+  int32_t waves_per_cu;    // resident compute waves per CU
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
 };
 
@@ -100,7 +102,7 @@ struct LaunchArgs {
   int32_t lds_x_off;           // byte offset of the feature tile in dynamic LDS
   int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
   int32_t acc_in_lds;
-  int32_t ilp;                 // PERFECT: trees walked at once per lane (4 or 8)
+  int32_t ilp;                 // PERFECT: trees walked at once per lane (1, 2 or 4)
   int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)
   const uint32_t *roots;       // PERFECT: per kernel tree the root's traversal record (2 words)
 };
@@ -108,6 +110,8 @@ struct LaunchArgs {
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                    void *stream);
+int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                          void *stream);
 int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                          void *stream);
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);

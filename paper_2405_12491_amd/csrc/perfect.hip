@@ -113,15 +113,16 @@ static int launch_perfect_df(const LaunchArgs &a, int waves, int64_t n_wg, int l
                              void *stream) {
   const bool simple = a.K == 1 && a.groups == 1;
   const int threads = 64 * (waves + 1);  // + the staging wave
+  // any plan works with any U (a chunk's last partial group is walked one tree at a time);
+  // lane-group plans pick U to fit the LDS
   if (a.out_leaf)
     return launch_common(perfect_kernel<D, 4, true, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-  if (a.ilp == 8) {
-    if (simple)
-      return launch_common(perfect_kernel<D, 8, false, true, FIN>, threads, n_wg, lds_bytes, stream, a);
-    return launch_common(perfect_kernel<D, 8, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-  }
   if (simple)
     return launch_common(perfect_kernel<D, 4, false, true, FIN>, threads, n_wg, lds_bytes, stream, a);
+  if (a.ilp == 1)
+    return launch_common(perfect_kernel<D, 1, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
+  if (a.ilp == 2)
+    return launch_common(perfect_kernel<D, 2, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(perfect_kernel<D, 4, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
 }
 

@@ -1,0 +1,126 @@
+// perfect_global.hip -- PERFECT forests on wide rows: the LDS holds only the row tile and the
+// node records are read from global memory, where a forest of a few MB stays in L2.
+//
+// With wide rows (hundreds of features) a row tile of 32 rows already fills most of the LDS,
+// so streaming the forest through LDS chunks leaves one or two compute waves per CU and the
+// chunk staging latency-bound; restaging the whole forest for every 32 rows also multiplies
+// the L2->LDS traffic.  Here G lane groups share each row tile and split the trees into
+// contiguous ranges (no chunks, no staging, no barriers inside the walk), so a CU runs as
+// many waves as the tile and the per-group class sums allow.
+#include "perfect_walk.h"
+
+namespace bridger {
+
+template <int D, int U, bool LEAVES, bool FIN>
+__global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x;
+  const int R = a.rows_per_wg, G = a.groups;
+  const uint32_t tb = (uint32_t)a.tree_bytes;
+  const int T = a.n_trees;
+  const int r = tid & (R - 1);
+  const int g = R >= 64 ? __builtin_amdgcn_readfirstlane(tid / R) : tid / R;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  constexpr uint32_t kLeafOff = 4u << D;
+  constexpr uint32_t kFirstLeaf = 1u << D;
+
+  if (g == 0) load_row_tile<FIN>(smem, a, r, row, row_ok);
+  __syncthreads();
+
+  double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
+  const int slot_stride = G * R;
+  const int t_begin = (int)(((int64_t)T * g) / G), t_end = (int)(((int64_t)T * (g + 1)) / G);
+  ClassAcc ca;
+  ca.k = 0;
+  ca.acc = class_init(a, 0, g == 0);
+  ca.next_b = a.class_begin[1];
+
+  auto finish = [&](auto &m, int q) {
+    constexpr int N = sizeof(m) / sizeof(m[0]);
+    if (LEAVES) {
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
+        if (row_ok) {
+          const int t = q + u;
+          a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
+              a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
+        }
+      }
+    } else {
+      float lv[N];
+#pragma unroll
+      for (int u = 0; u < N; ++u)
+        lv[u] = *reinterpret_cast<const float *>(a.nodes + (size_t)(q + u) * tb + kLeafOff +
+                                                 (m[u] << 2));
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
+        class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+        ca.acc += (double)lv[u];
+      }
+    }
+  };
+
+  int q = t_begin;
+  for (; q + U <= t_end; q += U) {
+    uint32_t m[U];
+    walk_trees_global<D, U, FIN>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
+    finish(m, q);
+  }
+  for (; q < t_end; ++q) {
+    uint32_t m[1];
+    walk_trees_global<D, 1, FIN>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
+    finish(m, q);
+  }
+  if (LEAVES) return;
+  class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  __syncthreads();
+  if (g == 0) {
+    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
+    for (int k = 0; k < a.K; ++k) {
+      double s = z[k * slot_stride];
+      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
+      z[k * slot_stride] = s;
+    }
+    if (row_ok) finalize_store(a, z, slot_stride, row);
+  }
+}
+
+// ---------------------------------------------------------------------- launchers
+template <int D, bool FIN>
+static int launch_global_df(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                            void *stream) {
+  const int threads = 64 * waves;
+  if (a.out_leaf)
+    return launch_common(perfect_global_kernel<D, 4, true, FIN>, threads, n_wg, lds_bytes, stream, a);
+  if (a.ilp == 4)
+    return launch_common(perfect_global_kernel<D, 4, false, FIN>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(perfect_global_kernel<D, 8, false, FIN>, threads, n_wg, lds_bytes, stream, a);
+}
+
+template <int D>
+static int launch_global_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                           void *stream) {
+  return a.finite_thresholds ? launch_global_df<D, true>(a, waves, n_wg, lds_bytes, stream)
+                             : launch_global_df<D, false>(a, waves, n_wg, lds_bytes, stream);
+}
+
+int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                          void *stream) {
+  switch (depth) {
+    case 1: return launch_global_d<1>(a, waves, n_wg, lds_bytes, stream);
+    case 2: return launch_global_d<2>(a, waves, n_wg, lds_bytes, stream);
+    case 3: return launch_global_d<3>(a, waves, n_wg, lds_bytes, stream);
+    case 4: return launch_global_d<4>(a, waves, n_wg, lds_bytes, stream);
+    case 5: return launch_global_d<5>(a, waves, n_wg, lds_bytes, stream);
+    case 6: return launch_global_d<6>(a, waves, n_wg, lds_bytes, stream);
+    case 7: return launch_global_d<7>(a, waves, n_wg, lds_bytes, stream);
+    case 8: return launch_global_d<8>(a, waves, n_wg, lds_bytes, stream);
+    case 9: return launch_global_d<9>(a, waves, n_wg, lds_bytes, stream);
+    case 10: return launch_global_d<10>(a, waves, n_wg, lds_bytes, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+}  // namespace bridger

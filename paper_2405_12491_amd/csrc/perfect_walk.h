@@ -75,4 +75,34 @@ __device__ __forceinline__ void walk_trees_root(const uint8_t *smem, uint32_t b0
   }
 }
 
+// The same walk over records read from global memory (L1/L2) instead of an LDS chunk: tree
+// u's block starts at byte t0_off + u * tb of `nodes`; the feature values still come from the
+// LDS tile.
+template <int D, int U, bool FIN>
+__device__ __forceinline__ void walk_trees_global(const uint8_t *smem, const uint8_t *nodes,
+                                                  size_t t0_off, uint32_t tb, uint32_t lane_off,
+                                                  uint32_t (&m)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) m[u] = 1u;
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    uint2 rec[U];
+    float xv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      rec[u] = *reinterpret_cast<const uint2 *>(nodes + t0_off + (size_t)u * tb + (m[u] << 3));
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (FIN) {
+        const float diff = __uint_as_float(rec[u].x) - xv[u];
+        m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
+      } else {
+        m[u] = 2u * m[u] + ((xv[u] <= __uint_as_float(rec[u].x)) ? 0u : 1u);
+      }
+    }
+  }
+}
+
 }  // namespace bridger

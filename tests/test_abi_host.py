@@ -256,7 +256,11 @@ def test_plan_respects_lds_capacity(name):
             assert R >= 32 and R & (R - 1) == 0
             assert p["lds_bytes"] <= 160 * 1024
             assert 2 * p["chunk_bytes"] + R * w.n_features * 4 <= p["lds_bytes"]
-            if k == B.BRIDGER_KERNEL_PERFECT:
+            if k == B.BRIDGER_KERNEL_PERFECT and p["chunk_bytes"] == 0:
+                # records read from global memory: the LDS holds the tile and class sums only
+                assert p["trees_per_chunk"] == 0 and p["n_chunks"] == 0
+                assert R * w.n_features * 4 + 8 * f.n_classes * R <= p["lds_bytes"]
+            elif k == B.BRIDGER_KERNEL_PERFECT:
                 tb = B.bridger_forest_packed(f.handle, 0, np.uint8).size // f.n_trees
                 assert p["trees_per_chunk"] * tb <= p["chunk_bytes"]
                 assert p["n_chunks"] * p["trees_per_chunk"] >= f.n_trees

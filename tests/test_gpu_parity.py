@@ -247,6 +247,46 @@ def test_classes_aggregates_transforms(agg, xform, K):
                     check_parity(model, X, k, f"K={K} agg={agg} x={xform} {B.KERNEL_NAMES[k]}", forest=f)
 
 
+# launch shapes and kernel variants the planner does not pick for these forests, forced with
+# the planner's tuning variables (read when a forest is created)
+VARIANT_ENVS = [
+    {"BRIDGER_GLOBAL": "1"},                                   # records from global memory
+    {"BRIDGER_GLOBAL": "1", "BRIDGER_NO_SIGN_STEP": "1"},
+    {"BRIDGER_NO_FIXED": "1"},                                 # run-time chunk geometry
+    {"BRIDGER_CHUNK_TREES": "4"},                              # compile-time chunks of 4, 8, 32
+    {"BRIDGER_CHUNK_TREES": "8"},
+    {"BRIDGER_CHUNK_TREES": "32"},
+    {"BRIDGER_ILP": "1", "BRIDGER_WAVES": "4", "BRIDGER_ROWS": "64"},   # 4 lane groups, 1 tree
+    {"BRIDGER_ILP": "2", "BRIDGER_WAVES": "2", "BRIDGER_ROWS": "64"},   # 2 lane groups, 2 trees
+]
+
+
+def _variant_models():
+    rng = np.random.default_rng(77)
+    K, T = 3, 23
+    trees = [perfect_tree_arrays(4, rng.integers(0, 6, 15), rng.standard_normal(15).astype(np.float32),
+                                 rng.standard_normal(16).astype(np.float32)) for _ in range(T)]
+    tc = rng.integers(0, K, T)
+    tc[:K] = np.arange(K)
+    multi = concat_trees(trees, 6, K, tc, AGG_SUM, XFORM_SOFTMAX, rng.standard_normal(K).astype(np.float32))
+    X6 = rng.standard_normal((1100, 6)).astype(np.float32)
+    g = make_workload("gbdt_d6", 1500)
+    r = make_workload("rf_d8", 700)
+    return [("gbdt_d6", g.forest, g.X()), ("rf_d8", r.forest, r.X()), ("multiclass", multi, X6)]
+
+
+@pytest.mark.parametrize("env", VARIANT_ENVS, ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
+def test_perfect_kernel_variants(env, monkeypatch):
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    for name, model, X in _variant_models():
+        with B.Forest(model) as f:
+            if not supported(f, B.BRIDGER_KERNEL_PERFECT):
+                continue
+            print(f"[variant] {env} {name} plan={f.plan(X.shape[0])}", flush=True)
+            check_parity(model, X, B.BRIDGER_KERNEL_PERFECT, f"{name} {env}", forest=f)
+
+
 def test_determinism_and_streams():
     import torch
     w = make_workload("gbdt_d6", 5000)
