@@ -487,17 +487,22 @@ Plan choose_plan(const PlanInput &in) {
   return pick->p;
 }
 
-// Wide rows: a plan for the global-node PERFECT kernel.  The LDS holds the row tile and the
-// per-group class sums only; G lane groups split the trees; up to 16 waves per workgroup (no
-// staging wave).  Picks the most resident waves (up to 16 per CU), then fewer lane groups,
-// then more rows per tile.
+// Wide rows: a plan for the global-node kernels (PERFECT and RAGGED).  The LDS holds the row
+// tile and the per-group class sums only; G lane groups split the trees; up to 16 waves per
+// workgroup (no staging wave).  Picks the most resident waves (every wave hides L2 round
+// trips), then fewer lane groups, then more rows per tile.
 Plan choose_global_plan(const PlanInput &in) {
   Plan best{};
-  auto key = [](const Plan &p) {
-    return std::make_tuple(std::min(p.waves_per_cu, 16), -p.groups, p.rows_per_wg);
+  const int force_waves = env_int("BRIDGER_WAVES", 0);
+  const int force_rows = env_int("BRIDGER_ROWS", 0);
+  const int wave_cap = env_int("BRIDGER_GLOBAL_WAVES_CU", 32);
+  auto key = [wave_cap](const Plan &p) {
+    return std::make_tuple(std::min(p.waves_per_cu, wave_cap), -p.groups, p.rows_per_wg);
   };
   for (int W : {1, 2, 4, 8, 16}) {
+    if (force_waves && W != force_waves) continue;
     for (int R = 32; R <= 64 * W; R *= 2) {
+      if (force_rows && R != force_rows) continue;
       const int G = 64 * W / R;
       if (G > 1 && (int64_t)G * 4 > in.n_trees) continue;  // a few trees per lane group
       const int64_t lds = (int64_t)in.F * R * 4 + (int64_t)in.K * G * R * 8;
@@ -695,6 +700,8 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
       err = launch_perfect_fixed(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else if (h->kernel_active == kPerfect)
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
+    else if (p.global_nodes)
+      err = launch_ragged_global(a, p.waves, n_wg, p.lds_bytes, stream);
     else
       err = launch_ragged(a, p.waves, n_wg, p.lds_bytes, stream);
   } else if (h->kernel_active == kGemm) {
@@ -852,8 +859,21 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
                     (int32_t)std::min<int64_t>(h->ragged_max_tree_bytes, INT32_MAX), false, visits};
       h->ragged_plan = choose_plan(pin);
+      // Big forests on wide rows: when the chunked plan leaves few waves per CU, read the
+      // records from global memory (the forest stays in L2 / the last-level cache).
+      const int gmode = env_int("BRIDGER_GLOBAL", -1);
+      if (gmode != 0) {
+        Plan g = choose_global_plan(pin);
+        g.ilp = env_int("BRIDGER_ILP", 2) == 1 ? 1 : 2;  // runs per lane
+        const bool few = h->ragged_plan.waves == 0 ||
+                         h->ragged_plan.waves_per_cu < kMinWavesPerCU;
+        if (g.waves > 0 &&
+            (gmode == 1 || (few && g.waves_per_cu > h->ragged_plan.waves_per_cu)))
+          h->ragged_plan = g;
+      }
       h->ragged_ok = h->ragged_plan.waves > 0;
-      if (h->ragged_ok) ragged_chunks(h, h->ragged_plan.chunk_bytes);
+      if (h->ragged_ok && !h->ragged_plan.global_nodes)
+        ragged_chunks(h, h->ragged_plan.chunk_bytes);
     }
     h->kernel_active = resolve_auto(h);
     const int forced = env_int("BRIDGER_KERNEL", 0);

@@ -65,7 +65,7 @@ struct Plan {
   int32_t lds_bytes;       // dynamic LDS per workgroup
   int32_t acc_in_lds;      // class/group partial sums kept in LDS
   int32_t ilp;             // PERFECT: trees walked at once per lane (1, 2 or 4)
-  int32_t global_nodes;    // PERFECT: records read from global memory, LDS holds only the tile
+  int32_t global_nodes;    // records read from global memory, LDS holds only the tile
   int32_t waves_per_cu;    // resident compute waves per CU
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
 };
@@ -115,6 +115,8 @@ int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_w
 int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                          void *stream);
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
+int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                         void *stream);
 int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream);
 int launch_gemm(int depth, const LaunchArgs &a, int64_t n_wg, void *stream);
 

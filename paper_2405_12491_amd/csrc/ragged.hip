@@ -100,7 +100,120 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   }
 }
 
+// Records read from global memory instead of LDS chunks (big forests on wide rows, where a
+// 64-row tile already takes most of the LDS and restaging every tree for every tile is the
+// bottleneck).  G lane groups share the row tile; group g walks the contiguous tree range
+// [T g / G, T (g + 1) / G) split into U runs, each a state machine over its records.  No
+// chunks, no staging, one barrier before the cross-group reduction.
+template <bool LEAVES, bool SIMPLE, int U>
+__global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
+  static_assert(U == 1 || LEAVES || SIMPLE, "several runs need one output per row");
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int tid = threadIdx.x;
+  const int R = a.rows_per_wg, G = a.groups;
+  const int r = tid & (R - 1);
+  const int g = tid / R;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const int shift = a.log2_row_bytes;
+  const int T = a.n_trees;
+
+  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  __syncthreads();
+
+  double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
+  const int slot_stride = G * R;
+  ClassAcc ca;
+  ca.k = 0;
+  ca.acc = class_init(a, 0, g == 0);
+  ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+
+  const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
+  const uint2 *recs = reinterpret_cast<const uint2 *>(a.nodes);
+  int64_t idx[U], end[U];
+  int t[U];
+  double run_acc[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int ta = ga + ((gb - ga) * u) / U, tz = ga + ((gb - ga) * (u + 1)) / U;
+    idx[u] = a.tree_start[ta];
+    end[u] = a.tree_start[tz];
+    t[u] = ta;
+    run_acc[u] = 0.0;
+  }
+  while (true) {
+    bool any = false;
+#pragma unroll
+    for (int u = 0; u < U; ++u) any = any || idx[u] < end[u];
+    if (!any) break;
+    uint2 rec[U];
+    float xv[U];
+    // a finished run re-reads its last record (the result is discarded)
+#pragma unroll
+    for (int u = 0; u < U; ++u) rec[u] = recs[idx[u] < end[u] ? idx[u] : end[u] - 1];
+#pragma unroll
+    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, ((rec[u].y >> 16) << shift) + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (idx[u] < end[u]) {
+        const uint32_t meta = rec[u].y;
+        const bool leaf = (meta & (uint32_t)kLeafFlag) != 0;
+        const uint32_t rel = meta & (uint32_t)kMaxRel;
+        const bool right = !(xv[u] <= __uint_as_float(rec[u].x)) && !leaf;
+        if (leaf) {
+          if (LEAVES) {
+            if (row_ok)
+              a.out_leaf[row * (int64_t)T + a.tree_order[t[u]]] = a.leaf_map[idx[u]];
+          } else if (U == 1) {
+            if (!SIMPLE) class_advance(a, ca, t[u], acc_lds, slot_stride, g == 0);
+            ca.acc += (double)__uint_as_float(rec[u].x);
+          } else {
+            run_acc[u] += (double)__uint_as_float(rec[u].x);
+          }
+          ++t[u];
+        }
+        // a valid record always moves forward; the max keeps the loop finite regardless
+        const uint32_t step = rel + (right ? 1u : 0u);
+        idx[u] += step > 1u ? step : 1u;
+      }
+    }
+  }
+  if (LEAVES) return;
+  if (U > 1) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) ca.acc += run_acc[u];
+  }
+  if (SIMPLE) {
+    acc_lds[0] = ca.acc;
+  } else {
+    class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  }
+  __syncthreads();
+  if (g == 0) {
+    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
+    for (int k = 0; k < a.K; ++k) {
+      double s = z[k * slot_stride];
+      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
+      z[k * slot_stride] = s;
+    }
+    if (row_ok) finalize_store(a, z, slot_stride, row);
+  }
+}
+
 // ---------------------------------------------------------------------- launchers
+int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                         void *stream) {
+  const int threads = 64 * waves;
+  if (a.out_leaf)
+    return launch_common(ragged_global_kernel<true, false, 1>, threads, n_wg, lds_bytes, stream, a);
+  if (a.K != 1)
+    return launch_common(ragged_global_kernel<false, false, 1>, threads, n_wg, lds_bytes, stream, a);
+  if (a.ilp == 2)
+    return launch_common(ragged_global_kernel<false, true, 2>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_global_kernel<false, true, 1>, threads, n_wg, lds_bytes, stream, a);
+}
+
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {
   const bool simple = a.K == 1;
   const int threads = 64 * (waves + 1);  // + the staging wave

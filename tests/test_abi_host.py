@@ -264,6 +264,10 @@ def test_plan_respects_lds_capacity(name):
                 tb = B.bridger_forest_packed(f.handle, 0, np.uint8).size // f.n_trees
                 assert p["trees_per_chunk"] * tb <= p["chunk_bytes"]
                 assert p["n_chunks"] * p["trees_per_chunk"] >= f.n_trees
+            elif p["chunk_bytes"] == 0:
+                # records read from global memory: no chunks
+                assert p["n_chunks"] == 0
+                assert R * w.n_features * 4 <= p["lds_bytes"]
             else:
                 chunks = B.bridger_forest_packed(f.handle, 4, np.int32)
                 start = B.bridger_forest_packed(f.handle, 1, np.int32)

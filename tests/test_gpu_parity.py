@@ -275,6 +275,32 @@ def _variant_models():
     return [("gbdt_d6", g.forest, g.X()), ("rf_d8", r.forest, r.X()), ("multiclass", multi, X6)]
 
 
+@pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1"}, {"BRIDGER_GLOBAL": "1", "BRIDGER_ILP": "2"},
+                                 {"BRIDGER_GLOBAL": "0"}],
+                         ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
+def test_ragged_kernel_variants(env, monkeypatch):
+    """The ragged kernel with records in LDS chunks and read from global memory (one or two
+    runs per lane), on ragged, multiclass and leaf-id cases."""
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    rng = np.random.default_rng(91)
+    models = []
+    w = make_workload("ragged_d12", 3 * 64 + 29)
+    models.append(("ragged_d12", w.forest, w.X()))
+    rf = random_tiny_forest(rng, 40, 6, max_depth=9)
+    X6 = rng.standard_normal((700, 6)).astype(np.float32)
+    models.append(("tiny_ragged", rf, X6))
+    multi = random_tiny_forest(rng, 40, 6, max_depth=9, n_classes=3, aggregate=AGG_MEAN,
+                               transform=XFORM_SOFTMAX)
+    models.append(("multiclass_ragged", multi, X6))
+    for name, model, X in models:
+        with B.Forest(model) as f:
+            if not supported(f, B.BRIDGER_KERNEL_RAGGED):
+                continue
+            print(f"[variant] {env} {name} plan={f.plan(X.shape[0])}", flush=True)
+            check_parity(model, X, B.BRIDGER_KERNEL_RAGGED, f"{name} {env}", forest=f)
+
+
 @pytest.mark.parametrize("env", VARIANT_ENVS, ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
 def test_perfect_kernel_variants(env, monkeypatch):
     for k, v in env.items():
