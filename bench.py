@@ -79,6 +79,9 @@ def parse():
     p.add_argument("--kernel", default="auto", choices=["auto", "perfect", "ragged", "direct", "gemm"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-rows", type=int, default=200_000)
+    p.add_argument("--binned", action="store_true",
+                   help="time prediction on 8/16-bit feature bins (bins made once, untimed; the "
+                        "binning pass is timed separately as bin_ms)")
     p.add_argument("--calib-copy", action="store_true",
                    help="time a plain device copy of X instead (counter calibration)")
     return p.parse_args()
@@ -169,8 +172,22 @@ def main():
         forest.kernel = {"perfect": 1, "ragged": 2, "direct": 3, "gemm": 4}[args.kernel]
     out = torch.empty((w.n_rows, w.forest.n_classes), dtype=torch.float32, device=dev)
     plan = forest.plan(w.n_rows)
+    bin_ms = None
+    if args.binned:
+        Xq = forest.bin(Xd)
+        torch.cuda.synchronize()
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record(stream)
+        for _ in range(5):
+            forest.bin(Xd, Xq)
+        b1.record(stream)
+        torch.cuda.synchronize()
+        bin_ms = b0.elapsed_time(b1) / 5
+        step = lambda: forest.predict_binned(Xq, out)
+    else:
+        step = lambda: forest.predict(Xd, out)
     for _ in range(args.warmup):
-        forest.predict(Xd, out)
+        step()
     torch.cuda.synchronize()
 
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -178,7 +195,7 @@ def main():
     t_wall = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        forest.predict(Xd, out)
+        step()
     e1.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
@@ -199,7 +216,8 @@ def main():
         visits_per_row = float(depth[lv.astype(np.int64) + offs[None, :]].sum()) / m
     visits = visits_per_row * n
     forest_bytes = B.bridger_forest_packed(forest.handle, 0, np.uint8).size
-    alg_bytes = n * w.n_features * 4 + n * f.n_classes * 4 + forest_bytes
+    x_elem = forest.bin_info()["bin_bytes"] if args.binned else 4
+    alg_bytes = n * w.n_features * x_elem + n * f.n_classes * 4 + forest_bytes
     s = ms / 1e3
     visits_per_s = visits / s
     line = {
@@ -220,6 +238,7 @@ def main():
             "n_rows": n, "n_features": w.n_features, "n_trees": f.n_trees,
             "n_classes": f.n_classes,
             "kernel": B.KERNEL_NAMES[forest.kernel],
+            "binned": bool(args.binned),
             "plan": {k: v for k, v in plan.items() if not isinstance(v, float)},
         },
         "roofline": {
@@ -241,6 +260,11 @@ def main():
                 "frac": alg_bytes / s / HBM_PEAK_BYTES_PER_S},
         "wall_s_timed_region": t_wall,
     }
+    if args.binned:
+        line["binning"] = {"bin_bytes": x_elem, "bin_ms": bin_ms,
+                           "note": "bins made once before the timed region; bin_ms is one "
+                                   "binning pass over the same rows"}
+        line["roofline"]["traffic"] = None
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, out, args.cpu_sample_rows)
     print(json.dumps(line), flush=True)

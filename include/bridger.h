@@ -145,6 +145,42 @@ bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X,
                                              int32_t n_features, int32_t *out_leaf,
                                              void *stream);
 
+/*
+ * Exact feature quantization (the "data type rewriting" of Table 2).  For each
+ * feature, the forest's distinct thresholds on it, ascending (-0 and +0 are one);
+ * the bin of a value x is the number of them strictly below x, and a NaN gets
+ * their count.  For a threshold t of rank k, x <= t exactly when bin(x) <= k, so
+ * predicting on bins reaches the same leaves as predicting on the fp32 rows.
+ *
+ * bin_info: *bin_bytes = 1 when every feature has at most 255 distinct
+ * thresholds, 2 when at most 65535, 0 when some feature has more (binning is then
+ * unsupported); *n_thresholds = their total count.  Any pointer may be NULL;
+ * works on host-only handles.
+ */
+bridger_status bridger_forest_bin_info(bridger_forest_t h, int32_t *bin_bytes,
+                                       int64_t *n_thresholds);
+
+/*
+ * Bin n_rows fp32 rows.  X as for predict; Xq a device pointer to n_rows x
+ * n_features elements of bin_bytes each (uint8 or uint16, row-major), aligned to
+ * bin_bytes, not overlapping X.  Asynchronous on stream.  BRIDGER_ERR_UNSUPPORTED
+ * when bin_bytes is 0.
+ */
+bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_rows,
+                                  int32_t n_features, void *Xq, void *stream);
+
+/*
+ * Predict (or write leaf ids) from binned rows Xq made by bridger_forest_bin for
+ * this handle; same outputs, rules and errors as predict / predict_leaves.  The
+ * feature tile then takes bin_bytes instead of 4 bytes per value.  Runs on the
+ * perfect and ragged kernel families (BRIDGER_ERR_UNSUPPORTED otherwise).
+ */
+bridger_status bridger_forest_predict_binned(bridger_forest_t h, const void *Xq, int64_t n_rows,
+                                             int32_t n_features, float *out, void *stream);
+bridger_status bridger_forest_predict_binned_leaves(bridger_forest_t h, const void *Xq,
+                                                    int64_t n_rows, int32_t n_features,
+                                                    int32_t *out_leaf, void *stream);
+
 /* Shape facts.  Any output pointer may be NULL.  all_perfect = 1 when every tree
  * is perfect with one common depth (then max_depth is that depth). */
 bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,
@@ -173,8 +209,9 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
  * Read-only view of a host copy of the packed layout, for inspection and tests:
  * which = 0 node records of the active kernel family, 1 per-tree start offsets,
  * 2 leaf-id map (kernel leaf slot -> caller node id), 3 kernel tree order
- * (kernel position -> caller tree index), 4 chunk table.  *ptr stays valid until
- * destroy or set_kernel.
+ * (kernel position -> caller tree index), 4 chunk table, 5 the binning thresholds
+ * (float, feature after feature, each ascending), 6 their per-feature offsets
+ * (int32 [n_features + 1]).  *ptr stays valid until destroy or set_kernel.
  */
 bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
                                      int64_t *bytes);

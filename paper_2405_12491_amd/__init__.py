@@ -59,6 +59,10 @@ def load_library(path: Optional[str] = None):
     lib.bridger_forest_predict.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_predict_leaves.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_info.argtypes = [P, P, P, P, P, P]
+    lib.bridger_forest_bin_info.argtypes = [P, P, P]
+    lib.bridger_forest_bin.argtypes = [P, P, I64, I32, P, P]
+    lib.bridger_forest_predict_binned.argtypes = [P, P, I64, I32, P, P]
+    lib.bridger_forest_predict_binned_leaves.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_set_kernel.argtypes = [P, I32]
     lib.bridger_forest_get_kernel.argtypes = [P, P]
     lib.bridger_forest_plan.argtypes = [P, I64, P, P, P, P, P, P, P, P]
@@ -69,7 +73,9 @@ def load_library(path: Optional[str] = None):
     lib.bridger_last_error.restype = ctypes.c_char_p
     for name in ("bridger_forest_create", "bridger_forest_create_ex", "bridger_forest_predict",
                  "bridger_forest_predict_leaves", "bridger_forest_info", "bridger_forest_set_kernel",
-                 "bridger_forest_get_kernel", "bridger_forest_plan", "bridger_forest_packed"):
+                 "bridger_forest_get_kernel", "bridger_forest_plan", "bridger_forest_packed",
+                 "bridger_forest_bin_info", "bridger_forest_bin", "bridger_forest_predict_binned",
+                 "bridger_forest_predict_binned_leaves"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -121,6 +127,34 @@ def bridger_forest_predict_leaves(h, X_ptr: int, n_rows: int, n_features: int, o
                                                         int(n_features), ctypes.c_void_p(out_ptr),
                                                         ctypes.c_void_p(stream)),
            "bridger_forest_predict_leaves")
+
+
+def bridger_forest_bin_info(h) -> dict:
+    b, n = ctypes.c_int32(), ctypes.c_int64()
+    _check(load_library().bridger_forest_bin_info(h, ctypes.byref(b), ctypes.byref(n)),
+           "bridger_forest_bin_info")
+    return {"bin_bytes": b.value, "n_thresholds": n.value}
+
+
+def bridger_forest_bin(h, X_ptr: int, n_rows: int, n_features: int, xq_ptr: int, stream: int = 0):
+    _check(load_library().bridger_forest_bin(h, ctypes.c_void_p(X_ptr), int(n_rows), int(n_features),
+                                             ctypes.c_void_p(xq_ptr), ctypes.c_void_p(stream)),
+           "bridger_forest_bin")
+
+
+def bridger_forest_predict_binned(h, xq_ptr: int, n_rows: int, n_features: int, out_ptr: int,
+                                  stream: int = 0):
+    _check(load_library().bridger_forest_predict_binned(h, ctypes.c_void_p(xq_ptr), int(n_rows),
+                                                        int(n_features), ctypes.c_void_p(out_ptr),
+                                                        ctypes.c_void_p(stream)),
+           "bridger_forest_predict_binned")
+
+
+def bridger_forest_predict_binned_leaves(h, xq_ptr: int, n_rows: int, n_features: int,
+                                         out_ptr: int, stream: int = 0):
+    _check(load_library().bridger_forest_predict_binned_leaves(
+        h, ctypes.c_void_p(xq_ptr), int(n_rows), int(n_features), ctypes.c_void_p(out_ptr),
+        ctypes.c_void_p(stream)), "bridger_forest_predict_binned_leaves")
 
 
 def bridger_forest_info(h) -> dict:
@@ -228,6 +262,52 @@ class Forest:
         stream = torch.cuda.current_stream(X.device).cuda_stream
         bridger_forest_predict_leaves(self._h, X.data_ptr(), X.shape[0], self.n_features,
                                       out.data_ptr(), stream)
+        return out
+
+    def bin_info(self) -> dict:
+        return bridger_forest_bin_info(self._h)
+
+    def bin(self, X, out=None):
+        """Bins of X (uint8 or uint16 CUDA tensor [n, F]) for predict_binned."""
+        import torch
+        self._check_x(X)
+        bb = self.bin_info()["bin_bytes"]
+        if bb == 0:
+            raise BridgerError(BRIDGER_ERR_UNSUPPORTED, "Forest.bin", "forest cannot be binned")
+        if out is None:
+            out = torch.empty((X.shape[0], self.n_features),
+                              dtype=torch.uint8 if bb == 1 else torch.int16, device=X.device)
+        stream = torch.cuda.current_stream(X.device).cuda_stream
+        bridger_forest_bin(self._h, X.data_ptr(), X.shape[0], self.n_features, out.data_ptr(), stream)
+        return out
+
+    def _check_q(self, Xq):
+        import torch
+        if not (isinstance(Xq, torch.Tensor) and Xq.is_cuda and Xq.element_size() in (1, 2)):
+            raise TypeError("Xq must be a CUDA tensor of 8- or 16-bit bins")
+        if Xq.dim() != 2 or Xq.shape[1] != self.n_features or not Xq.is_contiguous():
+            raise ValueError("Xq must be contiguous [n_rows, n_features]")
+        if Xq.element_size() != self.bin_info()["bin_bytes"]:
+            raise ValueError("Xq element size differs from the forest's bin size")
+
+    def predict_binned(self, Xq, out=None):
+        import torch
+        self._check_q(Xq)
+        if out is None:
+            out = torch.empty((Xq.shape[0], self.n_classes), dtype=torch.float32, device=Xq.device)
+        stream = torch.cuda.current_stream(Xq.device).cuda_stream
+        bridger_forest_predict_binned(self._h, Xq.data_ptr(), Xq.shape[0], self.n_features,
+                                      out.data_ptr(), stream)
+        return out
+
+    def predict_binned_leaves(self, Xq, out=None):
+        import torch
+        self._check_q(Xq)
+        if out is None:
+            out = torch.empty((Xq.shape[0], self.n_trees), dtype=torch.int32, device=Xq.device)
+        stream = torch.cuda.current_stream(Xq.device).cuda_stream
+        bridger_forest_predict_binned_leaves(self._h, Xq.data_ptr(), Xq.shape[0], self.n_features,
+                                             out.data_ptr(), stream)
         return out
 
     def close(self):

@@ -16,8 +16,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbridger.so")
 SOURCES = [os.path.join(CSRC, n) for n in
-           ("bridger_host.cpp", "perfect.hip", "perfect_fixed.hip", "perfect_global.hip",
-            "ragged.hip", "direct.hip", "gemm.hip")]
+           ("bridger_host.cpp", "perfect.hip", "perfect_binned.hip", "perfect_fixed.hip",
+            "perfect_global.hip", "ragged.hip", "direct.hip", "gemm.hip", "bin.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 ARCH = ["--offload-arch=gfx950"]

@@ -1,0 +1,84 @@
+// bin.hip -- exact feature quantization ("data type rewriting", Table 2): each fp32 feature
+// value becomes its bin, the number of the forest's distinct thresholds on that feature that
+// are strictly below it.  For a threshold t of rank k among them, x <= t iff bin(x) <= k
+// (-0.0 and +0.0 are one threshold; a NaN feature gets the table's size, above every rank,
+// so it goes right at every split as the fp32 compare sends it).
+//
+// A workgroup owns a block of rows.  It walks the features in runs whose threshold tables fit
+// its LDS buffer: stage the run's tables (direct global->LDS loads), then every (row, feature)
+// of the run binary-searches its feature's table in LDS.  A single table larger than the
+// buffer is searched in global memory instead.
+#include "kernel_common.h"
+
+namespace bridger {
+
+constexpr int kBinThreads = 256;
+
+__device__ __forceinline__ int lower_bound_f32(const float *t, int n, float x) {
+  int lo = 0, len = n;
+  while (len > 0) {
+    const int half = len >> 1;
+    if (t[lo + half] < x) {
+      lo += half + 1;
+      len -= half + 1;
+    } else {
+      len = half;
+    }
+  }
+  return lo;
+}
+
+template <int XB>
+__global__ __launch_bounds__(kBinThreads) void bin_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const float *tab = reinterpret_cast<const float *>(smem);
+  const int cap = a.chunk_bytes / 4;  // floats the LDS buffer holds
+  const int tid = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * a.rows_per_wg;
+  const int64_t r1 = (r0 + a.rows_per_wg < a.n_rows) ? r0 + a.rows_per_wg : a.n_rows;
+  const int F = a.F;
+  int f = 0;
+  while (f < F) {
+    const int base = a.q_off[f];
+    int fe = f;
+    while (fe < F && a.q_off[fe + 1] - base <= cap) ++fe;
+    const bool in_lds = fe > f;
+    if (!in_lds) fe = f + 1;  // one table too large for the buffer: search it in place
+    const int nf = fe - f;
+    if (in_lds) {
+      __syncthreads();  // the previous run's searches are done with the buffer
+      const int n = a.q_off[fe] - base;
+      for (int i = tid; i < n; i += kBinThreads) reinterpret_cast<float *>(smem)[i] = a.q_values[base + i];
+      __syncthreads();
+    }
+    const int64_t total = (r1 - r0) * nf;
+    for (int64_t i = tid; i < total; i += kBinThreads) {
+      const int64_t row = r0 + i / nf;
+      const int ff = f + (int)(i % nf);
+      const int64_t e = row * F + ff;
+      const float x = a.X[e];
+      const int o = a.q_off[ff] - base, cnt = a.q_off[ff + 1] - a.q_off[ff];
+      int b = cnt;
+      if (x == x) b = in_lds ? lower_bound_f32(tab + o, cnt, x)
+                             : lower_bound_f32(a.q_values + a.q_off[ff], cnt, x);
+      if (XB == 2) reinterpret_cast<uint16_t *>(a.xq)[e] = (uint16_t)b;
+      else reinterpret_cast<uint8_t *>(a.xq)[e] = (uint8_t)b;
+    }
+    f = fe;
+  }
+}
+
+int launch_bin(const LaunchArgs &a0, void *stream) {
+  LaunchArgs a = a0;
+  // about four row blocks per CU; each block restages the tables once
+  int64_t rows = (a.n_rows + 1023) / 1024;
+  rows = rows < 64 ? 64 : (rows > 16384 ? 16384 : rows);
+  a.rows_per_wg = (int32_t)rows;
+  a.chunk_bytes = 64 * 1024;
+  const int64_t blocks = (a.n_rows + rows - 1) / rows;
+  if (a.x_bytes == 2) return launch_common(bin_kernel<2>, kBinThreads, blocks, a.chunk_bytes, stream, a);
+  if (a.x_bytes == 1) return launch_common(bin_kernel<1>, kBinThreads, blocks, a.chunk_bytes, stream, a);
+  return (int)hipErrorInvalidValue;
+}
+
+}  // namespace bridger

@@ -101,6 +101,17 @@ struct bridger_forest {
   int64_t ragged_max_tree_bytes = 0;
   Plan ragged_plan{};
 
+  // exact feature quantization (Table 2 "data type rewriting"): per feature the distinct
+  // thresholds ascending (-0 stored as +0); a binned forest keeps each threshold's rank
+  int32_t bin_bytes = 0;                // 2 or 1; 0: some feature has 2^16 or more thresholds
+  std::vector<float> q_values;
+  std::vector<int32_t> q_off;           // [F + 1]
+  Plan perfect_bplan{}, ragged_bplan{};
+  bool perfect_bok = false, ragged_bok = false;
+  std::vector<uint8_t> perfect_btrav;   // PERFECT traversal copy for bins: {rank, f * R * bytes}
+  std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
+  std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
+
   // DIRECT
   std::vector<int32_t> direct_rec;  // 4 ints per record
   std::vector<int32_t> direct_root;
@@ -111,6 +122,9 @@ struct bridger_forest {
        *d_tree_order = nullptr;
   DevArrays d_perfect, d_ragged, d_direct;
   void *d_perfect_trav = nullptr, *d_perfect_roots = nullptr;
+  void *d_q_values = nullptr, *d_q_off = nullptr, *d_perfect_btrav = nullptr,
+       *d_ragged_brec = nullptr, *d_ragged_bchunk_first = nullptr,
+       *d_ragged_bchunk_rec = nullptr;
   double visits_per_row_est = 0;  // for the model: mean internal visits per row (all trees)
 };
 
@@ -355,7 +369,12 @@ struct PlanInput {
   int32_t tree_bytes;      // PERFECT: fixed block; RAGGED: largest tree
   bool perfect;
   double visits_per_row;
+  int32_t x_bytes = 4;     // element of the LDS tile: 4 (fp32) or 2 / 1 (bins)
 };
+
+// Smallest tile: bins pack 4 / x_bytes rows per 32-bit word and a half-wave's 32 rows must
+// fill 32 words of each feature's row, so R >= 32 * 4 / x_bytes.
+int min_rows(const PlanInput &in) { return 32 * (4 / in.x_bytes); }
 
 Plan choose_plan(const PlanInput &in) {
   // trees walked at once per lane (PERFECT): 4 unless the LDS only fits fewer trees per lane
@@ -380,12 +399,12 @@ Plan choose_plan(const PlanInput &in) {
     const int kTreesMultiple = ilp;
     for (int W : {1, 2, 4, 8}) {  // compute waves; each workgroup also has a staging wave
       if (force_waves && W != force_waves) continue;
-      for (int R = 32; R <= 64 * W; R *= 2) {
+      for (int R = min_rows(in); R <= 64 * W; R *= 2) {
         if (force_rows && R != force_rows) continue;
         const int G = 64 * W / R;
         if (G > 1 && !in.perfect && R < 64) continue;
         const bool acc_lds = in.K > 1 || G > 1;
-        const int64_t x_tile = (int64_t)in.F * R * 4;
+        const int64_t x_tile = (int64_t)in.F * R * in.x_bytes;
         const int64_t acc_bytes = acc_lds ? (int64_t)in.K * G * R * 8 : 0;
         for (int m = 1; m <= kMaxWavesPerCU / (W + 1); ++m) {  // workgroups per CU
           if (force_wg_per_cu && m != force_wg_per_cu) continue;
@@ -501,11 +520,11 @@ Plan choose_global_plan(const PlanInput &in) {
   };
   for (int W : {1, 2, 4, 8, 16}) {
     if (force_waves && W != force_waves) continue;
-    for (int R = 32; R <= 64 * W; R *= 2) {
+    for (int R = min_rows(in); R <= 64 * W; R *= 2) {
       if (force_rows && R != force_rows) continue;
       const int G = 64 * W / R;
       if (G > 1 && (int64_t)G * 4 > in.n_trees) continue;  // a few trees per lane group
-      const int64_t lds = (int64_t)in.F * R * 4 + (int64_t)in.K * G * R * 8;
+      const int64_t lds = (int64_t)in.F * R * in.x_bytes + (int64_t)in.K * G * R * 8;
       if (lds > kLdsBytesPerCU) continue;
       const int m = (int)std::min<int64_t>(kLdsBytesPerCU / lds, kMaxWavesPerCU / W);
       if (m < 1) continue;
@@ -527,22 +546,105 @@ Plan choose_global_plan(const PlanInput &in) {
   return best;
 }
 
-void ragged_chunks(bridger_forest *h, int64_t chunk_bytes) {
-  h->ragged_chunk_first.assign(1, 0);
-  h->ragged_chunk_rec.assign(1, 0);
+// Cut the RAGGED trees into chunks of at most chunk_bytes (whole trees, in kernel order).
+int32_t ragged_chunks(const bridger_forest *h, int64_t chunk_bytes, std::vector<int32_t> &first,
+                      std::vector<int32_t> &rec) {
+  first.assign(1, 0);
+  rec.assign(1, 0);
   int64_t cur = 0;
   for (int32_t k = 0; k < h->n_trees; ++k) {
     const int64_t tbytes = 8 * (int64_t)(h->ragged_tree_start[k + 1] - h->ragged_tree_start[k]);
     if (cur > 0 && cur + tbytes > chunk_bytes) {
-      h->ragged_chunk_first.push_back(k);
-      h->ragged_chunk_rec.push_back(h->ragged_tree_start[k]);
+      first.push_back(k);
+      rec.push_back(h->ragged_tree_start[k]);
       cur = 0;
     }
     cur += tbytes;
   }
-  h->ragged_chunk_first.push_back(h->n_trees);
-  h->ragged_chunk_rec.push_back(h->ragged_tree_start[h->n_trees]);
-  h->ragged_plan.n_chunks = (int32_t)h->ragged_chunk_first.size() - 1;
+  first.push_back(h->n_trees);
+  rec.push_back(h->ragged_tree_start[h->n_trees]);
+  return (int32_t)first.size() - 1;
+}
+
+// The chunked plan, or the global-node plan when the chunked one leaves fewer than eight
+// compute waves per CU (wide rows) and, for PERFECT, the forest fits in L2, or when a RAGGED
+// forest does not fit in L2.
+Plan pick_plan(const PlanInput &pin) {
+  Plan p = choose_plan(pin);
+  const int gmode = env_int("BRIDGER_GLOBAL", -1);  // tuning override: 0 off, 1 on
+  if (gmode == 0) return p;
+  Plan g = choose_global_plan(pin);
+  if (g.waves == 0) return p;
+  if (!pin.perfect) g.ilp = env_int("BRIDGER_ILP", 2) == 1 ? 1 : 2;  // runs per lane
+  const bool few = p.waves == 0 || p.waves_per_cu < kMinWavesPerCU;
+  const bool fits = !pin.perfect || pin.forest_bytes <= kL2BytesPerXcd;
+  if (gmode == 1 || (few && fits && g.waves_per_cu > p.waves_per_cu)) return g;
+  // a ragged forest larger than L2 is restaged from memory for every row tile; the walk
+  // touches only the few nodes on each row's path
+  if (!pin.perfect && pin.forest_bytes > kL2BytesPerXcd) return g;
+  return p;
+}
+
+// Per feature, the distinct thresholds ascending; false if a feature has 2^16 or more.
+bool build_quantization(bridger_forest *h, const int32_t *feat, const float *thr,
+                        const int32_t *left) {
+  std::vector<std::vector<float>> per(h->F);
+  for (int64_t i = 0; i < h->n_nodes; ++i)
+    if (left[i] != -1) per[feat[i]].push_back(thr[i] == 0.0f ? 0.0f : thr[i]);
+  size_t max_n = 0;
+  h->q_off.assign(h->F + 1, 0);
+  h->q_values.clear();
+  for (int32_t f = 0; f < h->F; ++f) {
+    std::vector<float> &u = per[f];
+    std::sort(u.begin(), u.end());
+    u.erase(std::unique(u.begin(), u.end()), u.end());
+    max_n = std::max(max_n, u.size());
+    h->q_off[f] = (int32_t)h->q_values.size();
+    h->q_values.insert(h->q_values.end(), u.begin(), u.end());
+  }
+  h->q_off[h->F] = (int32_t)h->q_values.size();
+  // a bin ranges over 0 .. n (n = the feature's threshold count, for values above all of them)
+  h->bin_bytes = max_n <= 255 ? 1 : (max_n <= 65535 ? 2 : 0);
+  return h->bin_bytes != 0;
+}
+
+uint32_t rank_of(const bridger_forest *h, int32_t f, float t) {
+  const float *b = h->q_values.data() + h->q_off[f];
+  const float *e = h->q_values.data() + h->q_off[f + 1];
+  return (uint32_t)(std::lower_bound(b, e, t == 0.0f ? 0.0f : t) - b);
+}
+
+// PERFECT traversal copy for bins: {rank, byte offset f * R * bin_bytes of the feature's row}.
+void build_perfect_btrav(bridger_forest *h) {
+  const int D = h->perfect_depth;
+  const int tb = h->perfect_tree_bytes;
+  const uint32_t row_bytes = (uint32_t)h->perfect_bplan.rows_per_wg * (uint32_t)h->bin_bytes;
+  h->perfect_btrav = h->perfect_blob;
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    uint8_t *blk = h->perfect_btrav.data() + (size_t)k * tb;
+    for (int m = 1; m < (1 << D); ++m) {
+      float th;
+      uint32_t f;
+      std::memcpy(&th, blk + 8 * m, 4);
+      std::memcpy(&f, blk + 8 * m + 4, 4);
+      const uint32_t r = rank_of(h, (int32_t)f, th), off = f * row_bytes;
+      std::memcpy(blk + 8 * m, &r, 4);
+      std::memcpy(blk + 8 * m + 4, &off, 4);
+    }
+  }
+}
+
+// RAGGED records for bins: an internal record's threshold becomes its rank.
+void build_ragged_brec(bridger_forest *h) {
+  h->ragged_brec = h->ragged_rec;
+  for (uint64_t &rec : h->ragged_brec) {
+    const uint32_t meta = (uint32_t)(rec >> 32);
+    if (meta & (uint32_t)kLeafFlag) continue;
+    float th;
+    const uint32_t w = (uint32_t)rec;
+    std::memcpy(&th, &w, 4);
+    rec = (uint64_t)rank_of(h, (int32_t)(meta >> 16), th) | ((uint64_t)meta << 32);
+  }
 }
 
 // ------------------------------------------------------------------- device io
@@ -573,6 +675,9 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_tree_order);
   free_dev(h->d_perfect_trav);
   free_dev(h->d_perfect_roots);
+  for (void **q : {&h->d_q_values, &h->d_q_off, &h->d_perfect_btrav, &h->d_ragged_brec,
+                   &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec})
+    free_dev(*q);
   for (DevArrays *d : {&h->d_perfect, &h->d_ragged, &h->d_direct}) {
     free_dev(d->nodes);
     free_dev(d->tree_start);
@@ -601,6 +706,17 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_ragged.chunk_rec, h->ragged_chunk_rec)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_ragged.leaf_map, h->ragged_rec_node)) != BRIDGER_OK) return s;
   }
+  if (h->bin_bytes) {
+    if ((s = upload(&h->d_q_values, h->q_values)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_q_off, h->q_off)) != BRIDGER_OK) return s;
+  }
+  if (h->perfect_bok)
+    if ((s = upload(&h->d_perfect_btrav, h->perfect_btrav, 1024)) != BRIDGER_OK) return s;
+  if (h->ragged_bok) {
+    if ((s = upload(&h->d_ragged_brec, h->ragged_brec, 1024)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_ragged_bchunk_first, h->ragged_bchunk_first)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_ragged_bchunk_rec, h->ragged_bchunk_rec)) != BRIDGER_OK) return s;
+  }
   if ((s = upload(&h->d_direct.nodes, h->direct_rec)) != BRIDGER_OK) return s;
   if ((s = upload(&h->d_direct.tree_start, h->direct_root)) != BRIDGER_OK) return s;
   if ((s = upload(&h->d_direct.leaf_map, h->direct_rec_node)) != BRIDGER_OK) return s;
@@ -619,7 +735,7 @@ int32_t resolve_auto(const bridger_forest *h) {
 }
 
 bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_rows,
-                             int32_t n_features, const void *out) {
+                             int32_t n_features, const void *out, int x_align = 4) {
   if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
   if (h->host_only) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "handle was created host-only");
   if (n_rows < 0) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_rows < 0");
@@ -628,8 +744,9 @@ bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_r
                 "n_features " + std::to_string(n_features) + " != forest's " + std::to_string(h->F));
   if (n_rows == 0) return BRIDGER_OK;
   if (!X || !out) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null X or output pointer");
-  if (((uintptr_t)X & 3) || ((uintptr_t)out & 3))
-    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "X and output must be 4-byte aligned");
+  if (((uintptr_t)X % (uintptr_t)x_align) || ((uintptr_t)out & 3))
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT,
+                "X must be aligned to its element size and the output to 4 bytes");
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != h->device)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "the handle's device is not current");
@@ -638,23 +755,33 @@ bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_r
   return BRIDGER_OK;
 }
 
-bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int32_t n_features,
-                          float *out, int32_t *out_leaf, void *stream) {
+// X is fp32 rows, or (binned) rows of bin_bytes-wide bins from bridger_forest_bin.
+bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int32_t n_features,
+                          float *out, int32_t *out_leaf, void *stream, bool binned) {
   g_last_error.clear();
-  bridger_status s = check_predict(h, X, n_rows, n_features, out ? (void *)out : (void *)out_leaf);
+  if (binned && h && !h->bin_bytes)
+    return fail(BRIDGER_ERR_UNSUPPORTED, "a feature has 65536 or more distinct thresholds");
+  const int xsz = binned && h ? h->bin_bytes : 4;
+  bridger_status s = check_predict(h, X, n_rows, n_features, out ? (void *)out : (void *)out_leaf,
+                                   xsz);
   if (s != BRIDGER_OK || n_rows == 0) return s;
+  if (binned && !((h->kernel_active == kPerfect && h->perfect_bok) ||
+                  (h->kernel_active == kRagged && h->ragged_bok)))
+    return fail(BRIDGER_ERR_UNSUPPORTED,
+                "binned prediction runs on the perfect and ragged kernels only");
   const uint8_t *xb = (const uint8_t *)X;
   const uint8_t *ob = out ? (const uint8_t *)out : (const uint8_t *)out_leaf;
-  const size_t xbytes = (size_t)n_rows * h->F * 4;
+  const size_t xbytes = (size_t)n_rows * h->F * xsz;
   const size_t obytes = (size_t)n_rows * (out ? h->K : h->n_trees) * 4;
   if (xb < ob + obytes && ob < xb + xbytes)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
 
   LaunchArgs a{};
-  a.X = X;
+  a.X = (const float *)X;
   a.n_rows = n_rows;
   a.F = h->F;
-  a.x_vec4 = ((uintptr_t)X % 16 == 0) && (h->F % 4 == 0);
+  a.x_bytes = xsz;
+  a.x_vec4 = ((uintptr_t)X % 16 == 0) && (((int64_t)h->F * xsz) % 16 == 0);
   a.out = out;
   a.out_leaf = out_leaf;
   a.class_begin = (const int32_t *)h->d_class_begin;
@@ -667,29 +794,33 @@ bridger_status do_predict(bridger_forest *h, const float *X, int64_t n_rows, int
   a.transform = h->transform;
   int err = 0;
   if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
-    const Plan &p = h->kernel_active == kPerfect ? h->perfect_plan : h->ragged_plan;
-    const DevArrays &d = h->kernel_active == kPerfect ? h->d_perfect : h->d_ragged;
-    a.nodes = h->kernel_active == kPerfect ? (const uint8_t *)h->d_perfect_trav
-                                           : (const uint8_t *)d.nodes;
+    const bool perfect = h->kernel_active == kPerfect;
+    const Plan &p = perfect ? (binned ? h->perfect_bplan : h->perfect_plan)
+                            : (binned ? h->ragged_bplan : h->ragged_plan);
+    const DevArrays &d = perfect ? h->d_perfect : h->d_ragged;
+    if (perfect)
+      a.nodes = (const uint8_t *)(binned ? h->d_perfect_btrav : h->d_perfect_trav);
+    else
+      a.nodes = (const uint8_t *)(binned ? h->d_ragged_brec : d.nodes);
     a.finite_thresholds = h->finite_thresholds ? 1 : 0;
     a.roots = (const uint32_t *)h->d_perfect_roots;
     a.tree_start = (const int32_t *)d.tree_start;
-    a.chunk_first = (const int32_t *)d.chunk_first;
-    a.chunk_rec = (const int32_t *)d.chunk_rec;
+    a.chunk_first = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_first : d.chunk_first);
+    a.chunk_rec = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_rec : d.chunk_rec);
     a.leaf_map = (const int32_t *)d.leaf_map;
     a.tree_bytes = h->perfect_tree_bytes;
     a.trees_per_chunk = p.trees_per_chunk;
     a.n_chunks = p.n_chunks;
     a.rows_per_wg = p.rows_per_wg;
-    a.log2_row_bytes = ilog2(4 * (int64_t)p.rows_per_wg);
+    a.log2_row_bytes = ilog2((int64_t)xsz * p.rows_per_wg);
     a.groups = p.groups;
     a.chunk_bytes = p.chunk_bytes;
     a.lds_x_off = p.global_nodes ? 0 : 2 * p.chunk_bytes;
-    a.lds_acc_off = a.lds_x_off + h->F * p.rows_per_wg * 4;
+    a.lds_acc_off = a.lds_x_off + h->F * p.rows_per_wg * xsz;
     a.acc_in_lds = p.acc_in_lds;
     a.ilp = p.ilp;
     const int64_t n_wg = (n_rows + p.rows_per_wg - 1) / p.rows_per_wg;
-    const bool fixed = h->kernel_active == kPerfect && !out_leaf && h->K == 1 &&
+    const bool fixed = h->kernel_active == kPerfect && !binned && !out_leaf && h->K == 1 &&
                        p.groups == 1 && p.waves <= 8 && h->finite_thresholds && p.ilp == 4 &&
                        perfect_fixed_ok(h->perfect_depth, p.trees_per_chunk) &&
                        p.chunk_bytes == p.trees_per_chunk * h->perfect_tree_bytes &&
@@ -839,41 +970,56 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       pack_perfect(h, D, tree_offsets, feature, threshold, left, right, value);
       PlanInput pin{1 << 20, n_features, n_classes, n_trees,
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
-      h->perfect_plan = choose_plan(pin);
-      // Wide rows: when streaming the forest through LDS chunks leaves few waves per CU and
-      // the forest fits in L2, read the records from global memory instead.
-      const int gmode = env_int("BRIDGER_GLOBAL", -1);  // tuning override: 0 off, 1 on
-      if (gmode != 0 && D <= kMaxPerfectDepth) {
-        const Plan g = choose_global_plan(pin);
-        const bool few = h->perfect_plan.waves == 0 ||
-                         h->perfect_plan.waves_per_cu < kMinWavesPerCU;
-        if (g.waves > 0 &&
-            (gmode == 1 || (few && pin.forest_bytes <= kL2BytesPerXcd &&
-                            g.waves_per_cu > h->perfect_plan.waves_per_cu)))
-          h->perfect_plan = g;
-      }
+      h->perfect_plan = pick_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
       if (h->perfect_ok) build_perfect_trav(h);
     }
-    if (pack_ragged(h, tree_offsets, feature, threshold, left, right, value)) {
+    const bool ragged_packed = pack_ragged(h, tree_offsets, feature, threshold, left, right, value);
+    if (ragged_packed) {
       PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
                     (int32_t)std::min<int64_t>(h->ragged_max_tree_bytes, INT32_MAX), false, visits};
-      h->ragged_plan = choose_plan(pin);
-      // Big forests on wide rows: when the chunked plan leaves few waves per CU, read the
-      // records from global memory (the forest stays in L2 / the last-level cache).
-      const int gmode = env_int("BRIDGER_GLOBAL", -1);
-      if (gmode != 0) {
-        Plan g = choose_global_plan(pin);
-        g.ilp = env_int("BRIDGER_ILP", 2) == 1 ? 1 : 2;  // runs per lane
-        const bool few = h->ragged_plan.waves == 0 ||
-                         h->ragged_plan.waves_per_cu < kMinWavesPerCU;
-        if (g.waves > 0 &&
-            (gmode == 1 || (few && g.waves_per_cu > h->ragged_plan.waves_per_cu)))
-          h->ragged_plan = g;
-      }
+      h->ragged_plan = pick_plan(pin);
       h->ragged_ok = h->ragged_plan.waves > 0;
       if (h->ragged_ok && !h->ragged_plan.global_nodes)
-        ragged_chunks(h, h->ragged_plan.chunk_bytes);
+        h->ragged_plan.n_chunks = ragged_chunks(h, h->ragged_plan.chunk_bytes,
+                                                h->ragged_chunk_first, h->ragged_chunk_rec);
+    }
+    // binned variants of the same layouts (used by bridger_forest_predict_binned)
+    if (build_quantization(h, feature, threshold, left)) {
+      if (h->perfect_ok) {
+        PlanInput pin{1 << 20, n_features, n_classes, n_trees, (double)h->perfect_blob.size(),
+                      h->perfect_tree_bytes, true, visits, h->bin_bytes};
+        h->perfect_bplan = pick_plan(pin);
+        h->perfect_bok = h->perfect_bplan.waves > 0;
+        if (h->perfect_bok) build_perfect_btrav(h);
+      }
+      if (ragged_packed) {
+        PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
+                      (int32_t)std::min<int64_t>(h->ragged_max_tree_bytes, INT32_MAX), false,
+                      visits, h->bin_bytes};
+        h->ragged_bplan = pick_plan(pin);
+        h->ragged_bok = h->ragged_bplan.waves > 0;
+        if (h->ragged_bok) {
+          build_ragged_brec(h);
+          if (!h->ragged_bplan.global_nodes)
+            h->ragged_bplan.n_chunks = ragged_chunks(h, h->ragged_bplan.chunk_bytes,
+                                                     h->ragged_bchunk_first, h->ragged_bchunk_rec);
+        }
+      }
+    }
+    if (env_int("BRIDGER_LOG", 0)) {
+      auto show = [](const char *what, const Plan &p) {
+        if (p.waves)
+          std::fprintf(stderr,
+                       "[bridger] %s plan: W=%d R=%d G=%d U=%d global=%d waves/CU=%d chunk=%d "
+                       "ct=%d chunks=%d lds=%d\n",
+                       what, p.waves, p.rows_per_wg, p.groups, p.ilp, p.global_nodes,
+                       p.waves_per_cu, p.chunk_bytes, p.trees_per_chunk, p.n_chunks, p.lds_bytes);
+      };
+      show("perfect", h->perfect_plan);
+      show("perfect binned", h->perfect_bplan);
+      show("ragged", h->ragged_plan);
+      show("ragged binned", h->ragged_bplan);
     }
     h->kernel_active = resolve_auto(h);
     const int forced = env_int("BRIDGER_KERNEL", 0);
@@ -924,13 +1070,61 @@ bridger_status bridger_forest_create(int32_t n_trees, const int64_t *tree_offset
 
 bridger_status bridger_forest_predict(bridger_forest_t h, const float *X, int64_t n_rows,
                                       int32_t n_features, float *out, void *stream) {
-  return do_predict(h, X, n_rows, n_features, out, nullptr, stream);
+  return do_predict(h, X, n_rows, n_features, out, nullptr, stream, false);
 }
 
 bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X, int64_t n_rows,
                                              int32_t n_features, int32_t *out_leaf,
                                              void *stream) {
-  return do_predict(h, X, n_rows, n_features, nullptr, out_leaf, stream);
+  return do_predict(h, X, n_rows, n_features, nullptr, out_leaf, stream, false);
+}
+
+bridger_status bridger_forest_bin_info(bridger_forest_t h, int32_t *bin_bytes,
+                                       int64_t *n_thresholds) {
+  g_last_error.clear();
+  if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
+  if (bin_bytes) *bin_bytes = h->bin_bytes;
+  if (n_thresholds) *n_thresholds = (int64_t)h->q_values.size();
+  return BRIDGER_OK;
+}
+
+bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_rows,
+                                  int32_t n_features, void *Xq, void *stream) {
+  g_last_error.clear();
+  if (h && !h->bin_bytes)
+    return fail(BRIDGER_ERR_UNSUPPORTED, "a feature has 65536 or more distinct thresholds");
+  bridger_status s = check_predict(h, X, n_rows, n_features, Xq, 4);
+  if (s != BRIDGER_OK || n_rows == 0) return s;
+  if ((uintptr_t)Xq % (uintptr_t)h->bin_bytes)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "Xq must be aligned to the bin size");
+  const uint8_t *xb = (const uint8_t *)X, *qb = (const uint8_t *)Xq;
+  const size_t xbytes = (size_t)n_rows * h->F * 4, qbytes = (size_t)n_rows * h->F * h->bin_bytes;
+  if (xb < qb + qbytes && qb < xb + xbytes)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "Xq overlaps X");
+  LaunchArgs a{};
+  a.X = X;
+  a.n_rows = n_rows;
+  a.F = h->F;
+  a.x_bytes = h->bin_bytes;
+  a.q_values = (const float *)h->d_q_values;
+  a.q_off = (const int32_t *)h->d_q_off;
+  a.xq = Xq;
+  const int err = launch_bin(a, stream);
+  if (err != 0)
+    return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
+                                        hipGetErrorString((hipError_t)err));
+  return BRIDGER_OK;
+}
+
+bridger_status bridger_forest_predict_binned(bridger_forest_t h, const void *Xq, int64_t n_rows,
+                                             int32_t n_features, float *out, void *stream) {
+  return do_predict(h, Xq, n_rows, n_features, out, nullptr, stream, true);
+}
+
+bridger_status bridger_forest_predict_binned_leaves(bridger_forest_t h, const void *Xq,
+                                                    int64_t n_rows, int32_t n_features,
+                                                    int32_t *out_leaf, void *stream) {
+  return do_predict(h, Xq, n_rows, n_features, nullptr, out_leaf, stream, true);
 }
 
 bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,
@@ -1034,6 +1228,8 @@ bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const vo
     return BRIDGER_OK;
   };
   if (which == 3) return give(h->tree_order.data(), h->tree_order.size() * 4);
+  if (which == 5) return give(h->q_values.data(), h->q_values.size() * 4);
+  if (which == 6) return give(h->q_off.data(), h->q_off.size() * 4);
   switch (h->kernel_active) {
     case kPerfect:
     case kGemm:

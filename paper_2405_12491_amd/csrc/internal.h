@@ -105,11 +105,18 @@ struct LaunchArgs {
   int32_t ilp;                 // PERFECT: trees walked at once per lane (1, 2 or 4)
   int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)
   const uint32_t *roots;       // PERFECT: per kernel tree the root's traversal record (2 words)
+  int32_t x_bytes;             // element of X and of the LDS tile: 4 (fp32) or 2 / 1 (bins)
+  const float *q_values;       // binning: sorted distinct thresholds of every feature
+  const int32_t *q_off;        // binning: [F + 1] offsets into q_values
+  void *xq;                    // binning: output bins [n_rows, F] of x_bytes each
 };
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                    void *stream);
+int launch_perfect_binned(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                          void *stream);
+int launch_bin(const LaunchArgs &a, void *stream);
 int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                           void *stream);
 int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

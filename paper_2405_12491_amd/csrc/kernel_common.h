@@ -41,6 +41,12 @@ typedef __attribute__((address_space(3))) uint8_t lds_byte;
 __device__ __forceinline__ float lds_f32(const uint8_t *, uint32_t addr) {
   return *(const __attribute__((address_space(3))) float *)(uintptr_t)addr;
 }
+__device__ __forceinline__ uint32_t lds_u16(const uint8_t *, uint32_t addr) {
+  return *(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)addr;
+}
+__device__ __forceinline__ uint32_t lds_u8(const uint8_t *, uint32_t addr) {
+  return *(const __attribute__((address_space(3))) uint8_t *)(uintptr_t)addr;
+}
 __device__ __forceinline__ uint2 lds_u64(const uint8_t *, uint32_t addr) {
   const uint64_t v = *(const __attribute__((address_space(3))) uint64_t *)(uintptr_t)addr;
   return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
@@ -128,6 +134,62 @@ __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a
   } else {
     for (int f = 0; f < a.F; ++f) put(f, xr[f]);
   }
+}
+
+// Byte offset of row r's element inside a feature's row of the LDS tile, for elements of XB
+// bytes.  fp32 (XB = 4): 4r.  Bins (XB = 2 or 1) pack P = 4 / XB rows per 32-bit word: row r
+// sits in word (r mod 32) + 32 (r div 32P), sub-word (r div 32) mod P, so the 32 rows of a
+// half-wave always hit 32 different banks whatever features they read (R is a multiple of 32P).
+template <int XB>
+__device__ __forceinline__ uint32_t tile_row_off(int r) {
+  if (XB == 4) return 4u * (uint32_t)r;
+  constexpr int P = 4 / XB;
+  return 4u * (uint32_t)((r & 31) + 32 * (r / (32 * P))) + (uint32_t)(XB * ((r >> 5) & (P - 1)));
+}
+
+// Load this lane's row of bins (F elements of XB bytes each, row-major in global memory) into
+// the feature-major LDS tile (zeros past the last row).  x_vec4: rows 16-byte aligned.
+template <int XB>
+__device__ __forceinline__ void load_row_tile_binned(uint8_t *smem, const LaunchArgs &a, int r,
+                                                     int64_t row, bool row_ok) {
+  static_assert(XB == 1 || XB == 2, "bins are 8 or 16 bits");
+  const uint32_t stride = (uint32_t)a.rows_per_wg * XB;  // one feature's row of the tile
+  const uint32_t base = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
+  auto put = [&](int f, uint32_t v) {
+    const uint32_t addr = base + (uint32_t)f * stride;
+    if (XB == 2) *(__attribute__((address_space(3))) uint16_t *)(uintptr_t)addr = (uint16_t)v;
+    else *(__attribute__((address_space(3))) uint8_t *)(uintptr_t)addr = (uint8_t)v;
+  };
+  if (!row_ok) {
+    for (int f = 0; f < a.F; ++f) put(f, 0u);
+    return;
+  }
+  const uint8_t *xr = reinterpret_cast<const uint8_t *>(a.X) + row * (int64_t)a.F * XB;
+  if (a.x_vec4) {
+    constexpr int E = 16 / XB;  // elements per 16-byte load
+    const uint4 *x4 = reinterpret_cast<const uint4 *>(xr);
+    const int n4 = (a.F * XB) >> 4;
+    for (int i = 0; i < n4; ++i) {
+      const uint4 v = x4[i];
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t word = w[(e * XB) >> 2];
+        put(i * E + e, (word >> (8 * ((e * XB) & 3))) & (XB == 2 ? 0xFFFFu : 0xFFu));
+      }
+    }
+  } else {
+    for (int f = 0; f < a.F; ++f)
+      put(f, XB == 2 ? (uint32_t)reinterpret_cast<const uint16_t *>(xr)[f] : (uint32_t)xr[f]);
+  }
+}
+
+// The tile load for element size XB (fp32 with NaN stored as +inf when NAN_TO_INF).
+template <int XB, bool NAN_TO_INF>
+__device__ __forceinline__ void load_tile_any(uint8_t *smem, const LaunchArgs &a, int r,
+                                              int64_t row, bool row_ok) {
+  if constexpr (XB == 4) load_row_tile<NAN_TO_INF>(smem, a, r, row, row_ok);
+  else load_row_tile_binned<XB>(smem, a, r, row, row_ok);
 }
 
 __device__ __forceinline__ double sigmoid_d(double z) {

@@ -1,140 +1,19 @@
-// perfect.hip -- gfx950 kernel for forests of perfect trees of one depth 1..10: any number of
-// classes, lane groups, scores or leaf ids, finite or infinite thresholds.
-#include "perfect_walk.h"
+// perfect.hip -- the generic PERFECT kernel on fp32 feature tiles (finite or infinite
+// thresholds); binned tiles are instantiated in perfect_binned.hip.
+#include "perfect_kernel.h"
 
 namespace bridger {
-
-template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN>
-__global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const int tid = threadIdx.x;
-  const int R = a.rows_per_wg, G = a.groups;
-  const uint32_t tb = (uint32_t)a.tree_bytes;
-  const int T = a.n_trees, CT = a.trees_per_chunk;
-  if (tid >= G * R) {
-    staging_wave(smem, a.n_chunks, (uint32_t)a.chunk_bytes, tid & 63, (LEAVES || SIMPLE) ? 0 : 1,
-                 [&](int c) {
-                   const int n0 = c * CT, n1 = (n0 + CT < T) ? n0 + CT : T;
-                   return std::make_pair(a.nodes + (size_t)n0 * tb, (n1 - n0) * (int)tb);
-                 });
-    return;
-  }
-  const int r = tid & (R - 1);
-  // with R >= 64 a wave lies inside one lane group, so the group index (and every tree
-  // address derived from it) is wave-uniform and lives in scalar registers
-  const int g = SIMPLE ? 0 : (R >= 64 ? __builtin_amdgcn_readfirstlane(tid / R) : tid / R);
-  const int64_t row = (int64_t)blockIdx.x * R + r;
-  const bool row_ok = row < a.n_rows;
-  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
-  // leaf j of a tree is at base + 8 * 2^D + 4j, i.e. base + 4m + 4 * 2^D for final slot m
-  constexpr uint32_t kLeafOff = 4u << D;
-  constexpr uint32_t kFirstLeaf = 1u << D;
-
-  if (g == 0) load_row_tile<FIN>(smem, a, r, row, row_ok);
-  __syncthreads();
-
-  double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
-  const int slot_stride = G * R;
-  ClassAcc ca;
-  ca.k = 0;
-  ca.acc = SIMPLE ? (a.aggregate == 0 ? (double)a.base[0] : 0.0) : class_init(a, 0, g == 0);
-  ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
-
-  // leaf ids or leaf values of N walked trees, kernel trees q .. q + N - 1
-  auto finish = [&](auto &m, int q, uint32_t b0) {
-    constexpr int N = sizeof(m) / sizeof(m[0]);
-    if (LEAVES) {
-#pragma unroll
-      for (int u = 0; u < N; ++u) {
-        if (row_ok) {
-          const int t = q + u;
-          a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
-              a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
-        }
-      }
-    } else {
-      float lv[N];
-#pragma unroll
-      for (int u = 0; u < N; ++u) lv[u] = lds_f32(smem, (m[u] << 2) + b0 + (uint32_t)u * tb + kLeafOff);
-#pragma unroll
-      for (int u = 0; u < N; ++u) {
-        if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
-        ca.acc += (double)lv[u];
-      }
-    }
-  };
-
-  for (int c = 0; c < a.n_chunks; ++c) {
-    const int t0 = c * CT;
-    const int t1 = (t0 + CT < T) ? t0 + CT : T;
-    const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
-    // whole groups of U trees, then (only when the chunk's tree count leaves one) a partial
-    // group walked one tree at a time
-    int q = t0 + U * g;
-    for (; q + U <= t1; q += U * G) {
-      const uint32_t b0 = buf + (uint32_t)(q - t0) * tb;
-      uint32_t m[U];
-      walk_trees<D, U, FIN>(smem, b0, tb, lane_off, m);
-      finish(m, q, b0);
-    }
-    for (; q < t1; ++q) {
-      const uint32_t b0 = buf + (uint32_t)(q - t0) * tb;
-      uint32_t m[1];
-      walk_trees<D, 1, FIN>(smem, b0, tb, lane_off, m);
-      finish(m, q, b0);
-    }
-    __syncthreads();
-  }
-  if (LEAVES) return;
-  if (SIMPLE) {
-    if (row_ok) {
-      double z = ca.acc;
-      if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
-      a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
-    }
-    return;
-  }
-  class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
-  __syncthreads();
-  if (g == 0) {
-    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
-    for (int k = 0; k < a.K; ++k) {
-      double s = z[k * slot_stride];
-      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
-      z[k * slot_stride] = s;
-    }
-    if (row_ok) finalize_store(a, z, slot_stride, row);
-  }
-}
-
-// ---------------------------------------------------------------------- launchers
-template <int D, bool FIN>
-static int launch_perfect_df(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
-                             void *stream) {
-  const bool simple = a.K == 1 && a.groups == 1;
-  const int threads = 64 * (waves + 1);  // + the staging wave
-  // any plan works with any U (a chunk's last partial group is walked one tree at a time);
-  // lane-group plans pick U to fit the LDS
-  if (a.out_leaf)
-    return launch_common(perfect_kernel<D, 4, true, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-  if (simple)
-    return launch_common(perfect_kernel<D, 4, false, true, FIN>, threads, n_wg, lds_bytes, stream, a);
-  if (a.ilp == 1)
-    return launch_common(perfect_kernel<D, 1, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-  if (a.ilp == 2)
-    return launch_common(perfect_kernel<D, 2, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(perfect_kernel<D, 4, false, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-}
 
 template <int D>
 static int launch_perfect_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                             void *stream) {
-  return a.finite_thresholds ? launch_perfect_df<D, true>(a, waves, n_wg, lds_bytes, stream)
-                             : launch_perfect_df<D, false>(a, waves, n_wg, lds_bytes, stream);
+  return a.finite_thresholds ? launch_perfect_dfx<D, true, 4>(a, waves, n_wg, lds_bytes, stream)
+                             : launch_perfect_dfx<D, false, 4>(a, waves, n_wg, lds_bytes, stream);
 }
 
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                    void *stream) {
+  if (a.x_bytes != 4) return launch_perfect_binned(depth, a, waves, n_wg, lds_bytes, stream);
   switch (depth) {
     case 1: return launch_perfect_d<1>(a, waves, n_wg, lds_bytes, stream);
     case 2: return launch_perfect_d<2>(a, waves, n_wg, lds_bytes, stream);

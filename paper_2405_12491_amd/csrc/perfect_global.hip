@@ -11,7 +11,7 @@
 
 namespace bridger {
 
-template <int D, int U, bool LEAVES, bool FIN>
+template <int D, int U, bool LEAVES, bool FIN, int XB>
 __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -22,11 +22,11 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   const int g = R >= 64 ? __builtin_amdgcn_readfirstlane(tid / R) : tid / R;
   const int64_t row = (int64_t)blockIdx.x * R + r;
   const bool row_ok = row < a.n_rows;
-  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
   constexpr uint32_t kLeafOff = 4u << D;
   constexpr uint32_t kFirstLeaf = 1u << D;
 
-  if (g == 0) load_row_tile<FIN>(smem, a, r, row, row_ok);
+  if (g == 0) load_tile_any<XB, FIN>(smem, a, r, row, row_ok);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -65,12 +65,12 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   int q = t_begin;
   for (; q + U <= t_end; q += U) {
     uint32_t m[U];
-    walk_trees_global<D, U, FIN>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
+    walk_trees_global<D, U, FIN, XB>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
     finish(m, q);
   }
   for (; q < t_end; ++q) {
     uint32_t m[1];
-    walk_trees_global<D, 1, FIN>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
+    walk_trees_global<D, 1, FIN, XB>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
     finish(m, q);
   }
   if (LEAVES) return;
@@ -88,22 +88,24 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
 }
 
 // ---------------------------------------------------------------------- launchers
-template <int D, bool FIN>
-static int launch_global_df(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
-                            void *stream) {
+template <int D, bool FIN, int XB>
+static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                             void *stream) {
   const int threads = 64 * waves;
   if (a.out_leaf)
-    return launch_common(perfect_global_kernel<D, 4, true, FIN>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_global_kernel<D, 4, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 4)
-    return launch_common(perfect_global_kernel<D, 4, false, FIN>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(perfect_global_kernel<D, 8, false, FIN>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_global_kernel<D, 4, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(perfect_global_kernel<D, 8, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
 }
 
 template <int D>
 static int launch_global_d(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                            void *stream) {
-  return a.finite_thresholds ? launch_global_df<D, true>(a, waves, n_wg, lds_bytes, stream)
-                             : launch_global_df<D, false>(a, waves, n_wg, lds_bytes, stream);
+  if (a.x_bytes == 2) return launch_global_dfx<D, true, 2>(a, waves, n_wg, lds_bytes, stream);
+  if (a.x_bytes == 1) return launch_global_dfx<D, true, 1>(a, waves, n_wg, lds_bytes, stream);
+  return a.finite_thresholds ? launch_global_dfx<D, true, 4>(a, waves, n_wg, lds_bytes, stream)
+                             : launch_global_dfx<D, false, 4>(a, waves, n_wg, lds_bytes, stream);
 }
 
 int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

@@ -18,7 +18,28 @@ namespace bridger {
 // (denormals are kept; ties and -0 are handled by storing thresholds of zero as +0), it is
 // -inf for x = +inf and +inf for x = -inf, and a NaN feature is stored as +inf, which every
 // finite threshold sends right as the compare would.  After D levels m - 2^D is the leaf.
-template <int D, int U, bool FIN>
+// One level for one tree: record {w, offset} and the lane's feature value (element size XB).
+// Bins (XB = 2, 1): w is the threshold's rank k and x <= t_k iff bin <= k, so the step is the
+// sign bit of k - bin (both below 2^16).
+template <bool FIN, int XB>
+__device__ __forceinline__ uint32_t gather_x(const uint8_t *smem, uint32_t addr) {
+  if constexpr (XB == 4) return __float_as_uint(lds_f32(smem, addr));
+  else if constexpr (XB == 2) return lds_u16(smem, addr);
+  else return lds_u8(smem, addr);
+}
+template <bool FIN, int XB>
+__device__ __forceinline__ uint32_t step_slot(uint32_t m, uint32_t w, uint32_t x) {
+  if constexpr (XB != 4) {
+    return __builtin_amdgcn_alignbit(m, w - x, 31);
+  } else if constexpr (FIN) {
+    const float diff = __uint_as_float(w) - __uint_as_float(x);
+    return __builtin_amdgcn_alignbit(m, __float_as_uint(diff), 31);
+  } else {
+    return 2u * m + ((__uint_as_float(x) <= __uint_as_float(w)) ? 0u : 1u);
+  }
+}
+
+template <int D, int U, bool FIN, int XB = 4>
 __device__ __forceinline__ void walk_trees(const uint8_t *smem, uint32_t b0, uint32_t tb,
                                            uint32_t lane_off, uint32_t (&m)[U]) {
 #pragma unroll
@@ -26,20 +47,13 @@ __device__ __forceinline__ void walk_trees(const uint8_t *smem, uint32_t b0, uin
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     uint2 rec[U];
-    float xv[U];
+    uint32_t xv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, (m[u] << 3) + b0 + (uint32_t)u * tb);
 #pragma unroll
-    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+    for (int u = 0; u < U; ++u) xv[u] = gather_x<FIN, XB>(smem, rec[u].y + lane_off);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (FIN) {
-        const float diff = __uint_as_float(rec[u].x) - xv[u];
-        m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
-      } else {
-        m[u] = 2u * m[u] + ((xv[u] <= __uint_as_float(rec[u].x)) ? 0u : 1u);
-      }
-    }
+    for (int u = 0; u < U; ++u) m[u] = step_slot<FIN, XB>(m[u], rec[u].x, xv[u]);
   }
 }
 
@@ -78,7 +92,7 @@ __device__ __forceinline__ void walk_trees_root(const uint8_t *smem, uint32_t b0
 // The same walk over records read from global memory (L1/L2) instead of an LDS chunk: tree
 // u's block starts at byte t0_off + u * tb of `nodes`; the feature values still come from the
 // LDS tile.
-template <int D, int U, bool FIN>
+template <int D, int U, bool FIN, int XB = 4>
 __device__ __forceinline__ void walk_trees_global(const uint8_t *smem, const uint8_t *nodes,
                                                   size_t t0_off, uint32_t tb, uint32_t lane_off,
                                                   uint32_t (&m)[U]) {
@@ -87,21 +101,14 @@ __device__ __forceinline__ void walk_trees_global(const uint8_t *smem, const uin
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     uint2 rec[U];
-    float xv[U];
+    uint32_t xv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u)
       rec[u] = *reinterpret_cast<const uint2 *>(nodes + t0_off + (size_t)u * tb + (m[u] << 3));
 #pragma unroll
-    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+    for (int u = 0; u < U; ++u) xv[u] = gather_x<FIN, XB>(smem, rec[u].y + lane_off);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (FIN) {
-        const float diff = __uint_as_float(rec[u].x) - xv[u];
-        m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
-      } else {
-        m[u] = 2u * m[u] + ((xv[u] <= __uint_as_float(rec[u].x)) ? 0u : 1u);
-      }
-    }
+    for (int u = 0; u < U; ++u) m[u] = step_slot<FIN, XB>(m[u], rec[u].x, xv[u]);
   }
 }
 

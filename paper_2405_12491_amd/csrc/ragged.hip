@@ -1,14 +1,21 @@
 // ragged.hip -- gfx950 kernel for forests of trees of any shape, staged through LDS.
-#include "kernel_common.h"
+#include "perfect_walk.h"
 
 namespace bridger {
+
+// x (fp32 bits, or a bin) against an internal record's w (threshold bits, or its rank).
+template <int XB>
+__device__ __forceinline__ bool goes_right(uint32_t x, uint32_t w) {
+  if constexpr (XB == 4) return !(__uint_as_float(x) <= __uint_as_float(w));
+  else return x > w;
+}
 
 // ======================================================================== RAGGED
 // Any tree shape.  Each lane runs a state machine over its group's trees of the chunk: at an
 // internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
 // adds the value and jumps to the next tree's root.  Lanes never wait for each other inside
 // a chunk, so a short path in one tree is not padded to the wave's longest path.
-template <bool LEAVES, bool SIMPLE>
+template <bool LEAVES, bool SIMPLE, int XB>
 __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -25,11 +32,11 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   const int g = tid / R;
   const int64_t row = (int64_t)blockIdx.x * R + r;
   const bool row_ok = row < a.n_rows;
-  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
   const int shift = a.log2_row_bytes;
   const int T = a.n_trees;
 
-  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  if (g == 0) load_tile_any<XB, false>(smem, a, r, row, row_ok);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -52,10 +59,10 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
     while (addr < end) {
       const uint2 rec = lds_u64(smem, addr);
       const uint32_t meta = rec.y;
-      const float xv = lds_f32(smem, ((meta >> 16) << shift) + lane_off);
+      const uint32_t xv = gather_x<false, XB>(smem, ((meta >> 16) << shift) + lane_off);
       const bool leaf = (meta & (uint32_t)kLeafFlag) != 0;
       const uint32_t rel = meta & (uint32_t)kMaxRel;
-      const bool right = !(xv <= __uint_as_float(rec.x)) && !leaf;
+      const bool right = goes_right<XB>(xv, rec.x) && !leaf;
       if (leaf) {
         if (LEAVES) {
           if (row_ok)
@@ -105,7 +112,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
 // bottleneck).  G lane groups share the row tile; group g walks the contiguous tree range
 // [T g / G, T (g + 1) / G) split into U runs, each a state machine over its records.  No
 // chunks, no staging, one barrier before the cross-group reduction.
-template <bool LEAVES, bool SIMPLE, int U>
+template <bool LEAVES, bool SIMPLE, int U, int XB>
 __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   static_assert(U == 1 || LEAVES || SIMPLE, "several runs need one output per row");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -115,11 +122,11 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   const int g = tid / R;
   const int64_t row = (int64_t)blockIdx.x * R + r;
   const bool row_ok = row < a.n_rows;
-  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)r;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
   const int shift = a.log2_row_bytes;
   const int T = a.n_trees;
 
-  if (g == 0) load_row_tile(smem, a, r, row, row_ok);
+  if (g == 0) load_tile_any<XB, false>(smem, a, r, row, row_ok);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -148,19 +155,20 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
     for (int u = 0; u < U; ++u) any = any || idx[u] < end[u];
     if (!any) break;
     uint2 rec[U];
-    float xv[U];
+    uint32_t xv[U];
     // a finished run re-reads its last record (the result is discarded)
 #pragma unroll
     for (int u = 0; u < U; ++u) rec[u] = recs[idx[u] < end[u] ? idx[u] : end[u] - 1];
 #pragma unroll
-    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, ((rec[u].y >> 16) << shift) + lane_off);
+    for (int u = 0; u < U; ++u)
+      xv[u] = gather_x<false, XB>(smem, ((rec[u].y >> 16) << shift) + lane_off);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (idx[u] < end[u]) {
         const uint32_t meta = rec[u].y;
         const bool leaf = (meta & (uint32_t)kLeafFlag) != 0;
         const uint32_t rel = meta & (uint32_t)kMaxRel;
-        const bool right = !(xv[u] <= __uint_as_float(rec[u].x)) && !leaf;
+        const bool right = goes_right<XB>(xv[u], rec[u].x) && !leaf;
         if (leaf) {
           if (LEAVES) {
             if (row_ok)
@@ -202,24 +210,42 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
 }
 
 // ---------------------------------------------------------------------- launchers
-int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
-                         void *stream) {
+template <int XB>
+static int launch_ragged_global_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                                  void *stream) {
   const int threads = 64 * waves;
   if (a.out_leaf)
-    return launch_common(ragged_global_kernel<true, false, 1>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(ragged_global_kernel<true, false, 1, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.K != 1)
-    return launch_common(ragged_global_kernel<false, false, 1>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(ragged_global_kernel<false, false, 1, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 2)
-    return launch_common(ragged_global_kernel<false, true, 2>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(ragged_global_kernel<false, true, 1>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(ragged_global_kernel<false, true, 2, XB>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_global_kernel<false, true, 1, XB>, threads, n_wg, lds_bytes, stream, a);
+}
+
+int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                         void *stream) {
+  if (a.x_bytes == 2) return launch_ragged_global_x<2>(a, waves, n_wg, lds_bytes, stream);
+  if (a.x_bytes == 1) return launch_ragged_global_x<1>(a, waves, n_wg, lds_bytes, stream);
+  return launch_ragged_global_x<4>(a, waves, n_wg, lds_bytes, stream);
+}
+
+template <int XB>
+static int launch_ragged_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                           void *stream) {
+  const bool simple = a.K == 1;
+  const int threads = 64 * (waves + 1);  // + the staging wave
+  if (a.out_leaf)
+    return launch_common(ragged_kernel<true, false, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (simple)
+    return launch_common(ragged_kernel<false, true, XB>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_kernel<false, false, XB>, threads, n_wg, lds_bytes, stream, a);
 }
 
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {
-  const bool simple = a.K == 1;
-  const int threads = 64 * (waves + 1);  // + the staging wave
-  if (a.out_leaf) return launch_common(ragged_kernel<true, false>, threads, n_wg, lds_bytes, stream, a);
-  if (simple) return launch_common(ragged_kernel<false, true>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(ragged_kernel<false, false>, threads, n_wg, lds_bytes, stream, a);
+  if (a.x_bytes == 2) return launch_ragged_x<2>(a, waves, n_wg, lds_bytes, stream);
+  if (a.x_bytes == 1) return launch_ragged_x<1>(a, waves, n_wg, lds_bytes, stream);
+  return launch_ragged_x<4>(a, waves, n_wg, lds_bytes, stream);
 }
 
 }  // namespace bridger
