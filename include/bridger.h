@@ -181,6 +181,32 @@ bridger_status bridger_forest_predict_binned_leaves(bridger_forest_t h, const vo
                                                     int64_t n_rows, int32_t n_features,
                                                     int32_t *out_leaf, void *stream);
 
+/*
+ * Preprocessing fused into prediction (the paper's cross-domain operator fusion,
+ * Sec. 4.3, with the scalers of its CML suite): every feature value x of feature f
+ * is transformed at the row load, before any compare, the forest's thresholds
+ * applying to the transformed value x'.  Each step is done in double precision
+ * and rounded to float, so the results match scikit-learn's transforms of float32
+ * data bit for bit:
+ *   BRIDGER_PRE_MINMAX        x1 = float(x * a[f]);  x' = float(x1 + b[f])
+ *                             (MinMaxScaler: a = scale_, b = min_)
+ *   BRIDGER_PRE_CENTER_SCALE  x1 = float(x - a[f]);  x' = float(x1 / b[f])
+ *                             (StandardScaler: a = mean_, b = scale_;
+ *                              RobustScaler: a = center_, b = scale_)
+ *   BRIDGER_PRE_BINARIZE      x' = (x > a[f]) ? 1 : 0   (Binarizer; NaN gives 0)
+ *   BRIDGER_PRE_NONE          x' = x (b and a may be NULL)
+ * a and b are host arrays of n_features doubles (b unused for BINARIZE), copied at
+ * the call; the setting applies to every later predict, predict_leaves and bin on
+ * the handle.  Call it with no prediction in flight on the handle (synchronous
+ * upload).  BRIDGER_ERR_INVALID_ARGUMENT on an unknown kind or a missing array.
+ */
+#define BRIDGER_PRE_NONE 0
+#define BRIDGER_PRE_MINMAX 1
+#define BRIDGER_PRE_CENTER_SCALE 2
+#define BRIDGER_PRE_BINARIZE 3
+bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, const double *a,
+                                             const double *b);
+
 /* Shape facts.  Any output pointer may be NULL.  all_perfect = 1 when every tree
  * is perfect with one common depth (then max_depth is that depth). */
 bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,

@@ -33,6 +33,7 @@ BRIDGER_KERNEL_AUTO, BRIDGER_KERNEL_PERFECT, BRIDGER_KERNEL_RAGGED, BRIDGER_KERN
 BRIDGER_KERNEL_GEMM = 4
 KERNEL_NAMES = {0: "auto", 1: "perfect", 2: "ragged", 3: "direct", 4: "gemm"}
 BRIDGER_CREATE_HOST_ONLY = 1
+BRIDGER_PRE_NONE, BRIDGER_PRE_MINMAX, BRIDGER_PRE_CENTER_SCALE, BRIDGER_PRE_BINARIZE = 0, 1, 2, 3
 
 _lib = None
 
@@ -60,6 +61,7 @@ def load_library(path: Optional[str] = None):
     lib.bridger_forest_predict_leaves.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_info.argtypes = [P, P, P, P, P, P]
     lib.bridger_forest_bin_info.argtypes = [P, P, P]
+    lib.bridger_forest_set_preprocess.argtypes = [P, I32, P, P]
     lib.bridger_forest_bin.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_predict_binned.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_predict_binned_leaves.argtypes = [P, P, I64, I32, P, P]
@@ -75,7 +77,7 @@ def load_library(path: Optional[str] = None):
                  "bridger_forest_predict_leaves", "bridger_forest_info", "bridger_forest_set_kernel",
                  "bridger_forest_get_kernel", "bridger_forest_plan", "bridger_forest_packed",
                  "bridger_forest_bin_info", "bridger_forest_bin", "bridger_forest_predict_binned",
-                 "bridger_forest_predict_binned_leaves"):
+                 "bridger_forest_predict_binned_leaves", "bridger_forest_set_preprocess"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -127,6 +129,14 @@ def bridger_forest_predict_leaves(h, X_ptr: int, n_rows: int, n_features: int, o
                                                         int(n_features), ctypes.c_void_p(out_ptr),
                                                         ctypes.c_void_p(stream)),
            "bridger_forest_predict_leaves")
+
+
+def bridger_forest_set_preprocess(h, kind: int, a=None, b=None):
+    """a, b: per-feature parameters (float64 numpy arrays) or None."""
+    av = None if a is None else np.ascontiguousarray(a, np.float64)
+    bv = None if b is None else np.ascontiguousarray(b, np.float64)
+    _check(load_library().bridger_forest_set_preprocess(h, int(kind), _vp(av), _vp(bv)),
+           "bridger_forest_set_preprocess")
 
 
 def bridger_forest_bin_info(h) -> dict:
@@ -263,6 +273,12 @@ class Forest:
         bridger_forest_predict_leaves(self._h, X.data_ptr(), X.shape[0], self.n_features,
                                       out.data_ptr(), stream)
         return out
+
+    def set_preprocess(self, kind: int, a=None, b=None):
+        for v in (a, b):
+            if v is not None and len(v) != self.n_features:
+                raise ValueError("preprocessing parameters need one value per feature")
+        bridger_forest_set_preprocess(self._h, kind, a, b)
 
     def bin_info(self) -> dict:
         return bridger_forest_bin_info(self._h)

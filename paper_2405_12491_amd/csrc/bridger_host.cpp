@@ -112,6 +112,11 @@ struct bridger_forest {
   std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
   std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
 
+  // fused preprocessing (BRIDGER_PRE_*)
+  int32_t pre_kind = 0;
+  std::vector<double> pre_a, pre_b;
+  void *d_pre_a = nullptr, *d_pre_b = nullptr;
+
   // DIRECT
   std::vector<int32_t> direct_rec;  // 4 ints per record
   std::vector<int32_t> direct_root;
@@ -676,7 +681,7 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_perfect_trav);
   free_dev(h->d_perfect_roots);
   for (void **q : {&h->d_q_values, &h->d_q_off, &h->d_perfect_btrav, &h->d_ragged_brec,
-                   &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec})
+                   &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b})
     free_dev(*q);
   for (DevArrays *d : {&h->d_perfect, &h->d_ragged, &h->d_direct}) {
     free_dev(d->nodes);
@@ -721,6 +726,12 @@ bridger_status upload_all(bridger_forest *h) {
   if ((s = upload(&h->d_direct.tree_start, h->direct_root)) != BRIDGER_OK) return s;
   if ((s = upload(&h->d_direct.leaf_map, h->direct_rec_node)) != BRIDGER_OK) return s;
   return BRIDGER_OK;
+}
+
+void set_preprocess_args(const bridger_forest *h, LaunchArgs &a) {
+  a.pre_kind = h->pre_kind;
+  a.pre_a = (const double *)h->d_pre_a;
+  a.pre_b = (const double *)h->d_pre_b;
 }
 
 bool gemm_ok(const bridger_forest *h) {
@@ -792,6 +803,7 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   a.K = h->K;
   a.aggregate = h->aggregate;
   a.transform = h->transform;
+  set_preprocess_args(h, a);
   int err = 0;
   if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
     const bool perfect = h->kernel_active == kPerfect;
@@ -1109,6 +1121,7 @@ bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_
   a.q_values = (const float *)h->d_q_values;
   a.q_off = (const int32_t *)h->d_q_off;
   a.xq = Xq;
+  set_preprocess_args(h, a);
   const int err = launch_bin(a, stream);
   if (err != 0)
     return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
@@ -1125,6 +1138,39 @@ bridger_status bridger_forest_predict_binned_leaves(bridger_forest_t h, const vo
                                                     int64_t n_rows, int32_t n_features,
                                                     int32_t *out_leaf, void *stream) {
   return do_predict(h, Xq, n_rows, n_features, nullptr, out_leaf, stream, true);
+}
+
+bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, const double *pa,
+                                             const double *pb) {
+  g_last_error.clear();
+  if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
+  if (kind < BRIDGER_PRE_NONE || kind > BRIDGER_PRE_BINARIZE)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown preprocessing kind");
+  if (kind != BRIDGER_PRE_NONE && !pa)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null parameter array a");
+  if ((kind == BRIDGER_PRE_MINMAX || kind == BRIDGER_PRE_CENTER_SCALE) && !pb)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null parameter array b");
+  std::vector<double> va, vb;
+  if (kind != BRIDGER_PRE_NONE) {
+    va.assign(pa, pa + h->F);
+    vb = pb ? std::vector<double>(pb, pb + h->F) : std::vector<double>(h->F, 0.0);
+  }
+  if (!h->host_only && kind != BRIDGER_PRE_NONE) {
+    if (!h->d_pre_a) {
+      bridger_status s = upload(&h->d_pre_a, va);
+      if (s != BRIDGER_OK) return s;
+      if ((s = upload(&h->d_pre_b, vb)) != BRIDGER_OK) return s;
+    } else if (hipMemcpy(h->d_pre_a, va.data(), 8 * va.size(), hipMemcpyHostToDevice) !=
+                   hipSuccess ||
+               hipMemcpy(h->d_pre_b, vb.data(), 8 * vb.size(), hipMemcpyHostToDevice) !=
+                   hipSuccess) {
+      return fail(BRIDGER_ERR_DEVICE, "hipMemcpy to device failed");
+    }
+  }
+  h->pre_kind = kind;
+  h->pre_a = std::move(va);
+  h->pre_b = std::move(vb);
+  return BRIDGER_OK;
 }
 
 bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,

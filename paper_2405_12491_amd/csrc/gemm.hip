@@ -45,7 +45,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(LaunchArgs a) {
     for (int s = 0; s < 16; ++s) {
       const int f = 4 * s + grp;
       float v = 0.0f;
-      if (s < n_steps && f < F && row < a.n_rows) v = a.X[row * (int64_t)F + f];
+      if (s < n_steps && f < F && row < a.n_rows) {
+        v = a.X[row * (int64_t)F + f];
+        if (a.pre_kind) v = preprocess(a, f, v);
+      }
       nonfinite |= !__builtin_isfinite(v);
       xa[s] = v;
     }
@@ -159,7 +162,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(LaunchArgs a) {
         for (int d = 0; d < D; ++d) {
           const float th = *reinterpret_cast<const float *>(tp + 8 * mm);
           const int f = *reinterpret_cast<const int32_t *>(tp + 8 * mm + 4);
-          mm = 2 * mm + ((xr[f] <= th) ? 0 : 1);
+          const float xv = a.pre_kind ? preprocess(a, f, xr[f]) : xr[f];
+          mm = 2 * mm + ((xv <= th) ? 0 : 1);
         }
         if (LEAVES)
           a.out_leaf[row * (int64_t)T + a.tree_order[t]] =

@@ -92,6 +92,21 @@ __device__ __forceinline__ void staging_wave(uint8_t *smem, int n_chunks, uint32
   for (int i = 0; i < tail; ++i) __syncthreads();
 }
 
+// The fused preprocessing of feature f (BRIDGER_PRE_* in bridger.h): each step in double,
+// rounded to float.
+__device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, float x) {
+  if (a.pre_kind == 1) {
+    const float x1 = (float)((double)x * a.pre_a[f]);
+    return (float)((double)x1 + a.pre_b[f]);
+  }
+  if (a.pre_kind == 2) {
+    const float x1 = (float)((double)x - a.pre_a[f]);
+    return (float)((double)x1 / a.pre_b[f]);
+  }
+  if (a.pre_kind == 3) return ((double)x > a.pre_a[f]) ? 1.0f : 0.0f;
+  return x;
+}
+
 // Load this lane's row into the feature-major LDS tile (zeros past the last row).  With
 // NAN_TO_INF a NaN feature is stored as +inf: against finite thresholds both compare false
 // (x <= t), so every split sends them the same way.
@@ -100,7 +115,9 @@ __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a
                                               int64_t row, bool row_ok) {
   float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
   const int R = a.rows_per_wg;
+  const bool pre = a.pre_kind != 0;
   auto put = [&](int f, float v) {
+    if (pre) v = preprocess(a, f, v);
     if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
     xt[f * R + r] = v;
   };

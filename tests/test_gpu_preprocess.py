@@ -1,0 +1,78 @@
+"""GPU parity of fused preprocessing: predictions (every kernel family) and bins of
+preprocessed rows against the oracle run on the oracle-preprocessed rows."""
+import numpy as np
+import pytest
+
+import paper_2405_12491_amd as B
+from oracle import binning
+from oracle import preprocess as P
+from parity_util import assert_leaves, assert_scores, gpu_predict, oracle_predict, to_dev
+from synth import make_workload
+
+pytestmark = pytest.mark.gpu
+
+KERNELS = [B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT,
+           B.BRIDGER_KERNEL_GEMM]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+    yield
+
+
+def _params(kind, X, rng):
+    from sklearn.preprocessing import MinMaxScaler, RobustScaler
+    Xf = np.nan_to_num(X, nan=0.0, posinf=0.0, neginf=0.0)   # scalers are fitted on finite data
+    if kind == P.MINMAX:
+        s = MinMaxScaler(feature_range=(-2, 2)).fit(Xf)
+        return s.scale_, s.min_
+    if kind == P.CENTER_SCALE:
+        s = RobustScaler().fit(Xf)
+        return s.center_, s.scale_
+    return rng.standard_normal(X.shape[1]) * 0.5, None
+
+
+@pytest.mark.parametrize("kind", [P.MINMAX, P.CENTER_SCALE, P.BINARIZE])
+@pytest.mark.parametrize("name,n", [("gbdt_d6", 1500), ("rf_d8", 700), ("ragged_d12", 150),
+                                    ("mc_gbdt_d8", 150), ("shallow_d3", 1100)])
+def test_fused_preprocessing(kind, name, n):
+    import torch
+    rng = np.random.default_rng(kind * 10 + n)
+    w = make_workload(name, n)
+    X = w.X()
+    X[3, 1] = np.nan
+    X[4, 2] = np.inf
+    X[5, 0] = -np.inf
+    a, b = _params(kind, X, rng)
+    Xp = P.apply(kind, a, b, X)
+    ref, ref_lv = oracle_predict(w.forest, Xp, leaves=True)
+    Xd = to_dev(X)
+    with B.Forest(w.forest) as f:
+        f.set_preprocess(kind, a, b)
+        for k in KERNELS:
+            try:
+                f.kernel = k
+            except B.BridgerError:
+                continue
+            what = f"{name} pre={kind} {B.KERNEL_NAMES[k]}"
+            print(f"[pre] {what}", flush=True)
+            assert_scores(gpu_predict(f, Xd), ref, what + " scores")
+            assert_leaves(gpu_predict(f, Xd, leaves=True), ref_lv, what + " leaves")
+        # bins of the preprocessed rows, and prediction on them
+        f.kernel = B.BRIDGER_KERNEL_AUTO
+        if f.bin_info()["bin_bytes"] and f.kernel in (B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED):
+            q = f.bin(Xd)
+            out = f.predict_binned(q)
+            torch.cuda.synchronize()
+            bb = f.bin_info()["bin_bytes"]
+            got = q.cpu().numpy().view(np.uint8 if bb == 1 else np.uint16).astype(np.int64)
+            assert np.array_equal(got, binning.bin_rows(binning.tables(w.forest), Xp)), name + " bins"
+            assert_scores(out.cpu().numpy().astype(np.float64), ref, f"{name} pre={kind} binned")
+        # switching the preprocessing off restores the plain prediction
+        f.set_preprocess(B.BRIDGER_PRE_NONE)
+        ref0, _ = oracle_predict(w.forest, X)
+        assert_scores(gpu_predict(f, Xd), ref0, f"{name} preprocessing off")
