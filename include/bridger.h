@@ -207,6 +207,17 @@ bridger_status bridger_forest_predict_binned_leaves(bridger_forest_t h, const vo
 bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, const double *a,
                                              const double *b);
 
+/*
+ * Classifier labels (int32 [n_rows], device): with several classes the class of
+ * largest value (the first on ties), taken on the double-precision class values
+ * before the link function (softmax keeps their order); with one output and a
+ * sigmoid link, 1 when the value is above zero (probability above one half), else
+ * 0.  BRIDGER_ERR_UNSUPPORTED for one output without a sigmoid (a regressor).
+ * Other arguments and rules as predict.
+ */
+bridger_status bridger_forest_predict_labels(bridger_forest_t h, const float *X, int64_t n_rows,
+                                             int32_t n_features, int32_t *labels, void *stream);
+
 /* Shape facts.  Any output pointer may be NULL.  all_perfect = 1 when every tree
  * is perfect with one common depth (then max_depth is that depth). */
 bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,

@@ -61,6 +61,7 @@ def load_library(path: Optional[str] = None):
     lib.bridger_forest_predict_leaves.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_info.argtypes = [P, P, P, P, P, P]
     lib.bridger_forest_bin_info.argtypes = [P, P, P]
+    lib.bridger_forest_predict_labels.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_set_preprocess.argtypes = [P, I32, P, P]
     lib.bridger_forest_bin.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_predict_binned.argtypes = [P, P, I64, I32, P, P]
@@ -77,7 +78,8 @@ def load_library(path: Optional[str] = None):
                  "bridger_forest_predict_leaves", "bridger_forest_info", "bridger_forest_set_kernel",
                  "bridger_forest_get_kernel", "bridger_forest_plan", "bridger_forest_packed",
                  "bridger_forest_bin_info", "bridger_forest_bin", "bridger_forest_predict_binned",
-                 "bridger_forest_predict_binned_leaves", "bridger_forest_set_preprocess"):
+                 "bridger_forest_predict_binned_leaves", "bridger_forest_set_preprocess",
+                 "bridger_forest_predict_labels"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -165,6 +167,14 @@ def bridger_forest_predict_binned_leaves(h, xq_ptr: int, n_rows: int, n_features
     _check(load_library().bridger_forest_predict_binned_leaves(
         h, ctypes.c_void_p(xq_ptr), int(n_rows), int(n_features), ctypes.c_void_p(out_ptr),
         ctypes.c_void_p(stream)), "bridger_forest_predict_binned_leaves")
+
+
+def bridger_forest_predict_labels(h, X_ptr: int, n_rows: int, n_features: int, out_ptr: int,
+                                  stream: int = 0):
+    _check(load_library().bridger_forest_predict_labels(h, ctypes.c_void_p(X_ptr), int(n_rows),
+                                                        int(n_features), ctypes.c_void_p(out_ptr),
+                                                        ctypes.c_void_p(stream)),
+           "bridger_forest_predict_labels")
 
 
 def bridger_forest_info(h) -> dict:
@@ -262,6 +272,16 @@ class Forest:
         stream = torch.cuda.current_stream(X.device).cuda_stream
         bridger_forest_predict(self._h, X.data_ptr(), X.shape[0], self.n_features, out.data_ptr(),
                                stream)
+        return out
+
+    def predict_labels(self, X, out=None):
+        import torch
+        self._check_x(X)
+        if out is None:
+            out = torch.empty((X.shape[0],), dtype=torch.int32, device=X.device)
+        stream = torch.cuda.current_stream(X.device).cuda_stream
+        bridger_forest_predict_labels(self._h, X.data_ptr(), X.shape[0], self.n_features,
+                                      out.data_ptr(), stream)
         return out
 
     def predict_leaves(self, X, out=None):

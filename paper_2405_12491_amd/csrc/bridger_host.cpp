@@ -768,22 +768,26 @@ bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_r
 
 // X is fp32 rows, or (binned) rows of bin_bytes-wide bins from bridger_forest_bin.
 bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int32_t n_features,
-                          float *out, int32_t *out_leaf, void *stream, bool binned) {
+                          float *out, int32_t *out_leaf, void *stream, bool binned,
+                          int32_t *out_label = nullptr) {
   g_last_error.clear();
+  if (out_label && h && h->K == 1 && h->transform != BRIDGER_XFORM_SIGMOID)
+    return fail(BRIDGER_ERR_UNSUPPORTED,
+                "labels need several classes or a sigmoid output (a classifier)");
   if (binned && h && !h->bin_bytes)
     return fail(BRIDGER_ERR_UNSUPPORTED, "a feature has 65536 or more distinct thresholds");
   const int xsz = binned && h ? h->bin_bytes : 4;
-  bridger_status s = check_predict(h, X, n_rows, n_features, out ? (void *)out : (void *)out_leaf,
-                                   xsz);
+  void *dst = out ? (void *)out : (out_leaf ? (void *)out_leaf : (void *)out_label);
+  bridger_status s = check_predict(h, X, n_rows, n_features, dst, xsz);
   if (s != BRIDGER_OK || n_rows == 0) return s;
   if (binned && !((h->kernel_active == kPerfect && h->perfect_bok) ||
                   (h->kernel_active == kRagged && h->ragged_bok)))
     return fail(BRIDGER_ERR_UNSUPPORTED,
                 "binned prediction runs on the perfect and ragged kernels only");
   const uint8_t *xb = (const uint8_t *)X;
-  const uint8_t *ob = out ? (const uint8_t *)out : (const uint8_t *)out_leaf;
+  const uint8_t *ob = (const uint8_t *)dst;
   const size_t xbytes = (size_t)n_rows * h->F * xsz;
-  const size_t obytes = (size_t)n_rows * (out ? h->K : h->n_trees) * 4;
+  const size_t obytes = (size_t)n_rows * (out ? h->K : (out_leaf ? h->n_trees : 1)) * 4;
   if (xb < ob + obytes && ob < xb + xbytes)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
 
@@ -795,6 +799,7 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   a.x_vec4 = ((uintptr_t)X % 16 == 0) && (((int64_t)h->F * xsz) % 16 == 0);
   a.out = out;
   a.out_leaf = out_leaf;
+  a.out_label = out_label;
   a.class_begin = (const int32_t *)h->d_class_begin;
   a.class_count = (const int32_t *)h->d_class_count;
   a.base = (const float *)h->d_base;
@@ -1089,6 +1094,11 @@ bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X,
                                              int32_t n_features, int32_t *out_leaf,
                                              void *stream) {
   return do_predict(h, X, n_rows, n_features, nullptr, out_leaf, stream, false);
+}
+
+bridger_status bridger_forest_predict_labels(bridger_forest_t h, const float *X, int64_t n_rows,
+                                             int32_t n_features, int32_t *labels, void *stream) {
+  return do_predict(h, X, n_rows, n_features, nullptr, nullptr, stream, false, labels);
 }
 
 bridger_status bridger_forest_bin_info(bridger_forest_t h, int32_t *bin_bytes,

@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(LaunchArgs a) {
           double zv = acc[r];
           if (a.aggregate == 1) zv = (double)a.base[0] + zv / (double)a.class_count[0];
           else zv += (double)a.base[0];
-          a.out[row] = (float)(a.transform == 1 ? sigmoid_d(zv) : zv);
+          store_one(a, row, zv);
         }
       }
     }
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(LaunchArgs a) {
       }
       if (!LEAVES) {
         if (a.aggregate == 1) zv = (double)a.base[0] + zv / (double)a.class_count[0];
-        a.out[row] = (float)(a.transform == 1 ? sigmoid_d(zv) : zv);
+        store_one(a, row, zv);
       }
     }
   }

@@ -78,6 +78,7 @@ struct LaunchArgs {
   int32_t x_vec4;          // rows are 16-byte aligned and F % 4 == 0
   float *out;              // [n_rows, K] (scores) or nullptr
   int32_t *out_leaf;       // [n_rows, n_trees] (leaf ids) or nullptr
+  int32_t *out_label;      // [n_rows] (class labels) or nullptr
   const uint8_t *nodes;    // packed records of the kernel family
   const int32_t *tree_start;   // RAGGED: record index of each kernel tree's root; DIRECT: same
   const int32_t *chunk_first;  // RAGGED: first kernel tree of each chunk [n_chunks + 1]

@@ -215,13 +215,31 @@ __device__ __forceinline__ double sigmoid_d(double z) {
   return e / (1.0 + e);
 }
 
-// Finish class values z[0..K) held in LDS (stride `stride` doubles) and store the row.
+// Store the finished value z of a one-output row: its score, or its label (z > 0, i.e. the
+// sigmoid above one half).
+__device__ __forceinline__ void store_one(const LaunchArgs &a, int64_t row, double z) {
+  if (a.out_label) a.out_label[row] = z > 0.0 ? 1 : 0;
+  else a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
+}
+
+// Finish class values z[0..K) held in LDS (stride `stride` doubles) and store the row: the
+// scores, or the label (the first class of largest value; one output: z > 0).
 __device__ void finalize_store(const LaunchArgs &a, double *z, int stride, int64_t row) {
   const int K = a.K;
   for (int k = 0; k < K; ++k) {
     double v = z[k * stride];
     if (a.aggregate == 1) v = (double)a.base[k] + v / (double)a.class_count[k];
     z[k * stride] = v;
+  }
+  if (a.out_label) {
+    if (K == 1) {
+      a.out_label[row] = z[0] > 0.0 ? 1 : 0;
+    } else {
+      int best = 0;
+      for (int k = 1; k < K; ++k) best = z[k * stride] > z[best * stride] ? k : best;
+      a.out_label[row] = best;
+    }
+    return;
   }
   float *o = a.out + row * (int64_t)K;
   if (a.transform == 1) {

@@ -92,7 +92,7 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     if (row_ok) {
       double z = ca.acc;
       if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
-      a.out[row] = (float)(a.transform == 1 ? sigmoid_d(z) : z);
+      store_one(a, row, z);
     }
     return;
   }
