@@ -107,50 +107,59 @@ __device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, float x)
   return x;
 }
 
-// Load this lane's row into the feature-major LDS tile (zeros past the last row).  With
+// Load part `part` of `parts` of this lane's row into the feature-major LDS tile (zeros past
+// the last row): the lane groups sharing a tile split each row's features between them.  With
 // NAN_TO_INF a NaN feature is stored as +inf: against finite thresholds both compare false
 // (x <= t), so every split sends them the same way.
 template <bool NAN_TO_INF = false>
 __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a, int r,
-                                              int64_t row, bool row_ok) {
+                                              int64_t row, bool row_ok, int part = 0,
+                                              int parts = 1) {
   float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
   const int R = a.rows_per_wg;
-  const bool pre = a.pre_kind != 0;
-  auto put = [&](int f, float v) {
-    if (pre) v = preprocess(a, f, v);
-    if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
-    xt[f * R + r] = v;
-  };
   if (!row_ok) {
-    for (int f = 0; f < a.F; ++f) xt[f * R + r] = 0.0f;
+    const int f0 = (a.F * part) / parts, f1 = (a.F * (part + 1)) / parts;
+    for (int f = f0; f < f1; ++f) xt[f * R + r] = 0.0f;
     return;
   }
   const float *xr = a.X + row * (int64_t)a.F;
-  if (a.x_vec4) {
-    const float4 *x4 = reinterpret_cast<const float4 *>(xr);
-    const int n4 = a.F >> 2;
-    int i = 0;
-    for (; i + 2 <= n4; i += 2) {
-      float4 v0 = x4[i], v1 = x4[i + 1];
-      put(4 * i + 0, v0.x);
-      put(4 * i + 1, v0.y);
-      put(4 * i + 2, v0.z);
-      put(4 * i + 3, v0.w);
-      put(4 * i + 4, v1.x);
-      put(4 * i + 5, v1.y);
-      put(4 * i + 6, v1.z);
-      put(4 * i + 7, v1.w);
+  auto body = [&](auto pre_tag) {
+    constexpr bool PRE = decltype(pre_tag)::value;
+    auto put = [&](int f, float v) {
+      if (PRE) v = preprocess(a, f, v);
+      if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
+      xt[f * R + r] = v;
+    };
+    if (a.x_vec4) {
+      const float4 *x4 = reinterpret_cast<const float4 *>(xr);
+      const int n4 = a.F >> 2;
+      const int i0 = (n4 * part) / parts, i1 = (n4 * (part + 1)) / parts;
+      int i = i0;
+      for (; i + 2 <= i1; i += 2) {
+        const float4 v0 = x4[i], v1 = x4[i + 1];
+        put(4 * i + 0, v0.x);
+        put(4 * i + 1, v0.y);
+        put(4 * i + 2, v0.z);
+        put(4 * i + 3, v0.w);
+        put(4 * i + 4, v1.x);
+        put(4 * i + 5, v1.y);
+        put(4 * i + 6, v1.z);
+        put(4 * i + 7, v1.w);
+      }
+      for (; i < i1; ++i) {
+        const float4 v = x4[i];
+        put(4 * i + 0, v.x);
+        put(4 * i + 1, v.y);
+        put(4 * i + 2, v.z);
+        put(4 * i + 3, v.w);
+      }
+    } else {
+      const int f0 = (a.F * part) / parts, f1 = (a.F * (part + 1)) / parts;
+      for (int f = f0; f < f1; ++f) put(f, xr[f]);
     }
-    for (; i < n4; ++i) {
-      float4 v = x4[i];
-      put(4 * i + 0, v.x);
-      put(4 * i + 1, v.y);
-      put(4 * i + 2, v.z);
-      put(4 * i + 3, v.w);
-    }
-  } else {
-    for (int f = 0; f < a.F; ++f) put(f, xr[f]);
-  }
+  };
+  if (a.pre_kind) body(std::true_type{});
+  else body(std::false_type{});
 }
 
 // Byte offset of row r's element inside a feature's row of the LDS tile, for elements of XB
@@ -164,11 +173,13 @@ __device__ __forceinline__ uint32_t tile_row_off(int r) {
   return 4u * (uint32_t)((r & 31) + 32 * (r / (32 * P))) + (uint32_t)(XB * ((r >> 5) & (P - 1)));
 }
 
-// Load this lane's row of bins (F elements of XB bytes each, row-major in global memory) into
-// the feature-major LDS tile (zeros past the last row).  x_vec4: rows 16-byte aligned.
+// Load part `part` of `parts` of this lane's row of bins (F elements of XB bytes each,
+// row-major in global memory) into the feature-major LDS tile (zeros past the last row).
+// x_vec4: rows 16-byte aligned.
 template <int XB>
 __device__ __forceinline__ void load_row_tile_binned(uint8_t *smem, const LaunchArgs &a, int r,
-                                                     int64_t row, bool row_ok) {
+                                                     int64_t row, bool row_ok, int part,
+                                                     int parts) {
   static_assert(XB == 1 || XB == 2, "bins are 8 or 16 bits");
   const uint32_t stride = (uint32_t)a.rows_per_wg * XB;  // one feature's row of the tile
   const uint32_t base = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
@@ -177,8 +188,9 @@ __device__ __forceinline__ void load_row_tile_binned(uint8_t *smem, const Launch
     if (XB == 2) *(__attribute__((address_space(3))) uint16_t *)(uintptr_t)addr = (uint16_t)v;
     else *(__attribute__((address_space(3))) uint8_t *)(uintptr_t)addr = (uint8_t)v;
   };
+  const int f0 = (a.F * part) / parts, f1 = (a.F * (part + 1)) / parts;
   if (!row_ok) {
-    for (int f = 0; f < a.F; ++f) put(f, 0u);
+    for (int f = f0; f < f1; ++f) put(f, 0u);
     return;
   }
   const uint8_t *xr = reinterpret_cast<const uint8_t *>(a.X) + row * (int64_t)a.F * XB;
@@ -186,7 +198,8 @@ __device__ __forceinline__ void load_row_tile_binned(uint8_t *smem, const Launch
     constexpr int E = 16 / XB;  // elements per 16-byte load
     const uint4 *x4 = reinterpret_cast<const uint4 *>(xr);
     const int n4 = (a.F * XB) >> 4;
-    for (int i = 0; i < n4; ++i) {
+    const int i0 = (n4 * part) / parts, i1 = (n4 * (part + 1)) / parts;
+    for (int i = i0; i < i1; ++i) {
       const uint4 v = x4[i];
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -196,17 +209,18 @@ __device__ __forceinline__ void load_row_tile_binned(uint8_t *smem, const Launch
       }
     }
   } else {
-    for (int f = 0; f < a.F; ++f)
+    for (int f = f0; f < f1; ++f)
       put(f, XB == 2 ? (uint32_t)reinterpret_cast<const uint16_t *>(xr)[f] : (uint32_t)xr[f]);
   }
 }
 
-// The tile load for element size XB (fp32 with NaN stored as +inf when NAN_TO_INF).
+// The tile load for element size XB (fp32 with NaN stored as +inf when NAN_TO_INF); part
+// `part` of `parts` of the row's features.
 template <int XB, bool NAN_TO_INF>
 __device__ __forceinline__ void load_tile_any(uint8_t *smem, const LaunchArgs &a, int r,
-                                              int64_t row, bool row_ok) {
-  if constexpr (XB == 4) load_row_tile<NAN_TO_INF>(smem, a, r, row, row_ok);
-  else load_row_tile_binned<XB>(smem, a, r, row, row_ok);
+                                              int64_t row, bool row_ok, int part, int parts) {
+  if constexpr (XB == 4) load_row_tile<NAN_TO_INF>(smem, a, r, row, row_ok, part, parts);
+  else load_row_tile_binned<XB>(smem, a, r, row, row_ok, part, parts);
 }
 
 __device__ __forceinline__ double sigmoid_d(double z) {

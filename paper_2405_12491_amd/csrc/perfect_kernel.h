@@ -32,7 +32,7 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   constexpr uint32_t kLeafOff = 4u << D;
   constexpr uint32_t kFirstLeaf = 1u << D;
 
-  if (g == 0) load_tile_any<XB, FIN>(smem, a, r, row, row_ok);
+  load_tile_any<XB, FIN>(smem, a, r, row, row_ok, g, G);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;

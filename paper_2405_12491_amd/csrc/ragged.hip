@@ -36,7 +36,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   const int shift = a.log2_row_bytes;
   const int T = a.n_trees;
 
-  if (g == 0) load_tile_any<XB, false>(smem, a, r, row, row_ok);
+  load_tile_any<XB, false>(smem, a, r, row, row_ok, g, G);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   const int shift = a.log2_row_bytes;
   const int T = a.n_trees;
 
-  if (g == 0) load_tile_any<XB, false>(smem, a, r, row, row_ok);
+  load_tile_any<XB, false>(smem, a, r, row, row_ok, g, G);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
