@@ -208,6 +208,27 @@ bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, c
                                              const double *b);
 
 /*
+ * Predict (or write leaf ids) from rows in compressed sparse row form (the
+ * "sparse operator replacing" of Table 2): row i's stored values are
+ * values[indptr[i] .. indptr[i+1]) at features indices[same range]; every feature
+ * not stored reads 0.0 (then goes through the fused preprocessing like any value).
+ * Device pointers: indptr int64 [n_rows + 1] (non-decreasing), indices int32 and
+ * values float [indptr[n_rows]].  Indices within a row must be distinct (a repeated
+ * index gives one of its values, unspecified which); indices outside
+ * [0, n_features) are ignored.  Same outputs and rules as predict /
+ * predict_leaves; runs on the perfect and ragged kernel families
+ * (BRIDGER_ERR_UNSUPPORTED otherwise).
+ */
+bridger_status bridger_forest_predict_csr(bridger_forest_t h, const int64_t *indptr,
+                                          const int32_t *indices, const float *values,
+                                          int64_t n_rows, int32_t n_features, float *out,
+                                          void *stream);
+bridger_status bridger_forest_predict_csr_leaves(bridger_forest_t h, const int64_t *indptr,
+                                                 const int32_t *indices, const float *values,
+                                                 int64_t n_rows, int32_t n_features,
+                                                 int32_t *out_leaf, void *stream);
+
+/*
  * Classifier labels (int32 [n_rows], device): with several classes the class of
  * largest value (the first on ties), taken on the double-precision class values
  * before the link function (softmax keeps their order); with one output and a

@@ -62,6 +62,8 @@ def load_library(path: Optional[str] = None):
     lib.bridger_forest_info.argtypes = [P, P, P, P, P, P]
     lib.bridger_forest_bin_info.argtypes = [P, P, P]
     lib.bridger_forest_predict_labels.argtypes = [P, P, I64, I32, P, P]
+    lib.bridger_forest_predict_csr.argtypes = [P, P, P, P, I64, I32, P, P]
+    lib.bridger_forest_predict_csr_leaves.argtypes = [P, P, P, P, I64, I32, P, P]
     lib.bridger_forest_set_preprocess.argtypes = [P, I32, P, P]
     lib.bridger_forest_bin.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_predict_binned.argtypes = [P, P, I64, I32, P, P]
@@ -79,7 +81,8 @@ def load_library(path: Optional[str] = None):
                  "bridger_forest_get_kernel", "bridger_forest_plan", "bridger_forest_packed",
                  "bridger_forest_bin_info", "bridger_forest_bin", "bridger_forest_predict_binned",
                  "bridger_forest_predict_binned_leaves", "bridger_forest_set_preprocess",
-                 "bridger_forest_predict_labels"):
+                 "bridger_forest_predict_labels", "bridger_forest_predict_csr",
+                 "bridger_forest_predict_csr_leaves"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -177,6 +180,15 @@ def bridger_forest_predict_labels(h, X_ptr: int, n_rows: int, n_features: int, o
            "bridger_forest_predict_labels")
 
 
+def bridger_forest_predict_csr(h, indptr_ptr: int, indices_ptr: int, values_ptr: int, n_rows: int,
+                               n_features: int, out_ptr: int, stream: int = 0, leaves: bool = False):
+    lib = load_library()
+    fn = lib.bridger_forest_predict_csr_leaves if leaves else lib.bridger_forest_predict_csr
+    _check(fn(h, ctypes.c_void_p(indptr_ptr), ctypes.c_void_p(indices_ptr), ctypes.c_void_p(values_ptr),
+              int(n_rows), int(n_features), ctypes.c_void_p(out_ptr), ctypes.c_void_p(stream)),
+           "bridger_forest_predict_csr" + ("_leaves" if leaves else ""))
+
+
 def bridger_forest_info(h) -> dict:
     v = [ctypes.c_int32() for _ in range(5)]
     _check(load_library().bridger_forest_info(h, *[ctypes.byref(x) for x in v]), "bridger_forest_info")
@@ -272,6 +284,21 @@ class Forest:
         stream = torch.cuda.current_stream(X.device).cuda_stream
         bridger_forest_predict(self._h, X.data_ptr(), X.shape[0], self.n_features, out.data_ptr(),
                                stream)
+        return out
+
+    def predict_csr(self, indptr, indices, values, n_rows: int, out=None, leaves: bool = False):
+        """Rows in CSR form: CUDA tensors indptr int64 [n+1], indices int32, values float32."""
+        import torch
+        for t, dt in ((indptr, torch.int64), (indices, torch.int32), (values, torch.float32)):
+            if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == dt and t.is_contiguous()):
+                raise TypeError("CSR arrays must be contiguous CUDA tensors (int64, int32, float32)")
+        if out is None:
+            cols = self.n_trees if leaves else self.n_classes
+            out = torch.empty((n_rows, cols), dtype=torch.int32 if leaves else torch.float32,
+                              device=values.device)
+        stream = torch.cuda.current_stream(values.device).cuda_stream
+        bridger_forest_predict_csr(self._h, indptr.data_ptr(), indices.data_ptr(), values.data_ptr(),
+                                   n_rows, self.n_features, out.data_ptr(), stream, leaves)
         return out
 
     def predict_labels(self, X, out=None):

@@ -767,10 +767,19 @@ bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_r
 }
 
 // X is fp32 rows, or (binned) rows of bin_bytes-wide bins from bridger_forest_bin.
+struct CsrRows {
+  const int64_t *indptr = nullptr;
+  const int32_t *indices = nullptr;
+};
+
 bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int32_t n_features,
                           float *out, int32_t *out_leaf, void *stream, bool binned,
-                          int32_t *out_label = nullptr) {
+                          int32_t *out_label = nullptr, const CsrRows *csr = nullptr) {
   g_last_error.clear();
+  if (csr && h && !(h->kernel_active == kPerfect || h->kernel_active == kRagged))
+    return fail(BRIDGER_ERR_UNSUPPORTED, "CSR rows run on the perfect and ragged kernels only");
+  if (csr && n_rows > 0 && (!csr->indptr || !csr->indices))
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null CSR array");
   if (out_label && h && h->K == 1 && h->transform != BRIDGER_XFORM_SIGMOID)
     return fail(BRIDGER_ERR_UNSUPPORTED,
                 "labels need several classes or a sigmoid output (a classifier)");
@@ -788,7 +797,7 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   const uint8_t *ob = (const uint8_t *)dst;
   const size_t xbytes = (size_t)n_rows * h->F * xsz;
   const size_t obytes = (size_t)n_rows * (out ? h->K : (out_leaf ? h->n_trees : 1)) * 4;
-  if (xb < ob + obytes && ob < xb + xbytes)
+  if (!csr && xb < ob + obytes && ob < xb + xbytes)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
 
   LaunchArgs a{};
@@ -796,7 +805,12 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   a.n_rows = n_rows;
   a.F = h->F;
   a.x_bytes = xsz;
-  a.x_vec4 = ((uintptr_t)X % 16 == 0) && (((int64_t)h->F * xsz) % 16 == 0);
+  a.x_vec4 = !csr && ((uintptr_t)X % 16 == 0) && (((int64_t)h->F * xsz) % 16 == 0);
+  if (csr) {
+    a.csr = 1;
+    a.csr_indptr = csr->indptr;
+    a.csr_indices = csr->indices;
+  }
   a.out = out;
   a.out_leaf = out_leaf;
   a.out_label = out_label;
@@ -1094,6 +1108,22 @@ bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X,
                                              int32_t n_features, int32_t *out_leaf,
                                              void *stream) {
   return do_predict(h, X, n_rows, n_features, nullptr, out_leaf, stream, false);
+}
+
+bridger_status bridger_forest_predict_csr(bridger_forest_t h, const int64_t *indptr,
+                                          const int32_t *indices, const float *values,
+                                          int64_t n_rows, int32_t n_features, float *out,
+                                          void *stream) {
+  CsrRows c{indptr, indices};
+  return do_predict(h, values, n_rows, n_features, out, nullptr, stream, false, nullptr, &c);
+}
+
+bridger_status bridger_forest_predict_csr_leaves(bridger_forest_t h, const int64_t *indptr,
+                                                 const int32_t *indices, const float *values,
+                                                 int64_t n_rows, int32_t n_features,
+                                                 int32_t *out_leaf, void *stream) {
+  CsrRows c{indptr, indices};
+  return do_predict(h, values, n_rows, n_features, nullptr, out_leaf, stream, false, nullptr, &c);
 }
 
 bridger_status bridger_forest_predict_labels(bridger_forest_t h, const float *X, int64_t n_rows,

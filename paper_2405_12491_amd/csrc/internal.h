@@ -110,6 +110,9 @@ struct LaunchArgs {
   const float *q_values;       // binning: sorted distinct thresholds of every feature
   const int32_t *q_off;        // binning: [F + 1] offsets into q_values
   void *xq;                    // binning: output bins [n_rows, F] of x_bytes each
+  int32_t csr;                 // rows in CSR form: X = values, plus the two arrays below
+  const int64_t *csr_indptr;   // [n_rows + 1]
+  const int32_t *csr_indices;  // [nnz] feature of each stored value
   int32_t pre_kind;            // fused preprocessing (BRIDGER_PRE_*), 0 = none
   const double *pre_a, *pre_b; // its per-feature parameters
 };

@@ -74,12 +74,14 @@ __device__ __forceinline__ void wait_stage() { __builtin_amdgcn_s_waitcnt(0); }
 // chunk_src(c) -> {global source, bytes} of chunk c.
 template <class ChunkSrc>
 __device__ __forceinline__ void staging_wave(uint8_t *smem, int n_chunks, uint32_t chunk_bytes,
-                                             int lane, int tail, ChunkSrc chunk_src) {
+                                             int lane, int tail, ChunkSrc chunk_src,
+                                             int lead = 0) {
   {
     const auto src = chunk_src(0);
     stage_async(smem, 0, src.first, src.second, 0, lane, 1);
     wait_stage();
   }
+  for (int i = 0; i < lead; ++i) __syncthreads();  // extra barriers of the tile load
   __syncthreads();
   for (int c = 0; c < n_chunks; ++c) {
     if (c + 1 < n_chunks) {
@@ -214,13 +216,44 @@ __device__ __forceinline__ void load_row_tile_binned(uint8_t *smem, const Launch
   }
 }
 
+// Rows given in CSR form (a.csr: X = values, a.csr_indptr, a.csr_indices), absent features
+// reading 0: fill this lane's part of its row with (preprocessed) zeros, wait for every part,
+// then write this lane's share of the row's stored entries.  Entries whose index lies outside
+// [0, F) are ignored.  Contains one barrier (every compute wave of the workgroup calls it).
+template <bool NAN_TO_INF>
+__device__ __forceinline__ void load_row_tile_csr(uint8_t *smem, const LaunchArgs &a, int r,
+                                                  int64_t row, bool row_ok, int part, int parts) {
+  float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
+  const int R = a.rows_per_wg, F = a.F;
+  auto fix = [&](int f, float v) {
+    if (a.pre_kind) v = preprocess(a, f, v);
+    if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
+    return v;
+  };
+  const int f0 = (F * part) / parts, f1 = (F * (part + 1)) / parts;
+  for (int f = f0; f < f1; ++f) xt[f * R + r] = row_ok ? fix(f, 0.0f) : 0.0f;
+  __syncthreads();
+  if (!row_ok) return;
+  const int64_t p0 = a.csr_indptr[row], n = a.csr_indptr[row + 1] - p0;
+  const int64_t e0 = p0 + (n * part) / parts, e1 = p0 + (n * (part + 1)) / parts;
+  for (int64_t e = e0; e < e1; ++e) {
+    const int f = a.csr_indices[e];
+    if (f >= 0 && f < F) xt[f * R + r] = fix(f, a.X[e]);
+  }
+}
+
 // The tile load for element size XB (fp32 with NaN stored as +inf when NAN_TO_INF); part
-// `part` of `parts` of the row's features.
+// `part` of `parts` of the row's features.  A CSR load adds one barrier (staging waves match
+// it with their `lead` barrier).
 template <int XB, bool NAN_TO_INF>
 __device__ __forceinline__ void load_tile_any(uint8_t *smem, const LaunchArgs &a, int r,
                                               int64_t row, bool row_ok, int part, int parts) {
-  if constexpr (XB == 4) load_row_tile<NAN_TO_INF>(smem, a, r, row, row_ok, part, parts);
-  else load_row_tile_binned<XB>(smem, a, r, row, row_ok, part, parts);
+  if constexpr (XB == 4) {
+    if (a.csr) load_row_tile_csr<NAN_TO_INF>(smem, a, r, row, row_ok, part, parts);
+    else load_row_tile<NAN_TO_INF>(smem, a, r, row, row_ok, part, parts);
+  } else {
+    load_row_tile_binned<XB>(smem, a, r, row, row_ok, part, parts);
+  }
 }
 
 __device__ __forceinline__ double sigmoid_d(double z) {

@@ -24,14 +24,14 @@ __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
     staging_wave(smem, n_chunks, CB, tid & 63, 0, [&](int c) {
       const int n0 = c * CT, n1 = (n0 + CT < T) ? n0 + CT : T;
       return std::make_pair(a.nodes + (size_t)n0 * TB, (n1 - n0) * (int)TB);
-    });
+    }, a.csr ? 1 : 0);
     return;
   }
 
   const int64_t row = (int64_t)blockIdx.x * R + tid;
   const bool row_ok = row < a.n_rows;
   const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)tid;
-  load_row_tile<true>(smem, a, tid, row, row_ok);
+  load_tile_any<4, true>(smem, a, tid, row, row_ok, 0, 1);
   __syncthreads();
 
   double acc = a.aggregate == 0 ? (double)a.base[0] : 0.0;

@@ -18,7 +18,7 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
                  [&](int c) {
                    const int n0 = c * CT, n1 = (n0 + CT < T) ? n0 + CT : T;
                    return std::make_pair(a.nodes + (size_t)n0 * tb, (n1 - n0) * (int)tb);
-                 });
+                 }, a.csr ? 1 : 0);
     return;
   }
   const int r = tid & (R - 1);

@@ -25,7 +25,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
                  (LEAVES || (SIMPLE && G == 1)) ? 0 : 1, [&](int c) {
                    return std::make_pair(a.nodes + 8 * (size_t)a.chunk_rec[c],
                                          8 * (a.chunk_rec[c + 1] - a.chunk_rec[c]));
-                 });
+                 }, a.csr ? 1 : 0);
     return;
   }
   const int r = tid & (R - 1);
