@@ -580,7 +580,10 @@ Plan pick_plan(const PlanInput &pin) {
   if (gmode == 0) return p;
   Plan g = choose_global_plan(pin);
   if (g.waves == 0) return p;
-  if (!pin.perfect) g.ilp = env_int("BRIDGER_ILP", 2) == 1 ? 1 : 2;  // runs per lane
+  if (!pin.perfect) {  // trees walked at once per lane
+    const int u = env_int("BRIDGER_ILP", 4);
+    g.ilp = (u == 1 || u == 2) ? u : 4;
+  }
   const bool few = p.waves == 0 || p.waves_per_cu < kMinWavesPerCU;
   const bool fits = !pin.perfect || pin.forest_bytes <= kL2BytesPerXcd;
   if (gmode == 1 || (few && fits && g.waves_per_cu > p.waves_per_cu)) return g;

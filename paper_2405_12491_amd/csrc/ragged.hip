@@ -110,11 +110,12 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
 // Records read from global memory instead of LDS chunks (big forests on wide rows, where a
 // 64-row tile already takes most of the LDS and restaging every tree for every tile is the
 // bottleneck).  G lane groups share the row tile; group g walks the contiguous tree range
-// [T g / G, T (g + 1) / G) split into U runs, each a state machine over its records.  No
-// chunks, no staging, one barrier before the cross-group reduction.
+// [T g / G, T (g + 1) / G), U trees at a time, in lockstep: the lanes of a wave descend the same
+// trees together (a lane that reached its leaf idles until the wave's deepest path ends), so
+// one wave-wide gather touches only the few cache lines of those trees' current levels
+// rather than records of many trees at once.  Leaves are added in tree order.
 template <bool LEAVES, bool SIMPLE, int U, int XB>
 __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
-  static_assert(U == 1 || LEAVES || SIMPLE, "several runs need one output per row");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
   const int R = a.rows_per_wg, G = a.groups;
@@ -138,60 +139,54 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
 
   const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
   const uint2 *recs = reinterpret_cast<const uint2 *>(a.nodes);
-  int64_t idx[U], end[U];
-  int t[U];
-  double run_acc[U];
+  // trees q .. q + N - 1 from their roots to their leaves
+  auto walk = [&](auto n_tag, int q) {
+    constexpr int N = decltype(n_tag)::value;
+    int64_t idx[N];
+    uint2 rec[N];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int ta = ga + ((gb - ga) * u) / U, tz = ga + ((gb - ga) * (u + 1)) / U;
-    idx[u] = a.tree_start[ta];
-    end[u] = a.tree_start[tz];
-    t[u] = ta;
-    run_acc[u] = 0.0;
-  }
-  while (true) {
-    bool any = false;
+    for (int u = 0; u < N; ++u) {
+      idx[u] = a.tree_start[q + u];
+      rec[u] = recs[idx[u]];
+    }
+    // validated trees are at most 64 deep; the bound keeps the loop finite regardless
+    for (int level = 0; level <= 64; ++level) {
+      bool inner[N];
+      bool any = false;
 #pragma unroll
-    for (int u = 0; u < U; ++u) any = any || idx[u] < end[u];
-    if (!any) break;
-    uint2 rec[U];
-    uint32_t xv[U];
-    // a finished run re-reads its last record (the result is discarded)
+      for (int u = 0; u < N; ++u) {
+        inner[u] = (rec[u].y & (uint32_t)kLeafFlag) == 0;
+        any = any || inner[u];
+      }
+      if (!any) break;
+      uint32_t xv[N];
 #pragma unroll
-    for (int u = 0; u < U; ++u) rec[u] = recs[idx[u] < end[u] ? idx[u] : end[u] - 1];
+      for (int u = 0; u < N; ++u)
+        xv[u] = gather_x<false, XB>(smem, ((rec[u].y >> 16) << shift) + lane_off);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      xv[u] = gather_x<false, XB>(smem, ((rec[u].y >> 16) << shift) + lane_off);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (idx[u] < end[u]) {
-        const uint32_t meta = rec[u].y;
-        const bool leaf = (meta & (uint32_t)kLeafFlag) != 0;
-        const uint32_t rel = meta & (uint32_t)kMaxRel;
-        const bool right = goes_right<XB>(xv[u], rec[u].x) && !leaf;
-        if (leaf) {
-          if (LEAVES) {
-            if (row_ok)
-              a.out_leaf[row * (int64_t)T + a.tree_order[t[u]]] = a.leaf_map[idx[u]];
-          } else if (U == 1) {
-            if (!SIMPLE) class_advance(a, ca, t[u], acc_lds, slot_stride, g == 0);
-            ca.acc += (double)__uint_as_float(rec[u].x);
-          } else {
-            run_acc[u] += (double)__uint_as_float(rec[u].x);
-          }
-          ++t[u];
+      for (int u = 0; u < N; ++u) {
+        if (inner[u]) {
+          // left child at rel (>= 1), right child next to it
+          const uint32_t rel = rec[u].y & (uint32_t)kMaxRel;
+          idx[u] += (int64_t)rel + (goes_right<XB>(xv[u], rec[u].x) ? 1 : 0);
+          rec[u] = recs[idx[u]];
         }
-        // a valid record always moves forward; the max keeps the loop finite regardless
-        const uint32_t step = rel + (right ? 1u : 0u);
-        idx[u] += step > 1u ? step : 1u;
       }
     }
-  }
-  if (LEAVES) return;
-  if (U > 1) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) ca.acc += run_acc[u];
-  }
+    for (int u = 0; u < N; ++u) {
+      if (LEAVES) {
+        if (row_ok) a.out_leaf[row * (int64_t)T + a.tree_order[q + u]] = a.leaf_map[idx[u]];
+      } else {
+        if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+        ca.acc += (double)__uint_as_float(rec[u].x);
+      }
+    }
+  };
+  int q = ga;
+  for (; q + U <= gb; q += U) walk(std::integral_constant<int, U>{}, q);
+  for (; q < gb; ++q) walk(std::integral_constant<int, 1>{}, q);
+  if (LEAVES) return;
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
   } else {
@@ -210,17 +205,23 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
 }
 
 // ---------------------------------------------------------------------- launchers
+template <int XB, int U>
+static int launch_ragged_global_xu(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                                   void *stream) {
+  const int threads = 64 * waves;
+  if (a.out_leaf)
+    return launch_common(ragged_global_kernel<true, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.K != 1)
+    return launch_common(ragged_global_kernel<false, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_global_kernel<false, true, U, XB>, threads, n_wg, lds_bytes, stream, a);
+}
+
 template <int XB>
 static int launch_ragged_global_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                                   void *stream) {
-  const int threads = 64 * waves;
-  if (a.out_leaf)
-    return launch_common(ragged_global_kernel<true, false, 1, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.K != 1)
-    return launch_common(ragged_global_kernel<false, false, 1, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.ilp == 2)
-    return launch_common(ragged_global_kernel<false, true, 2, XB>, threads, n_wg, lds_bytes, stream, a);
-  return launch_common(ragged_global_kernel<false, true, 1, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.ilp == 1) return launch_ragged_global_xu<XB, 1>(a, waves, n_wg, lds_bytes, stream);
+  if (a.ilp == 2) return launch_ragged_global_xu<XB, 2>(a, waves, n_wg, lds_bytes, stream);
+  return launch_ragged_global_xu<XB, 4>(a, waves, n_wg, lds_bytes, stream);
 }
 
 int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
