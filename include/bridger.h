@@ -186,24 +186,37 @@ bridger_status bridger_forest_predict_binned_leaves(bridger_forest_t h, const vo
  * Sec. 4.3, with the scalers of its CML suite): every feature value x of feature f
  * is transformed at the row load, before any compare, the forest's thresholds
  * applying to the transformed value x'.  Each step is done in double precision
- * and rounded to float, so the results match scikit-learn's transforms of float32
- * data bit for bit:
+ * and rounded to float, so the first three kinds match scikit-learn's transforms
+ * of float32 data bit for bit:
  *   BRIDGER_PRE_MINMAX        x1 = float(x * a[f]);  x' = float(x1 + b[f])
  *                             (MinMaxScaler: a = scale_, b = min_)
  *   BRIDGER_PRE_CENTER_SCALE  x1 = float(x - a[f]);  x' = float(x1 / b[f])
  *                             (StandardScaler: a = mean_, b = scale_;
  *                              RobustScaler: a = center_, b = scale_)
  *   BRIDGER_PRE_BINARIZE      x' = (x > a[f]) ? 1 : 0   (Binarizer; NaN gives 0)
+ *   BRIDGER_PRE_NORMALIZE     s = sum of double(x_f)^2 over the row, one add at a
+ *                             time in feature order (CSR rows: in stored order);
+ *                             n = sqrt(s), or 1 when s = 0; x' = float(x / n)
+ *                             (Normalizer, unit L2 rows: within a few ulps of
+ *                             scikit-learn's float32 arithmetic, and within half an
+ *                             ulp of the exact x / ||x|| but for rounding ties;
+ *                             a NaN makes the whole row NaN)
  *   BRIDGER_PRE_NONE          x' = x (b and a may be NULL)
- * a and b are host arrays of n_features doubles (b unused for BINARIZE), copied at
- * the call; the setting applies to every later predict, predict_leaves and bin on
- * the handle.  Call it with no prediction in flight on the handle (synchronous
+ * a and b are host arrays of n_features doubles (b unused for BINARIZE, neither
+ * for NORMALIZE: both may be NULL), copied at the call; the setting applies to
+ * every later predict, predict_leaves, predict_csr, predict_labels and bin on the
+ * handle.  Call it with no prediction in flight on the handle (synchronous
  * upload).  BRIDGER_ERR_INVALID_ARGUMENT on an unknown kind or a missing array.
+ * NORMALIZE runs a row-norm pass before the fused kernel, with n_rows doubles of
+ * scratch taken from the device's default stream-ordered memory pool and returned
+ * to it on the same stream after the kernel (BRIDGER_ERR_OUT_OF_MEMORY if the pool
+ * cannot supply them).
  */
 #define BRIDGER_PRE_NONE 0
 #define BRIDGER_PRE_MINMAX 1
 #define BRIDGER_PRE_CENTER_SCALE 2
 #define BRIDGER_PRE_BINARIZE 3
+#define BRIDGER_PRE_NORMALIZE 4
 bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, const double *a,
                                              const double *b);
 

@@ -34,6 +34,7 @@ BRIDGER_KERNEL_GEMM = 4
 KERNEL_NAMES = {0: "auto", 1: "perfect", 2: "ragged", 3: "direct", 4: "gemm"}
 BRIDGER_CREATE_HOST_ONLY = 1
 BRIDGER_PRE_NONE, BRIDGER_PRE_MINMAX, BRIDGER_PRE_CENTER_SCALE, BRIDGER_PRE_BINARIZE = 0, 1, 2, 3
+BRIDGER_PRE_NORMALIZE = 4
 
 _lib = None
 

@@ -17,7 +17,8 @@ BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbridger.so")
 SOURCES = [os.path.join(CSRC, n) for n in
            ("bridger_host.cpp", "perfect.hip", "perfect_binned.hip", "perfect_fixed.hip",
-            "perfect_global.hip", "ragged.hip", "direct.hip", "gemm.hip", "bin.hip")]
+            "perfect_global.hip", "ragged.hip", "direct.hip", "gemm.hip", "bin.hip",
+            "normalize.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 ARCH = ["--offload-arch=gfx950"]

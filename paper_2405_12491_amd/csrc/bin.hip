@@ -56,7 +56,7 @@ __global__ __launch_bounds__(kBinThreads) void bin_kernel(LaunchArgs a) {
       const int64_t row = r0 + i / nf;
       const int ff = f + (int)(i % nf);
       const int64_t e = row * F + ff;
-      const float x = a.pre_kind ? preprocess(a, ff, a.X[e]) : a.X[e];
+      const float x = a.pre_kind ? preprocess(a, ff, row, a.X[e]) : a.X[e];
       const int o = a.q_off[ff] - base, cnt = a.q_off[ff + 1] - a.q_off[ff];
       int b = cnt;
       if (x == x) b = in_lds ? lower_bound_f32(tab + o, cnt, x)

@@ -731,6 +731,35 @@ bridger_status upload_all(bridger_forest *h) {
   return BRIDGER_OK;
 }
 
+// The Normalizer's row norms: n_rows doubles of stream-ordered scratch from the device's default
+// memory pool, filled by the row-norm pass ahead of the fused kernel and handed back to the pool
+// on the same stream when this object goes out of scope (after the kernel is enqueued).
+struct RowNorms {
+  double *p = nullptr;
+  hipStream_t stream = nullptr;
+  ~RowNorms() {
+    if (p) (void)hipFreeAsync(p, stream);
+  }
+};
+
+bridger_status prepare_row_norms(const bridger_forest *h, LaunchArgs &a, void *stream,
+                                 RowNorms &rn) {
+  if (h->pre_kind != BRIDGER_PRE_NORMALIZE) return BRIDGER_OK;
+  if (hipMallocAsync((void **)&rn.p, (size_t)a.n_rows * sizeof(double), (hipStream_t)stream) !=
+      hipSuccess) {
+    (void)hipGetLastError();
+    rn.p = nullptr;
+    return fail(BRIDGER_ERR_OUT_OF_MEMORY, "no stream-ordered scratch for the row norms");
+  }
+  rn.stream = (hipStream_t)stream;
+  const int err = launch_row_norm(a, rn.p, stream);
+  if (err != 0)
+    return fail(BRIDGER_ERR_DEVICE, std::string("row-norm launch failed: ") +
+                                        hipGetErrorString((hipError_t)err));
+  a.row_norm = rn.p;
+  return BRIDGER_OK;
+}
+
 void set_preprocess_args(const bridger_forest *h, LaunchArgs &a) {
   a.pre_kind = h->pre_kind;
   a.pre_a = (const double *)h->d_pre_a;
@@ -825,7 +854,11 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   a.K = h->K;
   a.aggregate = h->aggregate;
   a.transform = h->transform;
-  set_preprocess_args(h, a);
+  RowNorms norms;
+  if (!binned) {
+    set_preprocess_args(h, a);
+    if ((s = prepare_row_norms(h, a, stream, norms)) != BRIDGER_OK) return s;
+  }
   int err = 0;
   if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
     const bool perfect = h->kernel_active == kPerfect;
@@ -1164,7 +1197,10 @@ bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_
   a.q_values = (const float *)h->d_q_values;
   a.q_off = (const int32_t *)h->d_q_off;
   a.xq = Xq;
+  a.x_vec4 = ((uintptr_t)X % 16 == 0) && (h->F % 4 == 0);
   set_preprocess_args(h, a);
+  RowNorms norms;
+  if ((s = prepare_row_norms(h, a, stream, norms)) != BRIDGER_OK) return s;
   const int err = launch_bin(a, stream);
   if (err != 0)
     return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
@@ -1187,18 +1223,18 @@ bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, c
                                              const double *pb) {
   g_last_error.clear();
   if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
-  if (kind < BRIDGER_PRE_NONE || kind > BRIDGER_PRE_BINARIZE)
+  if (kind < BRIDGER_PRE_NONE || kind > BRIDGER_PRE_NORMALIZE)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown preprocessing kind");
-  if (kind != BRIDGER_PRE_NONE && !pa)
-    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null parameter array a");
+  const bool params = kind != BRIDGER_PRE_NONE && kind != BRIDGER_PRE_NORMALIZE;
+  if (params && !pa) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null parameter array a");
   if ((kind == BRIDGER_PRE_MINMAX || kind == BRIDGER_PRE_CENTER_SCALE) && !pb)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null parameter array b");
   std::vector<double> va, vb;
-  if (kind != BRIDGER_PRE_NONE) {
+  if (params) {
     va.assign(pa, pa + h->F);
     vb = pb ? std::vector<double>(pb, pb + h->F) : std::vector<double>(h->F, 0.0);
   }
-  if (!h->host_only && kind != BRIDGER_PRE_NONE) {
+  if (!h->host_only && params) {
     if (!h->d_pre_a) {
       bridger_status s = upload(&h->d_pre_a, va);
       if (s != BRIDGER_OK) return s;

@@ -24,7 +24,7 @@ __global__ __launch_bounds__(256) void direct_kernel(LaunchArgs a) {
     int n = a.tree_start[t];
     int4 rc = recs[n];
     while (rc.y >= 0) {
-      const float xv = a.pre_kind ? preprocess(a, rc.y, xr[rc.y]) : xr[rc.y];
+      const float xv = a.pre_kind ? preprocess(a, rc.y, rr, xr[rc.y]) : xr[rc.y];
       n = (xv <= __int_as_float(rc.x)) ? rc.z : rc.w;
       rc = recs[n];
     }

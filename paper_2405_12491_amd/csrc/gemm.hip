@@ -47,7 +47,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(LaunchArgs a) {
       float v = 0.0f;
       if (s < n_steps && f < F && row < a.n_rows) {
         v = a.X[row * (int64_t)F + f];
-        if (a.pre_kind) v = preprocess(a, f, v);
+        if (a.pre_kind) v = preprocess(a, f, row, v);
       }
       nonfinite |= !__builtin_isfinite(v);
       xa[s] = v;
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(LaunchArgs a) {
         for (int d = 0; d < D; ++d) {
           const float th = *reinterpret_cast<const float *>(tp + 8 * mm);
           const int f = *reinterpret_cast<const int32_t *>(tp + 8 * mm + 4);
-          const float xv = a.pre_kind ? preprocess(a, f, xr[f]) : xr[f];
+          const float xv = a.pre_kind ? preprocess(a, f, row, xr[f]) : xr[f];
           mm = 2 * mm + ((xv <= th) ? 0 : 1);
         }
         if (LEAVES)

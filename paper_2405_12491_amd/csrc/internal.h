@@ -115,6 +115,7 @@ struct LaunchArgs {
   const int32_t *csr_indices;  // [nnz] feature of each stored value
   int32_t pre_kind;            // fused preprocessing (BRIDGER_PRE_*), 0 = none
   const double *pre_a, *pre_b; // its per-feature parameters
+  const double *row_norm;      // NORMALIZE: each row's L2 norm in double (1 for a zero row)
 };
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.
@@ -123,6 +124,7 @@ int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int 
 int launch_perfect_binned(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                           void *stream);
 int launch_bin(const LaunchArgs &a, void *stream);
+int launch_row_norm(const LaunchArgs &a, double *norm, void *stream);
 int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                           void *stream);
 int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

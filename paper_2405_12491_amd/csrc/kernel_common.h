@@ -94,9 +94,9 @@ __device__ __forceinline__ void staging_wave(uint8_t *smem, int n_chunks, uint32
   for (int i = 0; i < tail; ++i) __syncthreads();
 }
 
-// The fused preprocessing of feature f (BRIDGER_PRE_* in bridger.h): each step in double,
-// rounded to float.
-__device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, float x) {
+// The fused preprocessing of feature f of row `row` (BRIDGER_PRE_* in bridger.h): each step in
+// double, rounded to float.
+__device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, int64_t row, float x) {
   if (a.pre_kind == 1) {
     const float x1 = (float)((double)x * a.pre_a[f]);
     return (float)((double)x1 + a.pre_b[f]);
@@ -106,6 +106,7 @@ __device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, float x)
     return (float)((double)x1 / a.pre_b[f]);
   }
   if (a.pre_kind == 3) return ((double)x > a.pre_a[f]) ? 1.0f : 0.0f;
+  if (a.pre_kind == 4) return (float)((double)x / a.row_norm[row]);
   return x;
 }
 
@@ -128,7 +129,7 @@ __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a
   auto body = [&](auto pre_tag) {
     constexpr bool PRE = decltype(pre_tag)::value;
     auto put = [&](int f, float v) {
-      if (PRE) v = preprocess(a, f, v);
+      if (PRE) v = preprocess(a, f, row, v);
       if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
       xt[f * R + r] = v;
     };
@@ -226,7 +227,7 @@ __device__ __forceinline__ void load_row_tile_csr(uint8_t *smem, const LaunchArg
   float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
   const int R = a.rows_per_wg, F = a.F;
   auto fix = [&](int f, float v) {
-    if (a.pre_kind) v = preprocess(a, f, v);
+    if (a.pre_kind) v = preprocess(a, f, row, v);
     if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
     return v;
   };

@@ -33,10 +33,12 @@ def _params(kind, X, rng):
     if kind == P.CENTER_SCALE:
         s = RobustScaler().fit(Xf)
         return s.center_, s.scale_
+    if kind == P.NORMALIZE:
+        return None, None
     return rng.standard_normal(X.shape[1]) * 0.5, None
 
 
-@pytest.mark.parametrize("kind", [P.MINMAX, P.CENTER_SCALE, P.BINARIZE])
+@pytest.mark.parametrize("kind", [P.MINMAX, P.CENTER_SCALE, P.BINARIZE, P.NORMALIZE])
 @pytest.mark.parametrize("name,n", [("gbdt_d6", 1500), ("rf_d8", 700), ("ragged_d12", 150),
                                     ("mc_gbdt_d8", 150), ("shallow_d3", 1100)])
 def test_fused_preprocessing(kind, name, n):
@@ -76,3 +78,42 @@ def test_fused_preprocessing(kind, name, n):
         f.set_preprocess(B.BRIDGER_PRE_NONE)
         ref0, _ = oracle_predict(w.forest, X)
         assert_scores(gpu_predict(f, Xd), ref0, f"{name} preprocessing off")
+
+
+@pytest.mark.parametrize("name,n", [("gbdt_d6", 1500), ("rf_d8", 700), ("ragged_d12", 150),
+                                    ("mc_gbdt_d8", 150)])
+def test_normalize_at_ties(name, n):
+    """Normalizer with every threshold equal to some row's normalized feature value, so a last-bit
+    difference anywhere in the norm or the divide changes a leaf."""
+    import dataclasses
+    import torch
+    rng = np.random.default_rng(n + 7)
+    w = make_workload(name, n)
+    X = w.X()
+    X[2] = 0.0                                  # zero row: left unchanged
+    Xp = P.apply(P.NORMALIZE, None, None, X)
+    m = w.forest
+    thr = m.threshold.copy()
+    rows = rng.integers(0, n, thr.shape[0])
+    thr[:] = Xp[rows, np.clip(m.feature, 0, X.shape[1] - 1)]
+    model = dataclasses.replace(m, threshold=thr)
+    ref, ref_lv = oracle_predict(model, Xp, leaves=True)
+    Xd = to_dev(X)
+    with B.Forest(model) as f:
+        f.set_preprocess(B.BRIDGER_PRE_NORMALIZE)
+        for k in KERNELS:
+            try:
+                f.kernel = k
+            except B.BridgerError:
+                continue
+            what = f"{name} normalize ties {B.KERNEL_NAMES[k]}"
+            print(f"[pre] {what}", flush=True)
+            assert_scores(gpu_predict(f, Xd), ref, what + " scores")
+            assert_leaves(gpu_predict(f, Xd, leaves=True), ref_lv, what + " leaves")
+        f.kernel = B.BRIDGER_KERNEL_AUTO
+        if f.bin_info()["bin_bytes"]:
+            q = f.bin(Xd)
+            torch.cuda.synchronize()
+            bb = f.bin_info()["bin_bytes"]
+            got = q.cpu().numpy().view(np.uint8 if bb == 1 else np.uint16).astype(np.int64)
+            assert np.array_equal(got, binning.bin_rows(binning.tables(model), Xp)), name + " bins"

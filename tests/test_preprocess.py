@@ -167,4 +167,5 @@ def test_set_preprocess_argument_errors():
             B.bridger_forest_set_preprocess(f.handle, B.BRIDGER_PRE_BINARIZE, None, None)
         assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
         f.set_preprocess(B.BRIDGER_PRE_BINARIZE, a)
+        f.set_preprocess(B.BRIDGER_PRE_NORMALIZE)          # no parameters
         f.set_preprocess(B.BRIDGER_PRE_NONE)

@@ -30,6 +30,16 @@ def _random_csr(rng, n, F, density, sort=True, bad_index=False):
     return (np.array(indptr, np.int64), np.array(indices, np.int32), np.array(values, np.float32))
 
 
+def _sorted_csr(ip, ix, v):
+    """The same rows with each row's entries in ascending index order."""
+    ix2, v2 = ix.copy(), v.copy()
+    for i in range(len(ip) - 1):
+        o = np.argsort(ix[ip[i]:ip[i + 1]], kind="stable")
+        ix2[ip[i]:ip[i + 1]] = ix[ip[i]:ip[i + 1]][o]
+        v2[ip[i]:ip[i + 1]] = v[ip[i]:ip[i + 1]][o]
+    return ip, ix2, v2
+
+
 def test_densify_matches_scipy():
     import scipy.sparse as sp
     rng = np.random.default_rng(1)
@@ -69,13 +79,15 @@ def test_csr_prediction(case):
                 f.kernel = k
             except B.BridgerError:
                 continue
-            for pre in (P.NONE, P.MINMAX):
-                a = rng.uniform(0.5, 2.0, F) if pre else None
-                b = rng.uniform(-1, 1, F) if pre else None
+            for pre in (P.NONE, P.MINMAX, P.NORMALIZE):
+                a = rng.uniform(0.5, 2.0, F) if pre == P.MINMAX else None
+                b = rng.uniform(-1, 1, F) if pre == P.MINMAX else None
                 f.set_preprocess(pre, a, b)
                 ref, ref_lv = oracle_predict(model, P.apply(pre, a, b, X), leaves=True)
-                out = f.predict_csr(d(ip), d(ix), d(v), n)
-                lv = f.predict_csr(d(ip), d(ix), d(v), n, leaves=True)
+                # the row norm sums in stored order: ascending indices give the oracle's order
+                cip, cix, cv = _sorted_csr(ip, ix, v) if pre == P.NORMALIZE else (ip, ix, v)
+                out = f.predict_csr(d(cip), d(cix), d(cv), n)
+                lv = f.predict_csr(d(cip), d(cix), d(cv), n, leaves=True)
                 torch.cuda.synchronize()
                 what = f"{case} csr {B.KERNEL_NAMES[k]} pre={pre}"
                 assert_scores(out.cpu().numpy().astype(np.float64), ref, what)
