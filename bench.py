@@ -82,6 +82,14 @@ def parse():
     p.add_argument("--binned", action="store_true",
                    help="time prediction on 8/16-bit feature bins (bins made once, untimed; the "
                         "binning pass is timed separately as bin_ms)")
+    p.add_argument("--pre", default="none",
+                   choices=["none", "minmax", "center_scale", "binarize", "normalize"],
+                   help="fused preprocessing ahead of the forest (parameters fitted on the first "
+                        "row block; the Normalizer's row-norm pass is inside the timed step)")
+    p.add_argument("--csr", action="store_true",
+                   help="rows handed over in CSR form (built once, untimed)")
+    p.add_argument("--labels", action="store_true",
+                   help="write int32 class labels instead of scores")
     p.add_argument("--calib-copy", action="store_true",
                    help="time a plain device copy of X instead (counter calibration)")
     return p.parse_args()
@@ -96,6 +104,46 @@ def build_x(w, device):
         blk = x_rows(w.seed, w.x_kind, w.n_features, r, min(r + step, w.n_rows), **w.x_params)
         Xd[r:r + blk.shape[0]].copy_(torch.from_numpy(blk))
     return Xd
+
+
+PRE_KINDS = {"none": 0, "minmax": 1, "center_scale": 2, "binarize": 3, "normalize": 4}
+
+
+def pre_params(w, kind):
+    """Scaler parameters fitted on the workload's first row block: MinMaxScaler to [0, 1],
+    StandardScaler (mean, std), Binarizer at 0; none for the Normalizer."""
+    from synth import BLOCK_ROWS, x_rows
+    if kind in ("none", "normalize"):
+        return None, None
+    X = x_rows(w.seed, w.x_kind, w.n_features, 0, min(BLOCK_ROWS, w.n_rows),
+               **w.x_params).astype(np.float64)
+    if kind == "minmax":
+        lo, hi = X.min(0), X.max(0)
+        rng = np.where(hi > lo, hi - lo, 1.0)
+        return 1.0 / rng, -lo / rng
+    if kind == "center_scale":
+        sd = X.std(0)
+        return X.mean(0), np.where(sd > 0, sd, 1.0)
+    return np.zeros(w.n_features), None
+
+
+def build_csr(w, device):
+    """The workload's rows in CSR form (entries equal to 0.0 left out), built block by block on
+    the host: indptr int64 [n+1], indices int32, values float32, on `device`."""
+    import torch
+    from synth import BLOCK_ROWS, x_rows
+    ind, val, counts = [], [], []
+    step = BLOCK_ROWS * 4
+    for r in range(0, w.n_rows, step):
+        blk = x_rows(w.seed, w.x_kind, w.n_features, r, min(r + step, w.n_rows), **w.x_params)
+        nz = blk != 0.0
+        rr, cc = np.nonzero(nz)
+        ind.append(cc.astype(np.int32))
+        val.append(blk[rr, cc].astype(np.float32))
+        counts.append(nz.sum(1))
+    indptr = np.concatenate([[0], np.cumsum(np.concatenate(counts))]).astype(np.int64)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    return d(indptr), d(np.concatenate(ind)), d(np.concatenate(val))
 
 
 def node_depths(f):
@@ -114,19 +162,28 @@ def node_depths(f):
     return depth
 
 
-def cpu_baseline(w, out_dev, sample_rows):
-    """The CPU oracle timed on the host's cores over the first `sample_rows` rows; its
-    outputs are also compared with the GPU's for those rows."""
+def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False):
+    """The CPU oracle (with the oracle's preprocessing first, when fused) timed on the host's
+    cores over the first `sample_rows` rows; its outputs are also compared with the GPU's for
+    those rows (labels: the oracle's class of largest output)."""
     import oracle
+    from oracle import preprocess as P
     from synth import x_rows
     n = min(sample_rows, w.n_rows)
     X = x_rows(w.seed, w.x_kind, w.n_features, 0, n, **w.x_params)
     threads = max(1, min(16, len(os.sched_getaffinity(0))))
     t0 = time.perf_counter()
+    if pre[0] != "none":
+        X = P.apply(PRE_KINDS[pre[0]], pre[1], pre[2], X)
     ref, _, visits = oracle.predict(w.forest, X, threads=threads)
     dt = time.perf_counter() - t0
-    got = out_dev[:n].cpu().numpy().astype(np.float64)
-    ok = bool(np.all(np.abs(got - ref) <= 1e-6 + 1e-5 * np.abs(ref)))
+    got = out_dev[:n].cpu().numpy()
+    if labels:
+        lab = (ref[:, 0] > 0.5).astype(np.int64) if ref.shape[1] == 1 else ref.argmax(1)
+        ok = bool(np.mean(got.reshape(-1) == lab) > 0.9999)
+    else:
+        got = got.astype(np.float64)
+        ok = bool(np.all(np.abs(got - ref) <= 1e-6 + 1e-5 * np.abs(ref)))
     return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
             "sample": f"first {n:,} rows of the {w.n_rows:,}-row workload ({visits:,} node visits), "
                       f"{dt:.2f} s wall on {threads} threads",
@@ -170,10 +227,22 @@ def main():
     forest = B.Forest(w.forest)
     if args.kernel != "auto":
         forest.kernel = {"perfect": 1, "ragged": 2, "direct": 3, "gemm": 4}[args.kernel]
+    pre = (args.pre,) + pre_params(w, args.pre)
+    if args.pre != "none":
+        forest.set_preprocess(PRE_KINDS[args.pre], pre[1], pre[2])
     out = torch.empty((w.n_rows, w.forest.n_classes), dtype=torch.float32, device=dev)
     plan = forest.plan(w.n_rows)
     bin_ms = None
-    if args.binned:
+    csr_bytes = None
+    if args.labels:
+        out = torch.empty((w.n_rows, 1), dtype=torch.int32, device=dev)
+        step = lambda: forest.predict_labels(Xd, out.view(-1))
+    elif args.csr:
+        ip, ix, vv = build_csr(w, dev)
+        csr_bytes = ip.numel() * 8 + ix.numel() * 4 + vv.numel() * 4
+        Xd = None   # the dense rows are not needed any more
+        step = lambda: forest.predict_csr(ip, ix, vv, w.n_rows, out)
+    elif args.binned:
         Xq = forest.bin(Xd)
         torch.cuda.synchronize()
         b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -210,14 +279,18 @@ def main():
         visits_per_row = float(f.n_trees * info["max_depth"])
     else:
         m = min(4096, n)
-        lv = forest.predict_leaves(Xd[:m]).cpu().numpy()
+        if Xd is None:   # CSR rows: the sample's leaves from its CSR rows
+            lv = forest.predict_csr(ip[:m + 1], ix, vv, m, leaves=True).cpu().numpy()
+        else:
+            lv = forest.predict_leaves(Xd[:m]).cpu().numpy()
         depth = node_depths(f)
         offs = f.tree_offsets[:-1].astype(np.int64)
         visits_per_row = float(depth[lv.astype(np.int64) + offs[None, :]].sum()) / m
     visits = visits_per_row * n
     forest_bytes = B.bridger_forest_packed(forest.handle, 0, np.uint8).size
     x_elem = forest.bin_info()["bin_bytes"] if args.binned else 4
-    alg_bytes = n * w.n_features * x_elem + n * f.n_classes * 4 + forest_bytes
+    x_bytes = csr_bytes if args.csr else n * w.n_features * x_elem
+    alg_bytes = x_bytes + n * (1 if args.labels else f.n_classes) * 4 + forest_bytes
     s = ms / 1e3
     visits_per_s = visits / s
     line = {
@@ -239,6 +312,9 @@ def main():
             "n_classes": f.n_classes,
             "kernel": B.KERNEL_NAMES[forest.kernel],
             "binned": bool(args.binned),
+            "preprocess": args.pre,
+            "csr": bool(args.csr),
+            "labels": bool(args.labels),
             "plan": {k: v for k, v in plan.items() if not isinstance(v, float)},
         },
         "roofline": {
@@ -265,8 +341,13 @@ def main():
                            "note": "bins made once before the timed region; bin_ms is one "
                                    "binning pass over the same rows"}
         line["roofline"]["traffic"] = None
+    if args.pre != "none" or args.csr or args.labels:
+        line["roofline"]["traffic"] = None   # counters were taken on the plain prediction
+    if args.pre == "normalize":
+        line["note"] = ("a step is the row-norm pass plus the fused prediction; frac counts "
+                        "the step time against the prediction's visit bound")
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, out, args.cpu_sample_rows)
+        line["cpu_baseline"] = cpu_baseline(w, out, args.cpu_sample_rows, pre, args.labels)
     print(json.dumps(line), flush=True)
     forest.close()
 

@@ -94,26 +94,44 @@ __device__ __forceinline__ void staging_wave(uint8_t *smem, int n_chunks, uint32
   for (int i = 0; i < tail; ++i) __syncthreads();
 }
 
-// The fused preprocessing of feature f of row `row` (BRIDGER_PRE_* in bridger.h): each step in
-// double, rounded to float.
-__device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, int64_t row, float x) {
-  if (a.pre_kind == 1) {
+// The fused preprocessing of feature f (BRIDGER_PRE_* in bridger.h) with the kind fixed at
+// compile time: each step in double, rounded to float.  rn is the row's norm (NORMALIZE only).
+template <int KIND>
+__device__ __forceinline__ float preprocess_k(const LaunchArgs &a, int f, double rn, float x) {
+  if (KIND == 1) {
     const float x1 = (float)((double)x * a.pre_a[f]);
     return (float)((double)x1 + a.pre_b[f]);
   }
-  if (a.pre_kind == 2) {
+  if (KIND == 2) {
     const float x1 = (float)((double)x - a.pre_a[f]);
     return (float)((double)x1 / a.pre_b[f]);
   }
-  if (a.pre_kind == 3) return ((double)x > a.pre_a[f]) ? 1.0f : 0.0f;
-  if (a.pre_kind == 4) return (float)((double)x / a.row_norm[row]);
+  if (KIND == 3) return ((double)x > a.pre_a[f]) ? 1.0f : 0.0f;
+  if (KIND == 4) return (float)((double)x / rn);
   return x;
+}
+
+// The same with the kind read at run time; rn as above.
+__device__ __forceinline__ float preprocess_rt(const LaunchArgs &a, int f, double rn, float x) {
+  switch (a.pre_kind) {
+    case 1: return preprocess_k<1>(a, f, rn, x);
+    case 2: return preprocess_k<2>(a, f, rn, x);
+    case 3: return preprocess_k<3>(a, f, rn, x);
+    case 4: return preprocess_k<4>(a, f, rn, x);
+    default: return x;
+  }
+}
+
+// The same for feature f of row `row`.
+__device__ __forceinline__ float preprocess(const LaunchArgs &a, int f, int64_t row, float x) {
+  return preprocess_rt(a, f, a.pre_kind == 4 ? a.row_norm[row] : 1.0, x);
 }
 
 // Load part `part` of `parts` of this lane's row into the feature-major LDS tile (zeros past
 // the last row): the lane groups sharing a tile split each row's features between them.  With
 // NAN_TO_INF a NaN feature is stored as +inf: against finite thresholds both compare false
-// (x <= t), so every split sends them the same way.
+// (x <= t), so every split sends them the same way.  The row's norm (NORMALIZE) is loaded once
+// ahead of the loop.
 template <bool NAN_TO_INF = false>
 __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a, int r,
                                               int64_t row, bool row_ok, int part = 0,
@@ -128,8 +146,9 @@ __device__ __forceinline__ void load_row_tile(uint8_t *smem, const LaunchArgs &a
   const float *xr = a.X + row * (int64_t)a.F;
   auto body = [&](auto pre_tag) {
     constexpr bool PRE = decltype(pre_tag)::value;
+    const double rn = (PRE && a.pre_kind == 4) ? a.row_norm[row] : 1.0;
     auto put = [&](int f, float v) {
-      if (PRE) v = preprocess(a, f, row, v);
+      if (PRE) v = preprocess_rt(a, f, rn, v);
       if (NAN_TO_INF) v = (v != v) ? __builtin_inff() : v;
       xt[f * R + r] = v;
     };
