@@ -219,6 +219,21 @@ def random_tiny_forest(rng: np.random.Generator, n_trees: int, n_features: int, 
     return concat_trees(trees, n_features, n_classes, None, aggregate, transform)
 
 
+def with_vector_leaves(f: Forest, n_classes: int, rng: np.random.Generator,
+                       aggregate=AGG_MEAN, transform=XFORM_IDENTITY) -> Forest:
+    """The same trees with a class-probability vector in every leaf (a tree classifier's
+    leaves: random class counts, normalised), ``value`` of shape [N, n_classes] (zeros at
+    internal nodes).  Every tree votes in every class."""
+    leaf = f.left < 0
+    counts = rng.integers(0, 20, (f.n_nodes, n_classes)).astype(np.float64)
+    counts[leaf & (counts.sum(1) == 0), 0] = 1.0
+    v = np.zeros((f.n_nodes, n_classes), np.float32)
+    v[leaf] = (counts[leaf] / counts[leaf].sum(1, keepdims=True)).astype(np.float32)
+    return Forest(n_features=f.n_features, n_classes=n_classes, tree_offsets=f.tree_offsets,
+                  feature=f.feature, threshold=f.threshold, left=f.left, right=f.right, value=v,
+                  tree_class=None, aggregate=aggregate, transform=transform, base_score=None)
+
+
 # ------------------------------------------------------------------- workloads
 def _threshold_pool(seed, kind, n_features, x_params):
     return x_block(seed, kind, n_features, 0, **x_params)
