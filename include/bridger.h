@@ -79,7 +79,17 @@ enum {
   /* Validate and pack on the host only; no device is touched.  Predict calls on
    * such a handle fail with BRIDGER_ERR_INVALID_ARGUMENT.  Used to inspect the
    * packed layout and the launch plan on a machine without a GPU. */
-  BRIDGER_CREATE_HOST_ONLY = 1u
+  BRIDGER_CREATE_HOST_ONLY = 1u,
+  /* Vector leaves (tree classifiers: decision, extra and random forests of
+   * classification trees, whose leaves hold class probabilities; the aggregation
+   * category of Sec. 4.1): `value` holds n_classes floats per node, row-major
+   * [N, n_classes] (ignored at internal nodes), and every tree adds its leaf's
+   * vector to all n_classes outputs, in ascending tree order per class.  MEAN
+   * divides each class sum by n_trees (a random forest's averaged probabilities).
+   * tree_class must be NULL; the transform is IDENTITY or SOFTMAX.  Labels
+   * (predict_labels) are the class of largest averaged value.  Runs on the
+   * PERFECT, RAGGED and DIRECT kernels (GEMM: BRIDGER_ERR_UNSUPPORTED). */
+  BRIDGER_CREATE_VECTOR_LEAVES = 2u
 };
 
 /*

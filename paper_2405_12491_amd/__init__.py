@@ -33,6 +33,7 @@ BRIDGER_KERNEL_AUTO, BRIDGER_KERNEL_PERFECT, BRIDGER_KERNEL_RAGGED, BRIDGER_KERN
 BRIDGER_KERNEL_GEMM = 4
 KERNEL_NAMES = {0: "auto", 1: "perfect", 2: "ragged", 3: "direct", 4: "gemm"}
 BRIDGER_CREATE_HOST_ONLY = 1
+BRIDGER_CREATE_VECTOR_LEAVES = 2
 BRIDGER_PRE_NONE, BRIDGER_PRE_MINMAX, BRIDGER_PRE_CENTER_SCALE, BRIDGER_PRE_BINARIZE = 0, 1, 2, 3
 BRIDGER_PRE_NORMALIZE = 4
 
@@ -108,9 +109,12 @@ def _vp(a):
 def bridger_forest_create(n_trees, tree_offsets, feature, threshold, left, right, value,
                           n_features, n_classes, tree_class, aggregate, transform, base_score,
                           flags: int = 0) -> ctypes.c_void_p:
-    """Returns the opaque handle; arrays are numpy arrays of the documented dtypes."""
+    """Returns the opaque handle; arrays are numpy arrays of the documented dtypes.  A 2-D
+    ``value`` [N, n_classes] makes a vector-leaf forest (BRIDGER_CREATE_VECTOR_LEAVES)."""
     lib = load_library()
     h = ctypes.c_void_p()
+    if np.ndim(value) == 2:
+        flags |= BRIDGER_CREATE_VECTOR_LEAVES
     arrs = [np.ascontiguousarray(tree_offsets, np.int64), np.ascontiguousarray(feature, np.int32),
             np.ascontiguousarray(threshold, np.float32), np.ascontiguousarray(left, np.int32),
             np.ascontiguousarray(right, np.int32), np.ascontiguousarray(value, np.float32)]

@@ -117,6 +117,13 @@ struct bridger_forest {
   std::vector<double> pre_a, pre_b;
   void *d_pre_a = nullptr, *d_pre_b = nullptr;
 
+  // vector leaves (BRIDGER_CREATE_VECTOR_LEAVES): K class values per leaf, numbered as each
+  // kernel family finds its leaves (PERFECT: kernel tree x 2^D + leaf slot; RAGGED: record
+  // index; DIRECT: record index)
+  bool vec = false;
+  std::vector<float> vec_perfect, vec_ragged, vec_direct;
+  void *d_vec_perfect = nullptr, *d_vec_ragged = nullptr, *d_vec_direct = nullptr;
+
   // DIRECT
   std::vector<int32_t> direct_rec;  // 4 ints per record
   std::vector<int32_t> direct_root;
@@ -356,6 +363,40 @@ void pack_direct(bridger_forest *h, const int64_t *offs, const int32_t *feat, co
       h->direct_rec_node[r + i] = (int32_t)i;
     }
     r += n;
+  }
+}
+
+// Vector leaves: the K class values of every leaf, numbered as each kernel family finds its
+// leaves (PERFECT: kernel tree x 2^D + leaf slot; RAGGED and DIRECT: record index); zeros for
+// internal and filler records.
+void build_vector_leaves(bridger_forest *h, const int64_t *offs, const int32_t *left,
+                         const float *value) {
+  const int K = h->K;
+  auto put = [&](std::vector<float> &dst, size_t slot, int32_t t, int32_t nd) {
+    if (nd < 0) return;  // filler record
+    const int64_t i = offs[t] + nd;
+    if (left[i] != -1) return;
+    std::memcpy(&dst[slot * K], &value[i * K], sizeof(float) * K);
+  };
+  if (!h->perfect_leaf_map.empty()) {
+    const size_t n_leaf = (size_t)1 << h->perfect_depth;
+    h->vec_perfect.assign(n_leaf * h->n_trees * K, 0.0f);
+    for (int32_t k = 0; k < h->n_trees; ++k)
+      for (size_t j = 0; j < n_leaf; ++j)
+        put(h->vec_perfect, k * n_leaf + j, h->tree_order[k], h->perfect_leaf_map[k * n_leaf + j]);
+  }
+  if (!h->ragged_rec.empty()) {
+    h->vec_ragged.assign(h->ragged_rec.size() * K, 0.0f);
+    for (int32_t k = 0; k < h->n_trees; ++k)
+      for (int32_t r = h->ragged_tree_start[k]; r < h->ragged_tree_start[k + 1]; ++r)
+        put(h->vec_ragged, r, h->tree_order[k], h->ragged_rec_node[r]);
+  }
+  h->vec_direct.assign(h->direct_rec_node.size() * K, 0.0f);
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int32_t t = h->tree_order[k];
+    const int64_t n = offs[t + 1] - offs[t];
+    for (int64_t i = 0; i < n; ++i)
+      put(h->vec_direct, h->direct_root[k] + i, t, h->direct_rec_node[h->direct_root[k] + i]);
   }
 }
 
@@ -684,7 +725,8 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_perfect_trav);
   free_dev(h->d_perfect_roots);
   for (void **q : {&h->d_q_values, &h->d_q_off, &h->d_perfect_btrav, &h->d_ragged_brec,
-                   &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b})
+                   &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b,
+                   &h->d_vec_perfect, &h->d_vec_ragged, &h->d_vec_direct})
     free_dev(*q);
   for (DevArrays *d : {&h->d_perfect, &h->d_ragged, &h->d_direct}) {
     free_dev(d->nodes);
@@ -728,6 +770,13 @@ bridger_status upload_all(bridger_forest *h) {
   if ((s = upload(&h->d_direct.nodes, h->direct_rec)) != BRIDGER_OK) return s;
   if ((s = upload(&h->d_direct.tree_start, h->direct_root)) != BRIDGER_OK) return s;
   if ((s = upload(&h->d_direct.leaf_map, h->direct_rec_node)) != BRIDGER_OK) return s;
+  if (h->vec) {
+    if (!h->vec_perfect.empty() && (s = upload(&h->d_vec_perfect, h->vec_perfect)) != BRIDGER_OK)
+      return s;
+    if (!h->vec_ragged.empty() && (s = upload(&h->d_vec_ragged, h->vec_ragged)) != BRIDGER_OK)
+      return s;
+    if ((s = upload(&h->d_vec_direct, h->vec_direct)) != BRIDGER_OK) return s;
+  }
   return BRIDGER_OK;
 }
 
@@ -875,6 +924,8 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
     a.chunk_first = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_first : d.chunk_first);
     a.chunk_rec = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_rec : d.chunk_rec);
     a.leaf_map = (const int32_t *)d.leaf_map;
+    a.vec = h->vec ? 1 : 0;
+    a.leaf_vec = (const float *)(perfect ? h->d_vec_perfect : h->d_vec_ragged);
     a.tree_bytes = h->perfect_tree_bytes;
     a.trees_per_chunk = p.trees_per_chunk;
     a.n_chunks = p.n_chunks;
@@ -912,6 +963,8 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
     a.nodes = (const uint8_t *)h->d_direct.nodes;
     a.tree_start = (const int32_t *)h->d_direct.tree_start;
     a.leaf_map = (const int32_t *)h->d_direct.leaf_map;
+    a.vec = h->vec ? 1 : 0;
+    a.leaf_vec = (const float *)h->d_vec_direct;
     const int64_t n_wg = (n_rows + 255) / 256;
     err = launch_direct(a, n_wg, stream);
   }
@@ -954,8 +1007,12 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "sigmoid needs n_classes == 1");
   if (transform == BRIDGER_XFORM_SOFTMAX && n_classes < 2)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "softmax needs n_classes >= 2");
-  if (flags & ~(uint32_t)BRIDGER_CREATE_HOST_ONLY)
+  if (flags & ~(uint32_t)(BRIDGER_CREATE_HOST_ONLY | BRIDGER_CREATE_VECTOR_LEAVES))
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "unknown flags");
+  // one class: a vector leaf is a scalar leaf
+  const bool vec = (flags & BRIDGER_CREATE_VECTOR_LEAVES) && n_classes > 1;
+  if (vec && tree_class)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "vector leaves take no tree_class");
   if (tree_offsets[0] != 0) return fail(BRIDGER_ERR_INVALID_FOREST, "tree_offsets[0] != 0");
   for (int32_t t = 0; t < n_trees; ++t)
     if (tree_offsets[t + 1] <= tree_offsets[t])
@@ -964,7 +1021,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     return fail(BRIDGER_ERR_UNSUPPORTED, "too many nodes");
   std::vector<int32_t> klass(n_trees);
   for (int32_t t = 0; t < n_trees; ++t) {
-    klass[t] = tree_class ? tree_class[t] : t % n_classes;
+    klass[t] = vec ? 0 : (tree_class ? tree_class[t] : t % n_classes);
     if (klass[t] < 0 || klass[t] >= n_classes)
       return fail(BRIDGER_ERR_INVALID_ARGUMENT, "tree_class out of range");
   }
@@ -1008,9 +1065,11 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     h->all_perfect = all_perfect ? 1 : 0;
     h->perfect_depth = all_perfect ? common_depth : -1;
 
-    // class-major stable tree order
+    // class-major stable tree order (vector leaves: caller order, every tree in every class)
+    h->vec = vec;
     h->class_count.assign(n_classes, 0);
     for (int32_t t = 0; t < n_trees; ++t) h->class_count[klass[t]]++;
+    if (vec) h->class_count.assign(n_classes, n_trees);
     if (aggregate == BRIDGER_AGG_MEAN)
       for (int32_t k = 0; k < n_classes; ++k)
         if (h->class_count[k] == 0) {
@@ -1020,7 +1079,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         }
     h->class_begin.assign(n_classes + 1, 0);
     for (int32_t k = 0; k < n_classes; ++k)
-      h->class_begin[k + 1] = h->class_begin[k] + h->class_count[k];
+      h->class_begin[k + 1] = h->class_begin[k] + (vec ? (k == 0 ? n_trees : 0) : h->class_count[k]);
     h->tree_order.resize(n_trees);
     {
       std::vector<int32_t> fill(h->class_begin.begin(), h->class_begin.end() - 1);
@@ -1030,7 +1089,14 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     if (base_score)
       for (int32_t k = 0; k < n_classes; ++k) h->base[k] = base_score[k];
 
-    // packing
+    // packing (vector leaves: the packers lay out class 0's values; the class vectors follow)
+    std::vector<float> value0;
+    const float *value_vec = value;
+    if (vec) {
+      value0.resize(h->n_nodes);
+      for (int64_t i = 0; i < h->n_nodes; ++i) value0[i] = value[i * n_classes];
+      value = value0.data();
+    }
     pack_direct(h, tree_offsets, feature, threshold, left, right, value);
     const int D = h->perfect_depth;
     if (all_perfect && D >= 1 && D <= kMaxPerfectDepth) {
@@ -1074,6 +1140,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         }
       }
     }
+    if (vec) build_vector_leaves(h, tree_offsets, left, value_vec);
     if (env_int("BRIDGER_LOG", 0)) {
       auto show = [](const char *what, const Plan &p) {
         if (p.waves)

@@ -116,6 +116,8 @@ struct LaunchArgs {
   int32_t pre_kind;            // fused preprocessing (BRIDGER_PRE_*), 0 = none
   const double *pre_a, *pre_b; // its per-feature parameters
   const double *row_norm;      // NORMALIZE: each row's L2 norm in double (1 for a zero row)
+  int32_t vec;                 // vector leaves: K class values per leaf in leaf_vec
+  const float *leaf_vec;       // [leaf index][K], leaf index as the family numbers leaves
 };
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.

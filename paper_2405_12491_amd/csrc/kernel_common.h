@@ -357,6 +357,29 @@ __device__ __forceinline__ void class_flush_all(const LaunchArgs &a, ClassAcc &c
   }
 }
 
+// Vector leaves: each tree adds its leaf's K class values to all K class sums, which live in
+// LDS (slot k * slot_stride) from the start.  vec_add takes the leaves of N consecutive trees
+// (the family's leaf indices into a.leaf_vec) and adds them class by class in tree order: one
+// LDS read and write per class for the N trees.
+__device__ __forceinline__ void vec_init(const LaunchArgs &a, double *acc_lds, int slot_stride,
+                                         bool first_group) {
+  for (int k = 0; k < a.K; ++k) acc_lds[k * slot_stride] = class_init(a, k, first_group);
+}
+
+template <int N>
+__device__ __forceinline__ void vec_add(const LaunchArgs &a, double *acc_lds, int slot_stride,
+                                        const int64_t (&leaf)[N]) {
+  const float *v[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u) v[u] = a.leaf_vec + leaf[u] * a.K;
+  for (int k = 0; k < a.K; ++k) {
+    double s = acc_lds[k * slot_stride];
+#pragma unroll
+    for (int u = 0; u < N; ++u) s += (double)v[u][k];
+    acc_lds[k * slot_stride] = s;
+  }
+}
+
 // ====================================================================== launchers
 // Raise a kernel's dynamic-LDS limit once per (kernel, device) to the largest size used.
 static inline int ensure_lds_limit(const void *kernel, int lds_bytes) {

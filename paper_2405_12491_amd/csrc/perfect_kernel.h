@@ -6,7 +6,7 @@
 
 namespace bridger {
 
-template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB>
+template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, bool VEC = false>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -41,6 +41,7 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = SIMPLE ? (a.aggregate == 0 ? (double)a.base[0] : 0.0) : class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
 
   // leaf ids or leaf values of N walked trees, kernel trees q .. q + N - 1
   auto finish = [&](auto &m, int q, uint32_t b0) {
@@ -54,6 +55,11 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
               a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
         }
       }
+    } else if (VEC) {
+      int64_t leaf[N];
+#pragma unroll
+      for (int u = 0; u < N; ++u) leaf[u] = (int64_t)(q + u) * (1 << D) + (m[u] - kFirstLeaf);
+      vec_add(a, acc_lds, slot_stride, leaf);
     } else {
       float lv[N];
 #pragma unroll
@@ -96,7 +102,7 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     }
     return;
   }
-  class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  if (!VEC) class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   __syncthreads();
   if (g == 0) {
     double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
@@ -119,6 +125,8 @@ static int launch_perfect_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int 
   const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(perfect_kernel<D, 4, true, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec)  // vector leaves: K >= 2, so never the simple variant
+    return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, true>, threads, n_wg, lds_bytes, stream, a);
   if (simple)
     return launch_common(perfect_kernel<D, 4, false, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 1)

@@ -15,7 +15,7 @@ __device__ __forceinline__ bool goes_right(uint32_t x, uint32_t w) {
 // internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
 // adds the value and jumps to the next tree's root.  Lanes never wait for each other inside
 // a chunk, so a short path in one tree is not padded to the wave's longest path.
-template <bool LEAVES, bool SIMPLE, int XB>
+template <bool LEAVES, bool SIMPLE, int XB, bool VEC = false>
 __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -45,6 +45,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
 
   for (int c = 0; c < a.n_chunks; ++c) {
     const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
@@ -68,6 +69,9 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
           if (row_ok)
             a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
                 a.leaf_map[rec0 + (int)((addr - buf) >> 3)];
+        } else if (VEC) {
+          const int64_t leaf[1] = {rec0 + (int)((addr - buf) >> 3)};
+          vec_add(a, acc_lds, slot_stride, leaf);
         } else {
           if (!SIMPLE) class_advance(a, ca, t, acc_lds, slot_stride, g == 0);
           ca.acc += (double)__uint_as_float(rec.x);
@@ -92,7 +96,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   }
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
-  } else {
+  } else if (!VEC) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
@@ -114,7 +118,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
 // trees together (a lane that reached its leaf idles until the wave's deepest path ends), so
 // one wave-wide gather touches only the few cache lines of those trees' current levels
 // rather than records of many trees at once.  Leaves are added in tree order.
-template <bool LEAVES, bool SIMPLE, int U, int XB>
+template <bool LEAVES, bool SIMPLE, int U, int XB, bool VEC = false>
 __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -136,6 +140,7 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
+  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
 
   const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
   const uint2 *recs = reinterpret_cast<const uint2 *>(a.nodes);
@@ -173,6 +178,10 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
         }
       }
     }
+    if (VEC) {
+      vec_add(a, acc_lds, slot_stride, idx);
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < N; ++u) {
       if (LEAVES) {
@@ -189,7 +198,7 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   if (LEAVES) return;
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
-  } else {
+  } else if (!VEC) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
@@ -211,6 +220,8 @@ static int launch_ragged_global_xu(const LaunchArgs &a, int waves, int64_t n_wg,
   const int threads = 64 * waves;
   if (a.out_leaf)
     return launch_common(ragged_global_kernel<true, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec)
+    return launch_common(ragged_global_kernel<false, false, 4, XB, true>, threads, n_wg, lds_bytes, stream, a);
   if (a.K != 1)
     return launch_common(ragged_global_kernel<false, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(ragged_global_kernel<false, true, U, XB>, threads, n_wg, lds_bytes, stream, a);
@@ -238,6 +249,8 @@ static int launch_ragged_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds
   const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(ragged_kernel<true, false, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec)
+    return launch_common(ragged_kernel<false, false, XB, true>, threads, n_wg, lds_bytes, stream, a);
   if (simple)
     return launch_common(ragged_kernel<false, true, XB>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(ragged_kernel<false, false, XB>, threads, n_wg, lds_bytes, stream, a);

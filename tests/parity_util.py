@@ -75,3 +75,24 @@ def check_parity(model, X: np.ndarray, kernel: int, what: str, exact_sum: bool =
     finally:
         if own:
             forest.close()
+
+
+# Labels: where the oracle's top two values lie within TIE (relative) of each other, different
+# summation orders may legitimately split them, and any class that close to the top is accepted.
+TIE = 1e-12
+
+
+def check_labels(got, ref, what):
+    n, K = ref.shape
+    if K == 1:
+        want = (ref[:, 0] > 0.5).astype(np.int32)
+        sure = np.abs(ref[:, 0] - 0.5) > TIE
+    else:
+        want = np.argmax(ref, axis=1).astype(np.int32)
+        top = np.sort(ref, axis=1)
+        sure = (top[:, -1] - top[:, -2]) > TIE * np.maximum(1.0, np.abs(top[:, -1]))
+    bad = np.flatnonzero(sure & (got != want))
+    assert bad.size == 0, f"{what}: {bad.size} labels differ, first row {bad[:1]}"
+    for i in np.flatnonzero(~sure):   # near ties: any class within rounding of the top
+        assert K > 1 and ref[i, got[i]] >= ref[i].max() - TIE * max(1.0, abs(ref[i].max())), what
+    assert np.all((got >= 0) & (got < max(K, 2)))

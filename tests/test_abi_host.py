@@ -86,6 +86,22 @@ def test_validation_errors():
     assert _create_err(aggregate=AGG_MEAN, n_classes=2, tree_class=np.array([1], np.int32)) == ARG
     assert _create_err(aggregate=7) == ARG
     assert _create_err(flags=8) == ARG
+    # vector leaves: [N, K] values, no tree_class
+    f = _tiny()
+    v2 = np.stack([f.value, 1 - f.value], 1)
+    assert _create_err(value=v2, n_classes=2, tree_class=np.array([1], np.int32)) == ARG
+
+
+def test_vector_leaf_forest_on_host():
+    f = _tiny()
+    for K in (1, 3):
+        v = np.repeat(f.value[:, None], K, 1) * np.arange(1, K + 1, dtype=np.float32)[None, :]
+        h = B.bridger_forest_create(f.n_trees, f.tree_offsets, f.feature, f.threshold, f.left,
+                                    f.right, v, 2, K, None, AGG_MEAN, 0, None,
+                                    B.BRIDGER_CREATE_HOST_ONLY)
+        info = B.bridger_forest_info(h)
+        assert info["n_outputs"] == K and info["all_perfect"] == 1
+        B.load_library().bridger_forest_destroy(h)
 
 
 def test_null_pointer_arguments():

@@ -5,14 +5,13 @@ import numpy as np
 import pytest
 
 import paper_2405_12491_amd as B
-from parity_util import oracle_predict, to_dev
+from parity_util import check_labels as _check_labels, oracle_predict, to_dev
 from synth import (AGG_MEAN, XFORM_IDENTITY, XFORM_SOFTMAX, make_workload, random_tiny_forest)
 
 pytestmark = pytest.mark.gpu
 
 KERNELS = [B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT,
            B.BRIDGER_KERNEL_GEMM]
-TIE = 1e-12
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -22,22 +21,6 @@ def _cuda():
         pytest.skip("no GPU")
     B.load_library()
     yield
-
-
-def _check_labels(got, ref, what):
-    n, K = ref.shape
-    if K == 1:
-        want = (ref[:, 0] > 0.5).astype(np.int32)
-        sure = np.abs(ref[:, 0] - 0.5) > TIE
-    else:
-        want = np.argmax(ref, axis=1).astype(np.int32)
-        top = np.sort(ref, axis=1)
-        sure = (top[:, -1] - top[:, -2]) > TIE * np.maximum(1.0, np.abs(top[:, -1]))
-    bad = np.flatnonzero(sure & (got != want))
-    assert bad.size == 0, f"{what}: {bad.size} labels differ, first row {bad[:1]}"
-    for i in np.flatnonzero(~sure):   # near ties: any class within rounding of the top
-        assert K > 1 and ref[i, got[i]] >= ref[i].max() - TIE * max(1.0, abs(ref[i].max())), what
-    assert np.all((got >= 0) & (got < max(K, 2)))
 
 
 @pytest.mark.parametrize("case", ["mc_gbdt_d8", "gbdt_d6", "shallow_d3", "ragged_mean3"])
