@@ -90,6 +90,9 @@ def parse():
                    help="rows handed over in CSR form (built once, untimed)")
     p.add_argument("--labels", action="store_true",
                    help="write int32 class labels instead of scores")
+    p.add_argument("--vector", type=int, default=0, metavar="K",
+                   help="the workload's trees with a K-class probability vector in every leaf "
+                        "(a forest classifier: averaged class vectors)")
     p.add_argument("--calib-copy", action="store_true",
                    help="time a plain device copy of X instead (counter calibration)")
     return p.parse_args()
@@ -175,7 +178,11 @@ def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False
     t0 = time.perf_counter()
     if pre[0] != "none":
         X = P.apply(PRE_KINDS[pre[0]], pre[1], pre[2], X)
-    ref, _, visits = oracle.predict(w.forest, X, threads=threads)
+    if np.ndim(w.forest.value) == 2:
+        from oracle import vector as V
+        ref, _, visits = V.predict(w.forest, X, threads=threads, with_visits=True)
+    else:
+        ref, _, visits = oracle.predict(w.forest, X, threads=threads)
     dt = time.perf_counter() - t0
     got = out_dev[:n].cpu().numpy()
     if labels:
@@ -204,6 +211,11 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = make_workload(args.workload, args.rows)
+    if args.vector:
+        import dataclasses
+        from synth import with_vector_leaves
+        w = dataclasses.replace(w, forest=with_vector_leaves(
+            w.forest, args.vector, np.random.default_rng(1000 + args.vector)))
     Xd = build_x(w, dev)
     stream = torch.cuda.current_stream(dev)
 
@@ -315,6 +327,7 @@ def main():
             "preprocess": args.pre,
             "csr": bool(args.csr),
             "labels": bool(args.labels),
+            "vector_leaves": args.vector or None,
             "plan": {k: v for k, v in plan.items() if not isinstance(v, float)},
         },
         "roofline": {
@@ -341,7 +354,7 @@ def main():
                            "note": "bins made once before the timed region; bin_ms is one "
                                    "binning pass over the same rows"}
         line["roofline"]["traffic"] = None
-    if args.pre != "none" or args.csr or args.labels:
+    if args.pre != "none" or args.csr or args.labels or args.vector:
         line["roofline"]["traffic"] = None   # counters were taken on the plain prediction
     if args.pre == "normalize":
         line["note"] = ("a step is the row-norm pass plus the fused prediction; frac counts "

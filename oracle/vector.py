@@ -26,10 +26,11 @@ AGG_SUM, AGG_MEAN = 0, 1
 XFORM_IDENTITY, XFORM_SOFTMAX = 0, 2
 
 
-def leaves(forest, X: np.ndarray, threads: int = 1) -> np.ndarray:
-    """Tree-local leaf ids [n, T] from the scalar oracle's walk (the leaf values play no part)."""
-    _, lv, _ = _scalar_predict(_as_scalar(forest), X, want_leaves=True, threads=threads)
-    return lv
+def leaves(forest, X: np.ndarray, threads: int = 1, with_visits: bool = False):
+    """Tree-local leaf ids [n, T] from the scalar oracle's walk (the leaf values play no part);
+    with_visits: also the number of internal-node visits."""
+    _, lv, visits = _scalar_predict(_as_scalar(forest), X, want_leaves=True, threads=threads)
+    return (lv, visits) if with_visits else lv
 
 
 def _as_scalar(forest):
@@ -42,13 +43,14 @@ def _as_scalar(forest):
                                base_score=None)
 
 
-def predict(forest, X: np.ndarray, threads: int = 1):
-    """(out float64 [n, K], leaves int32 [n, T]) for a forest whose ``value`` is [N, K]."""
+def predict(forest, X: np.ndarray, threads: int = 1, with_visits: bool = False):
+    """(out float64 [n, K], leaves int32 [n, T]) for a forest whose ``value`` is [N, K]; with
+    with_visits, also the number of internal-node visits."""
     V = np.asarray(forest.value, np.float32)
     assert V.ndim == 2, "value must hold one row of class values per node"
     K = V.shape[1]
     T = int(forest.n_trees)
-    lv = leaves(forest, X, threads)
+    lv, visits = leaves(forest, X, threads, with_visits=True)
     n = lv.shape[0]
     base = np.zeros(K) if forest.base_score is None else np.asarray(forest.base_score, np.float64)
     acc = np.tile(base, (n, 1)) if forest.aggregate == AGG_SUM else np.zeros((n, K))
@@ -65,7 +67,7 @@ def predict(forest, X: np.ndarray, threads: int = 1):
         z = e / s[:, None]
     elif forest.transform != XFORM_IDENTITY:
         raise ValueError("vector leaves take the identity or softmax link")
-    return z, lv
+    return (z, lv, visits) if with_visits else (z, lv)
 
 
 def labels(out: np.ndarray) -> np.ndarray:

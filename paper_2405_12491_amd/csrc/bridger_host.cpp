@@ -366,32 +366,32 @@ void pack_direct(bridger_forest *h, const int64_t *offs, const int32_t *feat, co
   }
 }
 
-// Vector leaves: the K class values of every leaf, numbered as each kernel family finds its
-// leaves (PERFECT: kernel tree x 2^D + leaf slot; RAGGED and DIRECT: record index); zeros for
-// internal and filler records.
+// Vector leaves: the K class values of every leaf (rows of vec_stride(K) floats), numbered as
+// each kernel family finds its leaves (PERFECT: kernel tree x 2^D + leaf slot; RAGGED and
+// DIRECT: record index); zeros for internal and filler records and for the padding.
 void build_vector_leaves(bridger_forest *h, const int64_t *offs, const int32_t *left,
                          const float *value) {
-  const int K = h->K;
+  const int K = h->K, KS = vec_stride(K);  // rows padded with zeros to whole 16-byte groups
   auto put = [&](std::vector<float> &dst, size_t slot, int32_t t, int32_t nd) {
     if (nd < 0) return;  // filler record
     const int64_t i = offs[t] + nd;
     if (left[i] != -1) return;
-    std::memcpy(&dst[slot * K], &value[i * K], sizeof(float) * K);
+    std::memcpy(&dst[slot * KS], &value[i * K], sizeof(float) * K);
   };
   if (!h->perfect_leaf_map.empty()) {
     const size_t n_leaf = (size_t)1 << h->perfect_depth;
-    h->vec_perfect.assign(n_leaf * h->n_trees * K, 0.0f);
+    h->vec_perfect.assign(n_leaf * h->n_trees * KS, 0.0f);
     for (int32_t k = 0; k < h->n_trees; ++k)
       for (size_t j = 0; j < n_leaf; ++j)
         put(h->vec_perfect, k * n_leaf + j, h->tree_order[k], h->perfect_leaf_map[k * n_leaf + j]);
   }
   if (!h->ragged_rec.empty()) {
-    h->vec_ragged.assign(h->ragged_rec.size() * K, 0.0f);
+    h->vec_ragged.assign(h->ragged_rec.size() * KS, 0.0f);
     for (int32_t k = 0; k < h->n_trees; ++k)
       for (int32_t r = h->ragged_tree_start[k]; r < h->ragged_tree_start[k + 1]; ++r)
         put(h->vec_ragged, r, h->tree_order[k], h->ragged_rec_node[r]);
   }
-  h->vec_direct.assign(h->direct_rec_node.size() * K, 0.0f);
+  h->vec_direct.assign(h->direct_rec_node.size() * KS, 0.0f);
   for (int32_t k = 0; k < h->n_trees; ++k) {
     const int32_t t = h->tree_order[k];
     const int64_t n = offs[t + 1] - offs[t];

@@ -117,8 +117,11 @@ struct LaunchArgs {
   const double *pre_a, *pre_b; // its per-feature parameters
   const double *row_norm;      // NORMALIZE: each row's L2 norm in double (1 for a zero row)
   int32_t vec;                 // vector leaves: K class values per leaf in leaf_vec
-  const float *leaf_vec;       // [leaf index][K], leaf index as the family numbers leaves
+  const float *leaf_vec;       // [leaf index][vec_stride(K)], as the family numbers leaves
 };
+
+// Vector leaves: floats per leaf in leaf_vec, K rounded up to whole 16-byte groups.
+constexpr int32_t vec_stride(int32_t K) { return (K + 3) & ~3; }
 
 // Kernel launchers (defined in the .hip files).  Return a hipError_t as int.
 int launch_perfect(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

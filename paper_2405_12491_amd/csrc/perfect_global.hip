@@ -11,7 +11,8 @@
 
 namespace bridger {
 
-template <int D, int U, bool LEAVES, bool FIN, int XB, bool VEC = false>
+// VK: 0 scalar leaves; kVecRegClasses or 64 vector leaves (class sums in registers / LDS).
+template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -36,7 +37,9 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = a.class_begin[1];
-  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
+  double vacc[kVecRegClasses];
+  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   auto finish = [&](auto &m, int q) {
     constexpr int N = sizeof(m) / sizeof(m[0]);
@@ -49,11 +52,12 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
               a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
         }
       }
-    } else if (VEC) {
+    } else if (VK) {
       int64_t leaf[N];
 #pragma unroll
       for (int u = 0; u < N; ++u) leaf[u] = (int64_t)(q + u) * (1 << D) + (m[u] - kFirstLeaf);
-      vec_add(a, acc_lds, slot_stride, leaf);
+      if (VK == kVecRegClasses) vec_add_reg(a, vacc, leaf);
+      else vec_add(a, acc_lds, slot_stride, leaf);
     } else {
       float lv[N];
 #pragma unroll
@@ -80,7 +84,8 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
     finish(m, q);
   }
   if (LEAVES) return;
-  if (!VEC) class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  if (VK == kVecRegClasses) vec_store_reg(a, vacc, acc_lds, slot_stride);
+  else if (!VK) class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   __syncthreads();
   if (g == 0) {
     double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
@@ -100,8 +105,10 @@ static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int l
   const int threads = 64 * waves;
   if (a.out_leaf)
     return launch_common(perfect_global_kernel<D, 4, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= kVecRegClasses)
+    return launch_common(perfect_global_kernel<D, 4, false, FIN, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec)
-    return launch_common(perfect_global_kernel<D, 4, false, FIN, XB, true>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_global_kernel<D, 4, false, FIN, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 4)
     return launch_common(perfect_global_kernel<D, 4, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(perfect_global_kernel<D, 8, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);

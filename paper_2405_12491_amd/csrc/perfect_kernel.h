@@ -6,7 +6,9 @@
 
 namespace bridger {
 
-template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, bool VEC = false>
+// VK: 0 scalar leaves; kVecRegClasses vector leaves with the class sums in registers; 64
+// vector leaves with the class sums in LDS.
+template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -41,7 +43,9 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = SIMPLE ? (a.aggregate == 0 ? (double)a.base[0] : 0.0) : class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
-  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
+  double vacc[kVecRegClasses];
+  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   // leaf ids or leaf values of N walked trees, kernel trees q .. q + N - 1
   auto finish = [&](auto &m, int q, uint32_t b0) {
@@ -55,11 +59,12 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
               a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
         }
       }
-    } else if (VEC) {
+    } else if (VK) {
       int64_t leaf[N];
 #pragma unroll
       for (int u = 0; u < N; ++u) leaf[u] = (int64_t)(q + u) * (1 << D) + (m[u] - kFirstLeaf);
-      vec_add(a, acc_lds, slot_stride, leaf);
+      if (VK == kVecRegClasses) vec_add_reg(a, vacc, leaf);
+      else vec_add(a, acc_lds, slot_stride, leaf);
     } else {
       float lv[N];
 #pragma unroll
@@ -102,7 +107,8 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     }
     return;
   }
-  if (!VEC) class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  if (VK == kVecRegClasses) vec_store_reg(a, vacc, acc_lds, slot_stride);
+  else if (!VK) class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   __syncthreads();
   if (g == 0) {
     double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
@@ -125,8 +131,10 @@ static int launch_perfect_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int 
   const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(perfect_kernel<D, 4, true, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.vec)  // vector leaves: K >= 2, so never the simple variant
-    return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, true>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= kVecRegClasses)  // vector leaves: K >= 2, so never the simple variant
+    return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec)
+    return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (simple)
     return launch_common(perfect_kernel<D, 4, false, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 1)

@@ -15,7 +15,8 @@ __device__ __forceinline__ bool goes_right(uint32_t x, uint32_t w) {
 // internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
 // adds the value and jumps to the next tree's root.  Lanes never wait for each other inside
 // a chunk, so a short path in one tree is not padded to the wave's longest path.
-template <bool LEAVES, bool SIMPLE, int XB, bool VEC = false>
+// VK: 0 scalar leaves; kVecRegClasses or 64 vector leaves (class sums in registers / LDS).
+template <bool LEAVES, bool SIMPLE, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -45,7 +46,9 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
-  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
+  double vacc[kVecRegClasses];
+  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   for (int c = 0; c < a.n_chunks; ++c) {
     const uint32_t buf = (c & 1) ? (uint32_t)a.chunk_bytes : 0u;
@@ -69,9 +72,10 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
           if (row_ok)
             a.out_leaf[row * (int64_t)T + a.tree_order[t]] =
                 a.leaf_map[rec0 + (int)((addr - buf) >> 3)];
-        } else if (VEC) {
+        } else if (VK) {
           const int64_t leaf[1] = {rec0 + (int)((addr - buf) >> 3)};
-          vec_add(a, acc_lds, slot_stride, leaf);
+          if (VK == kVecRegClasses) vec_add_reg(a, vacc, leaf);
+          else vec_add(a, acc_lds, slot_stride, leaf);
         } else {
           if (!SIMPLE) class_advance(a, ca, t, acc_lds, slot_stride, g == 0);
           ca.acc += (double)__uint_as_float(rec.x);
@@ -96,7 +100,9 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   }
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
-  } else if (!VEC) {
+  } else if (VK == kVecRegClasses) {
+    vec_store_reg(a, vacc, acc_lds, slot_stride);
+  } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
@@ -118,7 +124,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
 // trees together (a lane that reached its leaf idles until the wave's deepest path ends), so
 // one wave-wide gather touches only the few cache lines of those trees' current levels
 // rather than records of many trees at once.  Leaves are added in tree order.
-template <bool LEAVES, bool SIMPLE, int U, int XB, bool VEC = false>
+template <bool LEAVES, bool SIMPLE, int U, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x;
@@ -140,7 +146,9 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
-  if (VEC) vec_init(a, acc_lds, slot_stride, g == 0);
+  double vacc[kVecRegClasses];
+  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
   const uint2 *recs = reinterpret_cast<const uint2 *>(a.nodes);
@@ -178,7 +186,11 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
         }
       }
     }
-    if (VEC) {
+    if (VK == kVecRegClasses) {
+      vec_add_reg(a, vacc, idx);
+      return;
+    }
+    if (VK == 64) {
       vec_add(a, acc_lds, slot_stride, idx);
       return;
     }
@@ -198,7 +210,9 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   if (LEAVES) return;
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
-  } else if (!VEC) {
+  } else if (VK == kVecRegClasses) {
+    vec_store_reg(a, vacc, acc_lds, slot_stride);
+  } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
@@ -220,8 +234,10 @@ static int launch_ragged_global_xu(const LaunchArgs &a, int waves, int64_t n_wg,
   const int threads = 64 * waves;
   if (a.out_leaf)
     return launch_common(ragged_global_kernel<true, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= kVecRegClasses)
+    return launch_common(ragged_global_kernel<false, false, 4, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec)
-    return launch_common(ragged_global_kernel<false, false, 4, XB, true>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(ragged_global_kernel<false, false, 4, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (a.K != 1)
     return launch_common(ragged_global_kernel<false, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(ragged_global_kernel<false, true, U, XB>, threads, n_wg, lds_bytes, stream, a);
@@ -249,8 +265,10 @@ static int launch_ragged_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds
   const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(ragged_kernel<true, false, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= kVecRegClasses)
+    return launch_common(ragged_kernel<false, false, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec)
-    return launch_common(ragged_kernel<false, false, XB, true>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(ragged_kernel<false, false, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (simple)
     return launch_common(ragged_kernel<false, true, XB>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(ragged_kernel<false, false, XB>, threads, n_wg, lds_bytes, stream, a);
