@@ -399,3 +399,58 @@ def test_workload_full_size_sampled(name):
             assert_leaves(lv, ref_lv, f"{name} full-size leaves @{a}")
     del Xd
     torch.cuda.empty_cache()
+
+
+def _chain_tree(depth, F, rng):
+    """A tree of the given depth shaped as a chain: internal node k (id 2k) has a leaf on its
+    left (id 2k + 1) and internal node k + 1 on its right; the last right child is a leaf.
+    Most thresholds are low, so most rows run deep; every eighth is 0.0."""
+    n = 2 * depth + 1
+    feat = np.full(n, -1, np.int32)
+    thr = np.zeros(n, np.float32)
+    left = np.full(n, -1, np.int32)
+    right = np.full(n, -1, np.int32)
+    val = rng.standard_normal(n).astype(np.float32)
+    for k in range(depth):
+        feat[2 * k] = k % F
+        thr[2 * k] = 0.0 if k % 8 == 7 else -5.0
+        left[2 * k], right[2 * k] = 2 * k + 1, 2 * k + 2
+        val[2 * k] = 0.0
+    return feat, thr, left, right, val
+
+
+def test_maximum_sizes():
+    """Limits: 64 classes; a depth-64 tree; perfect trees of depth 10 (the PERFECT limit) and 11;
+    rows of 5,000 features (no LDS plan fits: the DIRECT fallback)."""
+    rng = np.random.default_rng(64)
+    X12 = rng.standard_normal((777, 12)).astype(np.float32)
+    cases = []
+    T = 128
+    trees = [perfect_tree_arrays(3, rng.integers(0, 12, 7), rng.standard_normal(7).astype(np.float32),
+                                 rng.standard_normal(8).astype(np.float32)) for _ in range(T)]
+    cases.append(("64 classes", concat_trees(trees, 12, 64, np.arange(T) % 64, AGG_SUM, XFORM_SOFTMAX,
+                                             rng.standard_normal(64).astype(np.float32)), X12))
+    deep = [_chain_tree(64, 12, rng), _chain_tree(40, 12, rng)]
+    cases.append(("depth 64", concat_trees(deep, 12), X12))
+    for D in (10, 11):
+        n_int = (1 << D) - 1
+        trees = [perfect_tree_arrays(D, rng.integers(0, 12, n_int),
+                                     rng.standard_normal(n_int).astype(np.float32),
+                                     rng.standard_normal(n_int + 1).astype(np.float32))
+                 for _ in range(2)]
+        cases.append((f"perfect depth {D}", concat_trees(trees, 12), X12))
+    wide = random_tiny_forest(rng, 12, 5000, max_depth=6)
+    cases.append(("5000 features", wide, rng.standard_normal((300, 5000)).astype(np.float32)))
+    for name, model, X in cases:
+        with B.Forest(model) as f:
+            ran = []
+            for k in KERNELS:
+                if supported(f, k):
+                    print(f"[max] {name} {B.KERNEL_NAMES[k]}", flush=True)
+                    check_parity(model, X, k, f"{name} {B.KERNEL_NAMES[k]}", forest=f)
+                    ran.append(k)
+            assert B.BRIDGER_KERNEL_DIRECT in ran
+            if name == "perfect depth 10":
+                assert B.BRIDGER_KERNEL_PERFECT in ran
+            if name == "perfect depth 11":
+                assert B.BRIDGER_KERNEL_PERFECT not in ran
