@@ -78,7 +78,8 @@ def parse():
     p.add_argument("--rows", type=int, default=None, help="override the workload's row count")
     p.add_argument("--kernel", default="auto", choices=["auto", "perfect", "ragged", "direct", "gemm"])
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-rows", type=int, default=200_000)
+    # the CPU oracle's sample: the whole default batch, about 20 s of CPU work on 16 threads
+    p.add_argument("--cpu-sample-rows", type=int, default=1_000_000)
     p.add_argument("--binned", action="store_true",
                    help="time prediction on 8/16-bit feature bins (bins made once, untimed; the "
                         "binning pass is timed separately as bin_ms)")
