@@ -39,10 +39,10 @@ HBM_PEAK_BYTES_PER_S = 8.0e12
 # as null.
 KERNEL_SOURCES = ["perfect_fixed.hip", "perfect_walk.h", "kernel_common.h", "internal.h"]
 MEASURED_TRAFFIC = {
-    "kernel_sha256_prefix": "adca62ab0a835ac1",
+    "kernel_sha256_prefix": "9ebbbbd0e2b973e6",
     "workload": "gbdt_d6",
-    "fetch_kib": 57551.34, "write_kib": 3906.25,
-    "copy_bytes": 112_000_000, "copy_fetch_kib": 54702.109375, "copy_write_kib": 109375.0,
+    "fetch_kib": 57571.75, "write_kib": 3906.25,
+    "copy_bytes": 112_000_000, "copy_fetch_kib": 54699.0, "copy_write_kib": 109375.0,
 }
 
 
@@ -185,6 +185,15 @@ def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False
     else:
         ref, _, visits = oracle.predict(w.forest, X, threads=threads)
     dt = time.perf_counter() - t0
+    # the plain single-thread oracle on a tenth of the sample
+    n1 = max(1, n // 10)
+    t1 = time.perf_counter()
+    if np.ndim(w.forest.value) == 2:
+        from oracle import vector as V
+        V.predict(w.forest, X[:n1], threads=1)
+    else:
+        oracle.predict(w.forest, X[:n1], threads=1)
+    dt1 = time.perf_counter() - t1
     got = out_dev[:n].cpu().numpy()
     if labels:
         lab = (ref[:, 0] > 0.5).astype(np.int64) if ref.shape[1] == 1 else ref.argmax(1)
@@ -195,7 +204,9 @@ def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False
     return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
             "sample": f"first {n:,} rows of the {w.n_rows:,}-row workload ({visits:,} node visits), "
                       f"{dt:.2f} s wall on {threads} threads",
-            "visits_per_s": visits / dt, "agrees_with_gpu": ok}
+            "visits_per_s": visits / dt, "agrees_with_gpu": ok,
+            "single_thread": {"value": n1 / dt1, "unit": "rows/s", "cores": 1,
+                              "sample": f"first {n1:,} rows, {dt1:.2f} s wall"}}
 
 
 def main():
@@ -283,6 +294,27 @@ def main():
     t_wall = time.perf_counter() - t_wall
     ms = e0.elapsed_time(e1) / args.steps
 
+    # the same launches timed one by one (median of 20) and as 5 runs of K/5 (mean of the runs'
+    # per-launch times, the paper's mean of five), after the timed region
+    one = []
+    for _ in range(20):
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        step()
+        a1.record(stream)
+        a1.synchronize()
+        one.append(a0.elapsed_time(a1))
+    runs = []
+    per_run = max(1, args.steps // 5)
+    for _ in range(5):
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        for _ in range(per_run):
+            step()
+        a1.record(stream)
+        a1.synchronize()
+        runs.append(a0.elapsed_time(a1) / per_run)
+
     f = w.forest
     n = w.n_rows
     # visits per row: exact for perfect trees; otherwise the depth of the leaf each row
@@ -349,6 +381,8 @@ def main():
                 "peak_GBps": HBM_PEAK_BYTES_PER_S / 1e9,
                 "frac": alg_bytes / s / HBM_PEAK_BYTES_PER_S},
         "wall_s_timed_region": t_wall,
+        "launch_ms_median_of_20": float(np.median(one)),
+        "launch_ms_mean_of_5_runs": float(np.mean(runs)),
     }
     if args.binned:
         line["binning"] = {"bin_bytes": x_elem, "bin_ms": bin_ms,
