@@ -357,81 +357,6 @@ __device__ __forceinline__ void class_flush_all(const LaunchArgs &a, ClassAcc &c
   }
 }
 
-// Vector leaves: each tree adds its leaf's K class values to all K class sums, which live in
-// LDS (slot k * slot_stride) from the start.  vec_add takes the leaves of N consecutive trees
-// (the family's leaf indices into a.leaf_vec, whose rows are padded to whole 16-byte groups)
-// and adds them class by class in tree order: 16-byte loads (one cache line per lane and
-// group of four classes) and one LDS read and write per class for the N trees.
-__device__ __forceinline__ void vec_init(const LaunchArgs &a, double *acc_lds, int slot_stride,
-                                         bool first_group) {
-  for (int k = 0; k < a.K; ++k) acc_lds[k * slot_stride] = class_init(a, k, first_group);
-}
-
-template <int N>
-__device__ __forceinline__ void vec_add(const LaunchArgs &a, double *acc_lds, int slot_stride,
-                                        const int64_t (&leaf)[N]) {
-  const int K = a.K, groups = vec_stride(K) >> 2;
-  const float4 *v[N];
-#pragma unroll
-  for (int u = 0; u < N; ++u)
-    v[u] = reinterpret_cast<const float4 *>(a.leaf_vec) + leaf[u] * groups;
-  for (int k4 = 0; k4 < groups; ++k4) {
-    float4 w[N];
-#pragma unroll
-    for (int u = 0; u < N; ++u) w[u] = v[u][k4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int k = 4 * k4 + c;
-      if (k < K) {
-        double s = acc_lds[k * slot_stride];
-#pragma unroll
-        for (int u = 0; u < N; ++u) s += (double)(c == 0 ? w[u].x : c == 1 ? w[u].y : c == 2 ? w[u].z : w[u].w);
-        acc_lds[k * slot_stride] = s;
-      }
-    }
-  }
-}
-
-// Class sums in registers for K <= kVecRegClasses (vector kernels with VK = kVecRegClasses):
-// every class of the padded row is added, so the padding's zeros land in accumulators past K,
-// which are never stored.  Per class the trees are still added in order.
-constexpr int kVecRegClasses = 8;
-
-__device__ __forceinline__ void vec_init_reg(const LaunchArgs &a, double (&acc)[kVecRegClasses],
-                                             bool first_group) {
-#pragma unroll
-  for (int k = 0; k < kVecRegClasses; ++k) acc[k] = k < a.K ? class_init(a, k, first_group) : 0.0;
-}
-
-template <int N>
-__device__ __forceinline__ void vec_add_reg(const LaunchArgs &a, double (&acc)[kVecRegClasses],
-                                            const int64_t (&leaf)[N]) {
-  const int groups = vec_stride(a.K) >> 2;  // 1 or 2
-#pragma unroll
-  for (int u = 0; u < N; ++u) {
-    const float4 *v = reinterpret_cast<const float4 *>(a.leaf_vec) + leaf[u] * groups;
-    const float4 w0 = v[0];
-    acc[0] += (double)w0.x;
-    acc[1] += (double)w0.y;
-    acc[2] += (double)w0.z;
-    acc[3] += (double)w0.w;
-    if (groups > 1) {
-      const float4 w1 = v[1];
-      acc[4] += (double)w1.x;
-      acc[5] += (double)w1.y;
-      acc[6] += (double)w1.z;
-      acc[7] += (double)w1.w;
-    }
-  }
-}
-
-__device__ __forceinline__ void vec_store_reg(const LaunchArgs &a, const double (&acc)[kVecRegClasses],
-                                              double *acc_lds, int slot_stride) {
-#pragma unroll
-  for (int k = 0; k < kVecRegClasses; ++k)
-    if (k < a.K) acc_lds[k * slot_stride] = acc[k];
-}
-
 // ====================================================================== launchers
 // Raise a kernel's dynamic-LDS limit once per (kernel, device) to the largest size used.
 static inline int ensure_lds_limit(const void *kernel, int lds_bytes) {

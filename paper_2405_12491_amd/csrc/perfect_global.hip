@@ -8,13 +8,16 @@
 // contiguous ranges (no chunks, no staging, no barriers inside the walk), so a CU runs as
 // many waves as the tile and the per-group class sums allow.
 #include "perfect_walk.h"
+#include "vector_leaves.h"
 
 namespace bridger {
 
-// VK: 0 scalar leaves; kVecRegClasses or 64 vector leaves (class sums in registers / LDS).
+// VK: 0 scalar leaves; 4 or 8 (K <= VK) or 64 vector leaves (class sums in registers / LDS).
 template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
+  constexpr int VR = VK_REG ? VK : 4;
   const int tid = threadIdx.x;
   const int R = a.rows_per_wg, G = a.groups;
   const uint32_t tb = (uint32_t)a.tree_bytes;
@@ -37,8 +40,8 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = a.class_begin[1];
-  double vacc[kVecRegClasses];
-  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  double vacc[VR];
+  if (VK_REG) vec_init_reg(a, vacc, g == 0);
   if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   auto finish = [&](auto &m, int q) {
@@ -56,7 +59,7 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
       int64_t leaf[N];
 #pragma unroll
       for (int u = 0; u < N; ++u) leaf[u] = (int64_t)(q + u) * (1 << D) + (m[u] - kFirstLeaf);
-      if (VK == kVecRegClasses) vec_add_reg(a, vacc, leaf);
+      if (VK_REG) vec_add_reg(a, vacc, leaf);
       else vec_add(a, acc_lds, slot_stride, leaf);
     } else {
       float lv[N];
@@ -84,8 +87,11 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
     finish(m, q);
   }
   if (LEAVES) return;
-  if (VK == kVecRegClasses) vec_store_reg(a, vacc, acc_lds, slot_stride);
-  else if (!VK) class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  if (VK_REG) {
+    vec_store_reg(a, vacc, acc_lds, slot_stride);
+  } else if (!VK) {
+    class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
+  }
   __syncthreads();
   if (g == 0) {
     double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
@@ -105,8 +111,10 @@ static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int l
   const int threads = 64 * waves;
   if (a.out_leaf)
     return launch_common(perfect_global_kernel<D, 4, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.vec && a.K <= kVecRegClasses)
-    return launch_common(perfect_global_kernel<D, 4, false, FIN, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 4)
+    return launch_common(perfect_global_kernel<D, 4, false, FIN, XB, 4>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 8)  // two trees per lane: the rows of four would cost occupancy
+    return launch_common(perfect_global_kernel<D, 2, false, FIN, XB, 8>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec)
     return launch_common(perfect_global_kernel<D, 4, false, FIN, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 4)

@@ -1,5 +1,6 @@
 // ragged.hip -- gfx950 kernel for forests of trees of any shape, staged through LDS.
 #include "perfect_walk.h"
+#include "vector_leaves.h"
 
 namespace bridger {
 
@@ -15,10 +16,12 @@ __device__ __forceinline__ bool goes_right(uint32_t x, uint32_t w) {
 // internal record it gathers x[feature], compares and moves to left or left+1; at a leaf it
 // adds the value and jumps to the next tree's root.  Lanes never wait for each other inside
 // a chunk, so a short path in one tree is not padded to the wave's longest path.
-// VK: 0 scalar leaves; kVecRegClasses or 64 vector leaves (class sums in registers / LDS).
+// VK: 0 scalar leaves; 4 or 8 (K <= VK) or 64 vector leaves (class sums in registers / LDS).
 template <bool LEAVES, bool SIMPLE, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
+  constexpr int VR = VK_REG ? VK : 4;
   const int tid = threadIdx.x;
   const int R = a.rows_per_wg, G = a.groups;
   if (tid >= G * R) {
@@ -46,8 +49,8 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
-  double vacc[kVecRegClasses];
-  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  double vacc[VR];
+  if (VK_REG) vec_init_reg(a, vacc, g == 0);
   if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   for (int c = 0; c < a.n_chunks; ++c) {
@@ -74,7 +77,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
                 a.leaf_map[rec0 + (int)((addr - buf) >> 3)];
         } else if (VK) {
           const int64_t leaf[1] = {rec0 + (int)((addr - buf) >> 3)};
-          if (VK == kVecRegClasses) vec_add_reg(a, vacc, leaf);
+          if (VK_REG) vec_add_reg(a, vacc, leaf);
           else vec_add(a, acc_lds, slot_stride, leaf);
         } else {
           if (!SIMPLE) class_advance(a, ca, t, acc_lds, slot_stride, g == 0);
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
   }
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
-  } else if (VK == kVecRegClasses) {
+  } else if (VK_REG) {
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
@@ -127,6 +130,8 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
 template <bool LEAVES, bool SIMPLE, int U, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
+  constexpr int VR = VK_REG ? VK : 4;
   const int tid = threadIdx.x;
   const int R = a.rows_per_wg, G = a.groups;
   const int r = tid & (R - 1);
@@ -146,8 +151,8 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   ca.k = 0;
   ca.acc = class_init(a, 0, g == 0);
   ca.next_b = SIMPLE ? 0x7fffffff : a.class_begin[1];
-  double vacc[kVecRegClasses];
-  if (VK == kVecRegClasses) vec_init_reg(a, vacc, g == 0);
+  double vacc[VR];
+  if (VK_REG) vec_init_reg(a, vacc, g == 0);
   if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
 
   const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
@@ -186,7 +191,7 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
         }
       }
     }
-    if (VK == kVecRegClasses) {
+    if (VK_REG) {
       vec_add_reg(a, vacc, idx);
       return;
     }
@@ -210,7 +215,7 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   if (LEAVES) return;
   if (SIMPLE) {
     acc_lds[0] = ca.acc;
-  } else if (VK == kVecRegClasses) {
+  } else if (VK_REG) {
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
@@ -234,8 +239,10 @@ static int launch_ragged_global_xu(const LaunchArgs &a, int waves, int64_t n_wg,
   const int threads = 64 * waves;
   if (a.out_leaf)
     return launch_common(ragged_global_kernel<true, false, U, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.vec && a.K <= kVecRegClasses)
-    return launch_common(ragged_global_kernel<false, false, 4, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 4)
+    return launch_common(ragged_global_kernel<false, false, 4, XB, 4>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 8)
+    return launch_common(ragged_global_kernel<false, false, 4, XB, 8>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec)
     return launch_common(ragged_global_kernel<false, false, 4, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (a.K != 1)
@@ -265,8 +272,10 @@ static int launch_ragged_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds
   const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(ragged_kernel<true, false, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.vec && a.K <= kVecRegClasses)
-    return launch_common(ragged_kernel<false, false, XB, kVecRegClasses>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 4)
+    return launch_common(ragged_kernel<false, false, XB, 4>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 8)
+    return launch_common(ragged_kernel<false, false, XB, 8>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec)
     return launch_common(ragged_kernel<false, false, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (simple)
