@@ -139,7 +139,9 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
  *           read only
  *   out     device pointer, row-major float [n_rows, n_classes]; must not overlap X
  *   stream  a hipStream_t (NULL = the null stream); the call is asynchronous on it
- * n_features must equal the value given at create; n_rows == 0 launches nothing.
+ * n_features must equal the value given at create; n_rows == 0 launches nothing;
+ * n_rows up to 2^37 (more than 2^24 rows go out as several launches on the same
+ * stream, each over at most 2^24 rows).
  * Must be called with the handle's device current.  Launch failures return
  * BRIDGER_ERR_DEVICE; faults during execution surface at the caller's sync.
  */

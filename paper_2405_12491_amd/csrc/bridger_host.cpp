@@ -853,34 +853,12 @@ struct CsrRows {
   const int32_t *indices = nullptr;
 };
 
-bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int32_t n_features,
-                          float *out, int32_t *out_leaf, void *stream, bool binned,
-                          int32_t *out_label = nullptr, const CsrRows *csr = nullptr) {
-  g_last_error.clear();
-  if (csr && h && !(h->kernel_active == kPerfect || h->kernel_active == kRagged))
-    return fail(BRIDGER_ERR_UNSUPPORTED, "CSR rows run on the perfect and ragged kernels only");
-  if (csr && n_rows > 0 && (!csr->indptr || !csr->indices))
-    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null CSR array");
-  if (out_label && h && h->K == 1 && h->transform != BRIDGER_XFORM_SIGMOID)
-    return fail(BRIDGER_ERR_UNSUPPORTED,
-                "labels need several classes or a sigmoid output (a classifier)");
-  if (binned && h && !h->bin_bytes)
-    return fail(BRIDGER_ERR_UNSUPPORTED, "a feature has 65536 or more distinct thresholds");
-  const int xsz = binned && h ? h->bin_bytes : 4;
-  void *dst = out ? (void *)out : (out_leaf ? (void *)out_leaf : (void *)out_label);
-  bridger_status s = check_predict(h, X, n_rows, n_features, dst, xsz);
-  if (s != BRIDGER_OK || n_rows == 0) return s;
-  if (binned && !((h->kernel_active == kPerfect && h->perfect_bok) ||
-                  (h->kernel_active == kRagged && h->ragged_bok)))
-    return fail(BRIDGER_ERR_UNSUPPORTED,
-                "binned prediction runs on the perfect and ragged kernels only");
-  const uint8_t *xb = (const uint8_t *)X;
-  const uint8_t *ob = (const uint8_t *)dst;
-  const size_t xbytes = (size_t)n_rows * h->F * xsz;
-  const size_t obytes = (size_t)n_rows * (out ? h->K : (out_leaf ? h->n_trees : 1)) * 4;
-  if (!csr && xb < ob + obytes && ob < xb + xbytes)
-    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
-
+// One launch (plus the Normalizer's row-norm pass) over n_rows rows; do_predict splits larger
+// batches.
+bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, float *out,
+                           int32_t *out_leaf, int32_t *out_label, const CsrRows *csr,
+                           void *stream, bool binned, int xsz) {
+  bridger_status s = BRIDGER_OK;
   LaunchArgs a{};
   a.X = (const float *)X;
   a.n_rows = n_rows;
@@ -971,6 +949,51 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   if (err != 0)
     return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
                                         hipGetErrorString((hipError_t)err));
+  return BRIDGER_OK;
+}
+
+bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int32_t n_features,
+                          float *out, int32_t *out_leaf, void *stream, bool binned,
+                          int32_t *out_label = nullptr, const CsrRows *csr = nullptr) {
+  g_last_error.clear();
+  if (csr && h && !(h->kernel_active == kPerfect || h->kernel_active == kRagged))
+    return fail(BRIDGER_ERR_UNSUPPORTED, "CSR rows run on the perfect and ragged kernels only");
+  if (csr && n_rows > 0 && (!csr->indptr || !csr->indices))
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null CSR array");
+  if (out_label && h && h->K == 1 && h->transform != BRIDGER_XFORM_SIGMOID)
+    return fail(BRIDGER_ERR_UNSUPPORTED,
+                "labels need several classes or a sigmoid output (a classifier)");
+  if (binned && h && !h->bin_bytes)
+    return fail(BRIDGER_ERR_UNSUPPORTED, "a feature has 65536 or more distinct thresholds");
+  const int xsz = binned && h ? h->bin_bytes : 4;
+  void *dst = out ? (void *)out : (out_leaf ? (void *)out_leaf : (void *)out_label);
+  bridger_status s = check_predict(h, X, n_rows, n_features, dst, xsz);
+  if (s != BRIDGER_OK || n_rows == 0) return s;
+  if (binned && !((h->kernel_active == kPerfect && h->perfect_bok) ||
+                  (h->kernel_active == kRagged && h->ragged_bok)))
+    return fail(BRIDGER_ERR_UNSUPPORTED,
+                "binned prediction runs on the perfect and ragged kernels only");
+  const uint8_t *xb = (const uint8_t *)X;
+  const uint8_t *ob = (const uint8_t *)dst;
+  const size_t xbytes = (size_t)n_rows * h->F * xsz;
+  const size_t obytes = (size_t)n_rows * (out ? h->K : (out_leaf ? h->n_trees : 1)) * 4;
+  if (!csr && xb < ob + obytes && ob < xb + xbytes)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
+
+  // A dispatch counts its work-items in 32 bits: larger batches go out as several launches of
+  // at most kMaxRowsPerLaunch rows each (tile boundaries are unaffected: every tile size divides
+  // it).  CSR rows keep absolute entry offsets, so only indptr moves.
+  for (int64_t r0 = 0; r0 < n_rows; r0 += kMaxRowsPerLaunch) {
+    const int64_t nr = std::min<int64_t>(kMaxRowsPerLaunch, n_rows - r0);
+    CsrRows part;
+    if (csr) part = {csr->indptr + r0, csr->indices};
+    const void *xr = csr ? X : (const void *)((const uint8_t *)X + r0 * (int64_t)h->F * xsz);
+    s = launch_rows(h, xr, nr, out ? out + r0 * h->K : nullptr,
+                    out_leaf ? out_leaf + r0 * h->n_trees : nullptr,
+                    out_label ? out_label + r0 : nullptr, csr ? &part : nullptr, stream, binned,
+                    xsz);
+    if (s != BRIDGER_OK) return s;
+  }
   return BRIDGER_OK;
 }
 
@@ -1256,22 +1279,25 @@ bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_
   const size_t xbytes = (size_t)n_rows * h->F * 4, qbytes = (size_t)n_rows * h->F * h->bin_bytes;
   if (xb < qb + qbytes && qb < xb + xbytes)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "Xq overlaps X");
-  LaunchArgs a{};
-  a.X = X;
-  a.n_rows = n_rows;
-  a.F = h->F;
-  a.x_bytes = h->bin_bytes;
-  a.q_values = (const float *)h->d_q_values;
-  a.q_off = (const int32_t *)h->d_q_off;
-  a.xq = Xq;
-  a.x_vec4 = ((uintptr_t)X % 16 == 0) && (h->F % 4 == 0);
-  set_preprocess_args(h, a);
-  RowNorms norms;
-  if ((s = prepare_row_norms(h, a, stream, norms)) != BRIDGER_OK) return s;
-  const int err = launch_bin(a, stream);
-  if (err != 0)
-    return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
-                                        hipGetErrorString((hipError_t)err));
+  for (int64_t r0 = 0; r0 < n_rows; r0 += kMaxRowsPerLaunch) {  // bounded dispatches
+    const int64_t nr = std::min<int64_t>(kMaxRowsPerLaunch, n_rows - r0);
+    LaunchArgs a{};
+    a.X = X + r0 * (int64_t)h->F;
+    a.n_rows = nr;
+    a.F = h->F;
+    a.x_bytes = h->bin_bytes;
+    a.q_values = (const float *)h->d_q_values;
+    a.q_off = (const int32_t *)h->d_q_off;
+    a.xq = (uint8_t *)Xq + r0 * (int64_t)h->F * h->bin_bytes;
+    a.x_vec4 = ((uintptr_t)a.X % 16 == 0) && (h->F % 4 == 0);
+    set_preprocess_args(h, a);
+    RowNorms norms;
+    if ((s = prepare_row_norms(h, a, stream, norms)) != BRIDGER_OK) return s;
+    const int err = launch_bin(a, stream);
+    if (err != 0)
+      return fail(BRIDGER_ERR_DEVICE, std::string("kernel launch failed: ") +
+                                          hipGetErrorString((hipError_t)err));
+  }
   return BRIDGER_OK;
 }
 

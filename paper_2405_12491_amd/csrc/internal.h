@@ -37,6 +37,9 @@ constexpr int kLdsBytesPerCU = 163840;
 constexpr int kLeafFlag = 0x8000;
 constexpr int kMaxRel = 0x7FFF;
 constexpr int kMaxRaggedFeatures = 0xFFFF;
+// Rows per dispatch: every launch shape then stays far below the 32-bit work-item count of a
+// dispatch; predictions over more rows are issued as several launches.
+constexpr int64_t kMaxRowsPerLaunch = int64_t(1) << 24;
 constexpr int kMaxClasses = 64;  // class sums of one 256-row block fit LDS in every kernel
 
 enum Kernel { kAuto = 0, kPerfect = 1, kRagged = 2, kDirect = 3, kGemm = 4 };

@@ -454,3 +454,41 @@ def test_maximum_sizes():
                 assert B.BRIDGER_KERNEL_PERFECT in ran
             if name == "perfect depth 11":
                 assert B.BRIDGER_KERNEL_PERFECT not in ran
+
+
+def test_rows_beyond_one_launch():
+    """More rows than one dispatch takes (2^24): the rows go out as several launches, so the
+    rows on both sides of each launch boundary, CSR rows (whose entry offsets stay absolute),
+    the Normalizer's per-launch norms and the binning pass must all line up."""
+    import torch
+    from oracle import binning
+    from oracle import preprocess as P
+    rng = np.random.default_rng(24)
+    n = (1 << 24) + 4099
+    X = rng.standard_normal((n, 2)).astype(np.float32)
+    trees = [perfect_tree_arrays(2, rng.integers(0, 2, 3), rng.standard_normal(3).astype(np.float32) * 0.5,
+                                 rng.standard_normal(4).astype(np.float32)) for _ in range(3)]
+    model = concat_trees(trees, 2)
+    ref, ref_lv = oracle_predict(model, X, leaves=True)
+    Xd = to_dev(X)
+    with B.Forest(model) as f:
+        for k in (B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT):
+            f.kernel = k
+            what = f"{n} rows {B.KERNEL_NAMES[k]}"
+            print(f"[big] {what}", flush=True)
+            assert_scores(gpu_predict(f, Xd), ref, what)
+            assert_leaves(gpu_predict(f, Xd, leaves=True), ref_lv, what)
+        f.kernel = B.BRIDGER_KERNEL_PERFECT
+        ip = torch.arange(0, 2 * n + 1, 2, dtype=torch.int64, device="cuda")
+        ix = torch.tensor([0, 1], dtype=torch.int32, device="cuda").repeat(n)
+        out = f.predict_csr(ip, ix, Xd.view(-1), n)
+        torch.cuda.synchronize()
+        assert_scores(out.cpu().numpy(), ref, "csr rows")
+        del ip, ix, out
+        q = f.bin(Xd)
+        torch.cuda.synchronize()
+        got = q.cpu().numpy().view(np.uint8 if f.bin_info()["bin_bytes"] == 1 else np.uint16)
+        assert np.array_equal(got.astype(np.int64), binning.bin_rows(binning.tables(model), X)), "bins"
+        f.set_preprocess(B.BRIDGER_PRE_NORMALIZE)
+        refn, _ = oracle_predict(model, P.apply(P.NORMALIZE, None, None, X))
+        assert_scores(gpu_predict(f, Xd), refn, "normalized rows")
