@@ -625,12 +625,15 @@ Plan pick_plan(const PlanInput &pin) {
     const int u = env_int("BRIDGER_ILP", 4);
     g.ilp = (u == 1 || u == 2) ? u : 4;
   }
+  // Ragged trees: the global-node kernel, whose lanes walk their trees in lockstep with no
+  // barrier inside the walk, measured as fast or faster than the LDS-chunked state machine on
+  // every ragged forest tried (up to 1.9x on depth 10-12 trees, where a chunk holds few trees
+  // and every chunk's barrier waits for its deepest path); a forest larger than L2 would
+  // moreover be restaged from memory for every row tile.
+  if (!pin.perfect) return g;
   const bool few = p.waves == 0 || p.waves_per_cu < kMinWavesPerCU;
-  const bool fits = !pin.perfect || pin.forest_bytes <= kL2BytesPerXcd;
+  const bool fits = pin.forest_bytes <= kL2BytesPerXcd;
   if (gmode == 1 || (few && fits && g.waves_per_cu > p.waves_per_cu)) return g;
-  // a ragged forest larger than L2 is restaged from memory for every row tile; the walk
-  // touches only the few nodes on each row's path
-  if (!pin.perfect && pin.forest_bytes > kL2BytesPerXcd) return g;
   return p;
 }
 

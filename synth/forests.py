@@ -306,9 +306,15 @@ CONFIGS = {
         description="1000 ragged trees (split prob 0.85, max depth 12), 4M x 256 N(0,1) rows; sum"),
 }
 
-# Extra shallow-forest workloads used only to compare the matrix-multiply lowering with the
-# traversal kernels (not part of the five benchmark configurations).
+# Extra workloads (not part of the five benchmark configurations): shallow forests to compare
+# the matrix-multiply lowering with the traversal kernels, and a forest of ragged trees on
+# narrow rows (the shape of a random-forest classifier's trees; with class-vector leaves via
+# synth.with_vector_leaves) for the LDS-chunked ragged kernel.
 EXTRA_CONFIGS = {
+    "ragged_rf_28": dict(
+        seed=13, n_rows=1_000_000, n_features=28, x="normal", shape="ragged", p_split=0.85,
+        max_depth=12, n_trees=100, thr="column", leaf_sigma=1.0, agg=AGG_MEAN, xform=XFORM_IDENTITY,
+        description="100 ragged trees (split prob 0.85, max depth 12), 1M x 28 N(0,1) rows; mean"),
     "shallow_d3": dict(
         seed=11, n_rows=1_000_000, n_features=28, x="normal", shape="perfect", depth=3, n_trees=100,
         thr="column", leaf_sigma=0.1, agg=AGG_SUM, xform=XFORM_SIGMOID, base=0.0,

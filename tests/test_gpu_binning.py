@@ -15,7 +15,8 @@ pytestmark = pytest.mark.gpu
 
 SMALL_ROWS = {"dt_d3": 10_000, "rf_d8": 3 * 1024 + 77, "gbdt_d6": 3 * 1024 + 77,
               "mc_gbdt_d8": 2 * 32 * 3 + 45, "ragged_d12": 3 * 64 + 29,
-              "shallow_d3": 2 * 1024 + 5, "shallow_d4": 2 * 1024 + 5}
+              "shallow_d3": 2 * 1024 + 5, "shallow_d4": 2 * 1024 + 5,
+              "ragged_rf_28": 2 * 512 + 37}
 
 
 @pytest.fixture(scope="module", autouse=True)

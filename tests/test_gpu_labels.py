@@ -23,9 +23,13 @@ def _cuda():
     yield
 
 
-@pytest.mark.parametrize("case", ["mc_gbdt_d8", "gbdt_d6", "shallow_d3", "ragged_mean3"])
-def test_labels(case):
+@pytest.mark.parametrize("case", ["mc_gbdt_d8", "gbdt_d6", "shallow_d3", "ragged_mean3",
+                                  "ragged_mean3_chunked"])
+def test_labels(case, monkeypatch):
     import torch
+    if case.endswith("_chunked"):   # ragged trees through LDS chunks instead of global records
+        monkeypatch.setenv("BRIDGER_GLOBAL", "0")
+        case = case[:-len("_chunked")]
     rng = np.random.default_rng(4)
     if case == "ragged_mean3":
         model = random_tiny_forest(rng, 30, 6, max_depth=8, n_classes=3, aggregate=AGG_MEAN,

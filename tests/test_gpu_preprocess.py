@@ -40,9 +40,13 @@ def _params(kind, X, rng):
 
 @pytest.mark.parametrize("kind", [P.MINMAX, P.CENTER_SCALE, P.BINARIZE, P.NORMALIZE])
 @pytest.mark.parametrize("name,n", [("gbdt_d6", 1500), ("rf_d8", 700), ("ragged_d12", 150),
-                                    ("mc_gbdt_d8", 150), ("shallow_d3", 1100)])
-def test_fused_preprocessing(kind, name, n):
+                                    ("mc_gbdt_d8", 150), ("shallow_d3", 1100), ("ragged_rf_28", 700),
+                                    ("ragged_rf_28_chunked", 700)])
+def test_fused_preprocessing(kind, name, n, monkeypatch):
     import torch
+    if name.endswith("_chunked"):   # ragged trees through LDS chunks instead of global records
+        monkeypatch.setenv("BRIDGER_GLOBAL", "0")
+        name = name[:-len("_chunked")]
     rng = np.random.default_rng(kind * 10 + n)
     w = make_workload(name, n)
     X = w.X()

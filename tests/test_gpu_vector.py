@@ -38,9 +38,13 @@ def _case(name, rng):
     return with_vector_leaves(w.forest, K, rng), w.X()
 
 
-@pytest.mark.parametrize("name", ["rf_d8", "mc_gbdt_d8", "ragged_d12", "gbdt_d6", "tiny_ragged"])
-def test_vector_forest(name):
+@pytest.mark.parametrize("name", ["rf_d8", "mc_gbdt_d8", "ragged_d12", "gbdt_d6", "tiny_ragged",
+                                  "tiny_ragged_chunked"])
+def test_vector_forest(name, monkeypatch):
     import torch
+    if name.endswith("_chunked"):   # ragged trees through LDS chunks instead of global records
+        monkeypatch.setenv("BRIDGER_GLOBAL", "0")
+        name = name[:-len("_chunked")]
     rng = np.random.default_rng(len(name))
     model, X = _case(name, rng)
     ref, ref_lv = V.predict(model, X, threads=8)

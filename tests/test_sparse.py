@@ -57,11 +57,15 @@ def test_densify_matches_scipy():
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("case", ["mc_gbdt_d8", "gbdt_d6", "ragged_d12", "tiny_ragged"])
-def test_csr_prediction(case):
+@pytest.mark.parametrize("case", ["mc_gbdt_d8", "gbdt_d6", "ragged_d12", "tiny_ragged",
+                                  "tiny_ragged_chunked"])
+def test_csr_prediction(case, monkeypatch):
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
+    if case.endswith("_chunked"):   # ragged trees through LDS chunks instead of global records
+        monkeypatch.setenv("BRIDGER_GLOBAL", "0")
+        case = case[:-len("_chunked")]
     rng = np.random.default_rng({"mc_gbdt_d8": 1, "gbdt_d6": 2, "ragged_d12": 3, "tiny_ragged": 4}[case])
     if case == "tiny_ragged":
         model = random_tiny_forest(rng, 25, 9, max_depth=8)
