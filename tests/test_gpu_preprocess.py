@@ -121,3 +121,30 @@ def test_normalize_at_ties(name, n):
             bb = f.bin_info()["bin_bytes"]
             got = q.cpu().numpy().view(np.uint8 if bb == 1 else np.uint16).astype(np.int64)
             assert np.array_equal(got, binning.bin_rows(binning.tables(model), Xp)), name + " bins"
+
+
+def test_normalize_concurrent_streams():
+    """The Normalizer's row norms live in stream-ordered scratch taken per call: predictions in
+    flight on two streams at once (and many calls in a row) each get their own norms."""
+    import torch
+    rng = np.random.default_rng(5)
+    w = make_workload("gbdt_d6", 20_000)
+    X1 = w.X()
+    X2 = (rng.standard_normal(X1.shape) * 3).astype(np.float32)
+    ref1, _ = oracle_predict(w.forest, P.apply(P.NORMALIZE, None, None, X1))
+    ref2, _ = oracle_predict(w.forest, P.apply(P.NORMALIZE, None, None, X2))
+    d1, d2 = to_dev(X1), to_dev(X2)
+    with B.Forest(w.forest) as f:
+        f.set_preprocess(B.BRIDGER_PRE_NORMALIZE)
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        outs1, outs2 = [], []
+        for _ in range(8):
+            with torch.cuda.stream(s1):
+                outs1.append(f.predict(d1))
+            with torch.cuda.stream(s2):
+                outs2.append(f.predict(d2))
+        torch.cuda.synchronize()
+        for o in outs1:
+            assert_scores(o.cpu().numpy(), ref1, "stream 1")
+        for o in outs2:
+            assert_scores(o.cpu().numpy(), ref2, "stream 2")
