@@ -12,7 +12,9 @@
 
 namespace bridger {
 
-constexpr int kBinThreads = 256;
+// 16 waves per workgroup: each lane's binary search is a chain of dependent LDS reads, so the
+// pass needs many waves in flight per CU (two 64 KB workgroups fit a CU).
+constexpr int kBinThreads = 1024;
 
 __device__ __forceinline__ int lower_bound_f32(const float *t, int n, float x) {
   int lo = 0, len = n;
@@ -51,10 +53,12 @@ __global__ __launch_bounds__(kBinThreads) void bin_kernel(LaunchArgs a) {
       for (int i = tid; i < n; i += kBinThreads) reinterpret_cast<float *>(smem)[i] = a.q_values[base + i];
       __syncthreads();
     }
-    const int64_t total = (r1 - r0) * nf;
-    for (int64_t i = tid; i < total; i += kBinThreads) {
-      const int64_t row = r0 + i / nf;
-      const int ff = f + (int)(i % nf);
+    // a block's rows x the run's features stays below 2^31 (launch_bin): 32-bit indices
+    const uint32_t total = (uint32_t)(r1 - r0) * (uint32_t)nf;
+    for (uint32_t i = tid; i < total; i += kBinThreads) {
+      const uint32_t rq = i / (uint32_t)nf;
+      const int64_t row = r0 + rq;
+      const int ff = f + (int)(i - rq * (uint32_t)nf);
       const int64_t e = row * F + ff;
       const float x = a.pre_kind ? preprocess(a, ff, row, a.X[e]) : a.X[e];
       const int o = a.q_off[ff] - base, cnt = a.q_off[ff + 1] - a.q_off[ff];
@@ -73,6 +77,9 @@ int launch_bin(const LaunchArgs &a0, void *stream) {
   // about four row blocks per CU; each block restages the tables once
   int64_t rows = (a.n_rows + 1023) / 1024;
   rows = rows < 64 ? 64 : (rows > 16384 ? 16384 : rows);
+  // the kernel indexes a run's (row, feature) pairs with 32 bits
+  const int64_t cap = INT32_MAX / (a.F > 0 ? a.F : 1);
+  rows = rows > cap ? (cap > 0 ? cap : 1) : rows;
   a.rows_per_wg = (int32_t)rows;
   a.chunk_bytes = 64 * 1024;
   const int64_t blocks = (a.n_rows + rows - 1) / rows;
