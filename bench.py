@@ -366,6 +366,8 @@ def main():
             "labels": bool(args.labels),
             "vector_leaves": args.vector or None,
             "plan": {k: v for k, v in plan.items() if not isinstance(v, float)},
+            "plan_of": "binned rows use their own plan; this is the fp32 rows' plan"
+                       if args.binned else "fp32 rows",
         },
         "roofline": {
             "bound": "lds",
