@@ -255,7 +255,8 @@ static int launch_ragged_global_x(const LaunchArgs &a, int waves, int64_t n_wg, 
                                   void *stream) {
   if (a.ilp == 1) return launch_ragged_global_xu<XB, 1>(a, waves, n_wg, lds_bytes, stream);
   if (a.ilp == 2) return launch_ragged_global_xu<XB, 2>(a, waves, n_wg, lds_bytes, stream);
-  return launch_ragged_global_xu<XB, 4>(a, waves, n_wg, lds_bytes, stream);
+  if (a.ilp == 4) return launch_ragged_global_xu<XB, 4>(a, waves, n_wg, lds_bytes, stream);
+  return launch_ragged_global_xu<XB, 8>(a, waves, n_wg, lds_bytes, stream);
 }
 
 int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

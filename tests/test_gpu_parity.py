@@ -276,7 +276,7 @@ def _variant_models():
 
 
 @pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1"}, {"BRIDGER_GLOBAL": "1", "BRIDGER_ILP": "2"},
-                                 {"BRIDGER_GLOBAL": "0"}],
+                                 {"BRIDGER_GLOBAL": "1", "BRIDGER_ILP": "4"}, {"BRIDGER_GLOBAL": "0"}],
                          ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
 def test_ragged_kernel_variants(env, monkeypatch):
     """The ragged kernel with records in LDS chunks and read from global memory (one or two
