@@ -35,23 +35,32 @@ HBM_PEAK_BYTES_PER_S = 8.0e12
 # HBM bytes per launch of the default workload's kernel from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE runs (KiB per dispatch), each scaled by what the same counter reads for a plain
 # copy of known size (profiles/perfect_fixed_kernel_gbdt_d6_1Mx28_500trees.md).  Valid only for
-# the kernel sources they were measured on (KERNEL_SOURCES); any other source reports traffic
-# as null.
+# the kernel sources they were measured on (KERNEL_SOURCES, compared without their comments
+# and whitespace); any other source reports traffic as null.
 KERNEL_SOURCES = ["perfect_fixed.hip", "perfect_walk.h", "kernel_common.h", "internal.h"]
 MEASURED_TRAFFIC = {
-    "kernel_sha256_prefix": "c0e854e8e64762be",
+    "kernel_sha256_prefix": "3cfcb52c2b2e993f",
     "workload": "gbdt_d6",
     "fetch_kib": 57553.875, "write_kib": 3906.25,
     "copy_bytes": 112_000_000, "copy_fetch_kib": 54699.0, "copy_write_kib": 109375.0,
 }
 
 
+def strip_comments(src: str) -> str:
+    """C/C++ source without comments and with whitespace collapsed (the kernel sources hold no
+    string literal containing a comment marker)."""
+    import re
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def kernel_sources_sha() -> str:
     import hashlib
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2405_12491_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2405_12491_amd", "csrc", name), encoding="utf-8") as f:
+            h.update(strip_comments(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -67,7 +67,8 @@ struct Plan {
   int32_t n_chunks;
   int32_t lds_bytes;       // dynamic LDS per workgroup
   int32_t acc_in_lds;      // class/group partial sums kept in LDS
-  int32_t ilp;             // PERFECT: trees walked at once per lane (1, 2 or 4)
+  int32_t ilp;             // trees walked at once per lane: chunked PERFECT 1, 2 or 4; global
+                           // PERFECT 4 or 8; global RAGGED 1, 2, 4 or 8
   int32_t global_nodes;    // records read from global memory, LDS holds only the tile
   int32_t waves_per_cu;    // resident compute waves per CU
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
@@ -106,7 +107,7 @@ struct LaunchArgs {
   int32_t lds_x_off;           // byte offset of the feature tile in dynamic LDS
   int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
   int32_t acc_in_lds;
-  int32_t ilp;                 // PERFECT: trees walked at once per lane (1, 2 or 4)
+  int32_t ilp;                 // trees walked at once per lane (the plan's ilp)
   int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)
   const uint32_t *roots;       // PERFECT: per kernel tree the root's traversal record (2 words)
   int32_t x_bytes;             // element of X and of the LDS tile: 4 (fp32) or 2 / 1 (bins)
