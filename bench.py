@@ -31,6 +31,7 @@ N_CU, CLOCK_HZ, LDS_LANES_PER_CLK = 256, 2.4e9, 32
 GATHERS_PER_VISIT = 2
 PEAK_VISITS_PER_S = N_CU * CLOCK_HZ * LDS_LANES_PER_CLK / GATHERS_PER_VISIT
 HBM_PEAK_BYTES_PER_S = 8.0e12
+MFMA_F32_PEAK_FLOP_S = 157.3e12   # MI355X dense fp32 matrix peak (the GEMM lowering's bound)
 
 # HBM bytes per launch of the default workload's kernel from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE runs (KiB per dispatch), each scaled by what the same counter reads for a plain
@@ -400,6 +401,17 @@ def main():
         "launch_ms_median_of_20": float(np.median(one)),
         "launch_ms_mean_of_5_runs": float(np.mean(runs)),
     }
+    if forest.kernel == B.BRIDGER_KERNEL_GEMM:
+        # the matrix lowering is bound by its fp32 one-hot product: 2F flops per (row, internal
+        # node), algorithmic (the kernel also multiplies the unused heap slot and pads F to 4)
+        depth = info["max_depth"]
+        flops = 2.0 * w.n_features * n * f.n_trees * ((1 << depth) - 1)
+        line["roofline"] = {
+            "bound": "mfma", "achieved": flops / s / 1e12, "peak": MFMA_F32_PEAK_FLOP_S / 1e12,
+            "unit": "TFLOP/s", "frac": flops / s / MFMA_F32_PEAK_FLOP_S, "traffic": None,
+            "what": "the one-hot product S = X . A on v_mfma_f32_16x16x4f32 (2F flops per row and "
+                    "internal node) against the dense fp32 matrix peak; the int8 path match adds "
+                    "<1% of that work at 32x the rate"}
     if args.binned:
         line["binning"] = {"bin_bytes": x_elem, "bin_ms": bin_ms,
                            "note": "bins made once before the timed region; bin_ms is one "
