@@ -1,0 +1,111 @@
+"""Randomized differential parity: seeded random forests of many shapes (ragged and perfect,
+1-9 features, 1-4 classes, sum/mean, identity/sigmoid/softmax, thresholds on a coarse grid so
+ties are common, NaN and infinite inputs, scalar and vector leaves) on every kernel family that
+takes them, against the oracles: scores, leaf ids and labels; binned and CSR rows too."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import paper_2405_12491_amd as B
+from oracle import sparse as S
+from oracle import vector as V
+from parity_util import assert_leaves, assert_scores, check_labels, oracle_predict, to_dev
+from synth import (AGG_MEAN, AGG_SUM, XFORM_IDENTITY, XFORM_SIGMOID, XFORM_SOFTMAX, concat_trees,
+                   perfect_tree_arrays, random_tiny_forest, with_vector_leaves)
+
+pytestmark = pytest.mark.gpu
+
+KERNELS = [B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED, B.BRIDGER_KERNEL_DIRECT,
+           B.BRIDGER_KERNEL_GEMM]
+GRID = np.array([-1.5, -0.5, -0.0, 0.0, 0.25, 0.5, 1.0, 2.0], np.float32)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+    yield
+
+
+def _random_case(seed):
+    rng = np.random.default_rng(1000 + seed)
+    F = int(rng.integers(1, 10))
+    K = int(rng.integers(1, 5))
+    agg = AGG_MEAN if rng.random() < 0.4 else AGG_SUM
+    if K == 1:
+        xform = XFORM_SIGMOID if rng.random() < 0.5 else XFORM_IDENTITY
+    else:
+        xform = XFORM_SOFTMAX if rng.random() < 0.5 else XFORM_IDENTITY
+    T = int(rng.integers(K, 3 * K + 20))
+    if rng.random() < 0.4:   # perfect trees of one depth
+        D = int(rng.integers(1, 7))
+        trees = [perfect_tree_arrays(D, rng.integers(0, F, (1 << D) - 1),
+                                     GRID[rng.integers(0, len(GRID), (1 << D) - 1)],
+                                     rng.standard_normal(1 << D).astype(np.float32)) for _ in range(T)]
+        tc = rng.integers(0, K, T)
+        tc[:K] = np.arange(K)
+        model = concat_trees(trees, F, K, tc if K > 1 else None, agg, xform,
+                             rng.standard_normal(K).astype(np.float32))
+    else:
+        model = random_tiny_forest(rng, T, F, max_depth=int(rng.integers(1, 11)),
+                                   p_split=float(rng.uniform(0.5, 0.9)), thr_grid=GRID,
+                                   n_classes=K, aggregate=agg, transform=xform)
+        if agg == AGG_MEAN and K > 1:   # every class needs a tree: class of tree t is t mod K
+            assert T >= K
+    vector = K > 1 and xform != XFORM_SIGMOID and rng.random() < 0.3
+    if vector:
+        model = with_vector_leaves(model, K, rng, aggregate=agg, transform=xform)
+    n = int(rng.integers(1, 1500))
+    X = GRID[rng.integers(0, len(GRID), (n, F))] + (rng.random((n, F)) < 0.3) * rng.standard_normal((n, F))
+    X = X.astype(np.float32)
+    X[rng.random((n, F)) < 0.02] = np.nan
+    X[rng.random((n, F)) < 0.01] = np.inf
+    X[rng.random((n, F)) < 0.01] = -np.inf
+    return model, X, vector
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_forests(seed):
+    import torch
+    model, X, vector = _random_case(seed)
+    if vector:
+        ref, ref_lv = V.predict(model, X)
+    else:
+        ref, ref_lv = oracle_predict(model, X, leaves=True)
+    Xd = to_dev(X)
+    K = model.n_classes
+    classifier = K > 1 or model.transform == XFORM_SIGMOID
+    with B.Forest(model) as f:
+        ran = 0
+        for k in KERNELS:
+            try:
+                f.kernel = k
+            except B.BridgerError as e:
+                assert e.status == B.BRIDGER_ERR_UNSUPPORTED
+                continue
+            what = f"seed {seed} {B.KERNEL_NAMES[k]}"
+            out = f.predict(Xd)
+            lv = f.predict_leaves(Xd)
+            lab = f.predict_labels(Xd) if classifier else None
+            torch.cuda.synchronize()
+            assert_scores(out.cpu().numpy(), ref, what + " scores")
+            assert_leaves(lv.cpu().numpy(), ref_lv, what + " leaves")
+            if classifier:
+                check_labels(lab.cpu().numpy(), ref, what + " labels")
+            ran += 1
+        assert ran >= 1
+        f.kernel = B.BRIDGER_KERNEL_AUTO
+        if f.kernel in (B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED):
+            if f.bin_info()["bin_bytes"]:
+                out = f.predict_binned(f.bin(Xd))
+                torch.cuda.synchronize()
+                assert_scores(out.cpu().numpy(), ref, f"seed {seed} binned")
+            nz = np.nonzero(np.where(np.isnan(X), 1.0, X))
+            ip = np.concatenate([[0], np.cumsum(np.bincount(nz[0], minlength=X.shape[0]))]).astype(np.int64)
+            d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+            out = f.predict_csr(d(ip), d(nz[1].astype(np.int32)), d(X[nz].astype(np.float32)), X.shape[0])
+            torch.cuda.synchronize()
+            assert_scores(out.cpu().numpy(), ref, f"seed {seed} csr")
