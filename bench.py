@@ -104,6 +104,9 @@ def parse():
     p.add_argument("--vector", type=int, default=0, metavar="K",
                    help="the workload's trees with a K-class probability vector in every leaf "
                         "(a forest classifier: averaged class vectors)")
+    p.add_argument("--graph", type=int, default=0, metavar="N",
+                   help="capture N predictions in a HIP graph and time its replays (a step is "
+                        "then one replay; times are reported per prediction)")
     p.add_argument("--calib-copy", action="store_true",
                    help="time a plain device copy of X instead (counter calibration)")
     return p.parse_args()
@@ -293,6 +296,18 @@ def main():
         step = lambda: forest.predict_binned(Xq, out)
     else:
         step = lambda: forest.predict(Xd, out)
+    per_step = 1
+    if args.graph:
+        # N predictions captured once on the launch stream, replayed as one step (launch-bound
+        # small batches); the eager first call does the kernels' one-time set-up
+        step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=torch.cuda.Stream(dev)):   # capture off the null stream
+            for _ in range(args.graph):
+                step()
+        step = graph.replay   # replays on the current (timed) stream
+        per_step = args.graph
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -306,7 +321,7 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = e0.elapsed_time(e1) / args.steps / per_step
 
     # the same launches timed one by one (median of 20) and as 5 runs of K/5 (mean of the runs'
     # per-launch times, the paper's mean of five), after the timed region
@@ -317,7 +332,7 @@ def main():
         step()
         a1.record(stream)
         a1.synchronize()
-        one.append(a0.elapsed_time(a1))
+        one.append(a0.elapsed_time(a1) / per_step)
     runs = []
     per_run = max(1, args.steps // 5)
     for _ in range(5):
@@ -327,7 +342,7 @@ def main():
             step()
         a1.record(stream)
         a1.synchronize()
-        runs.append(a0.elapsed_time(a1) / per_run)
+        runs.append(a0.elapsed_time(a1) / per_run / per_step)
 
     f = w.forest
     n = w.n_rows
@@ -375,6 +390,7 @@ def main():
             "csr": bool(args.csr),
             "labels": bool(args.labels),
             "vector_leaves": args.vector or None,
+            "graph": args.graph or None,
             "plan": {k: v for k, v in plan.items() if not isinstance(v, float)},
             "plan_of": "binned rows use their own plan; this is the fp32 rows' plan"
                        if args.binned else "fp32 rows",

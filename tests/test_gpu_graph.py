@@ -1,0 +1,67 @@
+"""Predictions captured in a HIP graph (torch.cuda.CUDAGraph on the launch stream): the graph is
+replayed several times, with the program's own eager work (new rows written into the captured
+input buffer) and synchronizations between replays, and every replay is checked against the
+eager prediction on the same rows."""
+import numpy as np
+import pytest
+
+import paper_2405_12491_amd as B
+from parity_util import assert_leaves, assert_scores, oracle_predict
+from synth import make_workload, random_tiny_forest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+    yield
+
+
+def _cases():
+    rng = np.random.default_rng(8)
+    out = []
+    for name, n in (("gbdt_d6", 3000), ("dt_d3", 10_000), ("mc_gbdt_d8", 200), ("rf_d8", 1500)):
+        w = make_workload(name, n)
+        out.append((name, w.forest, [w.X(n)] + [x.astype(np.float32) for x in
+                                                 (rng.standard_normal((n, w.n_features)),) * 1]))
+    m = random_tiny_forest(rng, 30, 7, max_depth=9)
+    out.append(("tiny_ragged", m, [rng.standard_normal((2000, 7)).astype(np.float32) for _ in range(2)]))
+    return out
+
+
+@pytest.mark.parametrize("case", range(5))
+def test_predict_in_graph(case):
+    import torch
+    name, model, Xs = _cases()[case]
+    n, F = Xs[0].shape
+    Xd = torch.from_numpy(Xs[0]).cuda()
+    out = torch.empty((n, model.n_classes), dtype=torch.float32, device="cuda")
+    leaves = torch.empty((n, model.n_trees), dtype=torch.int32, device="cuda")
+    with B.Forest(model) as f:
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            f.predict(Xd, out)           # eager first call: the kernels' one-time set-up
+            f.predict_leaves(Xd, leaves)
+        s.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            f.predict(Xd, out)
+            f.predict_leaves(Xd, leaves)
+        for rep in range(4):
+            X = Xs[rep % len(Xs)] if rep < 2 else (Xs[0] * np.float32(0.5 + rep)).astype(np.float32)
+            Xd.copy_(torch.from_numpy(X))        # eager work between replays
+            torch.cuda.synchronize()
+            out.zero_()
+            leaves.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            ref, ref_lv = oracle_predict(model, X, leaves=True)
+            assert_scores(out.cpu().numpy(), ref, f"{name} replay {rep}")
+            assert_leaves(leaves.cpu().numpy(), ref_lv, f"{name} replay {rep} leaves")
+            eager = f.predict(Xd)
+            torch.cuda.synchronize()
+            assert np.array_equal(eager.cpu().numpy().view(np.uint32), out.cpu().numpy().view(np.uint32))
