@@ -65,3 +65,33 @@ def test_predict_in_graph(case):
             eager = f.predict(Xd)
             torch.cuda.synchronize()
             assert np.array_equal(eager.cpu().numpy().view(np.uint32), out.cpu().numpy().view(np.uint32))
+
+
+def test_normalizer_in_graph():
+    """The Normalizer's row-norm scratch is stream-ordered (hipMallocAsync / hipFreeAsync on the
+    launch stream), which a graph records as allocation nodes: replays must still match."""
+    import torch
+    from oracle import preprocess as P
+    rng = np.random.default_rng(12)
+    w = make_workload("gbdt_d6", 3000)
+    X0 = w.X(3000)
+    Xd = torch.from_numpy(X0).cuda()
+    out = torch.empty((3000, 1), dtype=torch.float32, device="cuda")
+    with B.Forest(w.forest) as f:
+        f.set_preprocess(B.BRIDGER_PRE_NORMALIZE)
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            f.predict(Xd, out)
+        s.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            f.predict(Xd, out)
+        for rep in range(4):
+            X = (rng.standard_normal(X0.shape) * (rep + 1)).astype(np.float32)
+            Xd.copy_(torch.from_numpy(X))
+            torch.cuda.synchronize()
+            out.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            ref, _ = oracle_predict(w.forest, P.apply(P.NORMALIZE, None, None, X))
+            assert_scores(out.cpu().numpy(), ref, f"normalized replay {rep}")
