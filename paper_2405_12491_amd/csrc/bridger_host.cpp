@@ -109,6 +109,7 @@ struct bridger_forest {
   Plan perfect_bplan{}, ragged_bplan{};
   bool perfect_bok = false, ragged_bok = false;
   std::vector<uint8_t> perfect_btrav;   // PERFECT traversal copy for bins: {rank, f * R * bytes}
+  std::vector<uint32_t> perfect_broots;  // per tree: the binned copy's root record
   std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
   std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
 
@@ -133,7 +134,7 @@ struct bridger_forest {
   void *d_class_begin = nullptr, *d_class_count = nullptr, *d_base = nullptr,
        *d_tree_order = nullptr;
   DevArrays d_perfect, d_ragged, d_direct;
-  void *d_perfect_trav = nullptr, *d_perfect_roots = nullptr;
+  void *d_perfect_trav = nullptr, *d_perfect_roots = nullptr, *d_perfect_broots = nullptr;
   void *d_q_values = nullptr, *d_q_off = nullptr, *d_perfect_btrav = nullptr,
        *d_ragged_brec = nullptr, *d_ragged_bchunk_first = nullptr,
        *d_ragged_bchunk_rec = nullptr;
@@ -542,10 +543,15 @@ Plan choose_plan(const PlanInput &in) {
     if (c.p.est_seconds > 1.02 * t_min) continue;
     if (!pick) { pick = &c; continue; }
     // a CU issues from its four SIMDs: below two compute waves per SIMD, more waves come
-    // before a single lane group
-    auto key = [](const Cand &x) {
+    // before a single lane group.  Bins: at equal resident waves, 4-wave workgroups before
+    // 8-wave ones (measured on the depth-6, 500-tree, 28-feature forest with 16-bit bins: 8
+    // waves x 3 workgroups 0.46 ms, 4 waves x 6 workgroups 0.42 ms; fp32 tiles show no
+    // difference, 0.423 against 0.424 ms, and keep the fewer chunks)
+    const bool bins = in.x_bytes < 4;
+    auto key = [bins](const Cand &x) {
       return std::make_tuple(std::min(x.waves_cu, kMinWavesPerCU), x.single, x.p.ilp,
-                             x.waves_cu, x.overlap, -x.p.n_chunks);
+                             x.waves_cu, bins ? -std::max(x.p.waves, 4) : 0, x.overlap,
+                             -x.p.n_chunks);
     };
     if (key(c) > key(*pick)) pick = &c;
   }
@@ -684,6 +690,9 @@ void build_perfect_btrav(bridger_forest *h) {
       std::memcpy(blk + 8 * m + 4, &off, 4);
     }
   }
+  h->perfect_broots.assign((size_t)2 * h->n_trees, 0);
+  for (int32_t k = 0; k < h->n_trees; ++k)
+    std::memcpy(&h->perfect_broots[2 * (size_t)k], h->perfect_btrav.data() + (size_t)k * tb + 8, 8);
 }
 
 // RAGGED records for bins: an internal record's threshold becomes its rank.
@@ -727,6 +736,7 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_tree_order);
   free_dev(h->d_perfect_trav);
   free_dev(h->d_perfect_roots);
+  free_dev(h->d_perfect_broots);
   for (void **q : {&h->d_q_values, &h->d_q_off, &h->d_perfect_btrav, &h->d_ragged_brec,
                    &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b,
                    &h->d_vec_perfect, &h->d_vec_ragged, &h->d_vec_direct})
@@ -763,8 +773,10 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_q_values, h->q_values)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_q_off, h->q_off)) != BRIDGER_OK) return s;
   }
-  if (h->perfect_bok)
+  if (h->perfect_bok) {
     if ((s = upload(&h->d_perfect_btrav, h->perfect_btrav, 1024)) != BRIDGER_OK) return s;
+    if ((s = upload(&h->d_perfect_broots, h->perfect_broots)) != BRIDGER_OK) return s;
+  }
   if (h->ragged_bok) {
     if ((s = upload(&h->d_ragged_brec, h->ragged_brec, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_ragged_bchunk_first, h->ragged_bchunk_first)) != BRIDGER_OK) return s;
@@ -900,7 +912,7 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
     else
       a.nodes = (const uint8_t *)(binned ? h->d_ragged_brec : d.nodes);
     a.finite_thresholds = h->finite_thresholds ? 1 : 0;
-    a.roots = (const uint32_t *)h->d_perfect_roots;
+    a.roots = (const uint32_t *)(binned ? h->d_perfect_broots : h->d_perfect_roots);
     a.tree_start = (const int32_t *)d.tree_start;
     a.chunk_first = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_first : d.chunk_first);
     a.chunk_rec = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_rec : d.chunk_rec);
@@ -919,8 +931,10 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
     a.acc_in_lds = p.acc_in_lds;
     a.ilp = p.ilp;
     const int64_t n_wg = (n_rows + p.rows_per_wg - 1) / p.rows_per_wg;
-    const bool fixed = h->kernel_active == kPerfect && !binned && !out_leaf && h->K == 1 &&
-                       p.groups == 1 && p.waves <= 8 && h->finite_thresholds && p.ilp == 4 &&
+    // (bins compare exactly whatever the thresholds; fp32 needs them finite)
+    const bool fixed = h->kernel_active == kPerfect && !out_leaf && h->K == 1 && !h->vec &&
+                       p.groups == 1 && p.waves <= 8 && (binned || h->finite_thresholds) &&
+                       p.ilp == 4 &&
                        perfect_fixed_ok(h->perfect_depth, p.trees_per_chunk) &&
                        p.chunk_bytes == p.trees_per_chunk * h->perfect_tree_bytes &&
                        h->fixed_chunks;

@@ -4,11 +4,11 @@
 namespace bridger {
 
 // Compile-time chunk geometry for the common case (one class, one lane group, finite
-// thresholds): CT trees per chunk and the tree block size are constants and the chunk loop is
-// unrolled over the two buffers, so every tree's LDS base folds into the gathers' offset field
-// and a level's node address is a single shift.  A last chunk with fewer than CT trees is
-// walked with run-time bases.
-template <int D, int CT>
+// thresholds or bins): CT trees per chunk and the tree block size are constants and the chunk
+// loop is unrolled over the two buffers, so every tree's LDS base folds into the gathers'
+// offset field and a level's node address is a single shift.  A last chunk with fewer than CT
+// trees is walked with run-time bases.  XB: fp32 rows (4) or rows of 16- / 8-bit bins.
+template <int D, int CT, int XB = 4>
 __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr int U = 4;
@@ -30,8 +30,8 @@ __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
 
   const int64_t row = (int64_t)blockIdx.x * R + tid;
   const bool row_ok = row < a.n_rows;
-  const uint32_t lane_off = (uint32_t)a.lds_x_off + 4u * (uint32_t)tid;
-  load_tile_any<4, true>(smem, a, tid, row, row_ok, 0, 1);
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + tile_row_off<XB>(tid);
+  load_tile_any<XB, true>(smem, a, tid, row, row_ok, 0, 1);
   __syncthreads();
 
   double acc = a.aggregate == 0 ? (double)a.base[0] : 0.0;
@@ -51,7 +51,7 @@ __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
 #pragma unroll
       for (int j = 0; j < CT / U; ++j) {
         uint32_t m[U];
-        walk_trees_root<D, U>(smem, BUF + (uint32_t)(j * U) * TB, TB, lane_off, root + j * U, m);
+        walk_trees_root<D, U, XB>(smem, BUF + (uint32_t)(j * U) * TB, TB, lane_off, root + j * U, m);
         float lv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -64,7 +64,7 @@ __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
       for (; q + U <= T; q += U) {
         const uint32_t b0 = BUF + (uint32_t)(q - t0) * TB;
         uint32_t m[U];
-        walk_trees<D, U, true>(smem, b0, TB, lane_off, m);
+        walk_trees<D, U, true, XB>(smem, b0, TB, lane_off, m);
         float lv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) lv[u] = lds_f32(smem, (m[u] << 2) + b0 + (uint32_t)u * TB + kLeafOff);
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
       for (; q < T; ++q) {
         const uint32_t b0 = BUF + (uint32_t)(q - t0) * TB;
         uint32_t m[1];
-        walk_trees<D, 1, true>(smem, b0, TB, lane_off, m);
+        walk_trees<D, 1, true, XB>(smem, b0, TB, lane_off, m);
         acc += (double)lds_f32(smem, (m[0] << 2) + b0 + kLeafOff);
       }
     }
@@ -97,10 +97,16 @@ __global__ __launch_bounds__(1024) void perfect_fixed_kernel(LaunchArgs a) {
 template <int D, int CT>
 static int launch_fixed_dc(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                            void *stream) {
-  if constexpr (perfect_fixed_ok(D, CT))
-    return launch_common(perfect_fixed_kernel<D, CT>, 64 * (waves + 1), n_wg, lds_bytes, stream, a);
-  else
+  if constexpr (perfect_fixed_ok(D, CT)) {
+    const int threads = 64 * (waves + 1);
+    if (a.x_bytes == 2)
+      return launch_common(perfect_fixed_kernel<D, CT, 2>, threads, n_wg, lds_bytes, stream, a);
+    if (a.x_bytes == 1)
+      return launch_common(perfect_fixed_kernel<D, CT, 1>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_fixed_kernel<D, CT, 4>, threads, n_wg, lds_bytes, stream, a);
+  } else {
     return (int)hipErrorInvalidValue;
+  }
 }
 
 template <int D>

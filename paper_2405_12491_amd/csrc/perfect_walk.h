@@ -58,34 +58,28 @@ __device__ __forceinline__ void walk_trees(const uint8_t *smem, uint32_t b0, uin
 }
 
 // Same walk with the root records given as wave-uniform values (scalar registers): level 0
-// then needs only the feature gather.
-template <int D, int U>
+// then needs only the feature gather.  Finite thresholds (fp32) or bins (XB = 2, 1).
+template <int D, int U, int XB = 4>
 __device__ __forceinline__ void walk_trees_root(const uint8_t *smem, uint32_t b0, uint32_t tb,
                                                 uint32_t lane_off, const uint2 *root,
                                                 uint32_t (&m)[U]) {
   {
-    float xv[U];
+    uint32_t xv[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, root[u].y + lane_off);
+    for (int u = 0; u < U; ++u) xv[u] = gather_x<true, XB>(smem, root[u].y + lane_off);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float diff = __uint_as_float(root[u].x) - xv[u];
-      m[u] = __builtin_amdgcn_alignbit(1u, __float_as_uint(diff), 31);
-    }
+    for (int u = 0; u < U; ++u) m[u] = step_slot<true, XB>(1u, root[u].x, xv[u]);
   }
 #pragma unroll
   for (int d = 1; d < D; ++d) {
     uint2 rec[U];
-    float xv[U];
+    uint32_t xv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) rec[u] = lds_u64(smem, (m[u] << 3) + b0 + (uint32_t)u * tb);
 #pragma unroll
-    for (int u = 0; u < U; ++u) xv[u] = lds_f32(smem, rec[u].y + lane_off);
+    for (int u = 0; u < U; ++u) xv[u] = gather_x<true, XB>(smem, rec[u].y + lane_off);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float diff = __uint_as_float(rec[u].x) - xv[u];
-      m[u] = __builtin_amdgcn_alignbit(m[u], __float_as_uint(diff), 31);
-    }
+    for (int u = 0; u < U; ++u) m[u] = step_slot<true, XB>(m[u], rec[u].x, xv[u]);
   }
 }
 
