@@ -301,6 +301,63 @@ def test_ragged_kernel_variants(env, monkeypatch):
             check_parity(model, X, B.BRIDGER_KERNEL_RAGGED, f"{name} {env}", forest=f)
 
 
+def _class_layouts(T, rng):
+    """Class assignments that stress the global kernels' class slots (a lane group's tree
+    range is contiguous in class order): empty classes, one-tree classes next to classes
+    spread over several groups, and classes given in shuffled tree order."""
+    K1 = 7
+    tc1 = np.array([0] * 20 + [1] + [3] * 2 + [4] * 30 + [6] * (T - 53))  # 2 and 5 empty
+    K2 = 12
+    tc2 = np.arange(T) % K2                                                # interleaved
+    K3 = 3
+    tc3 = np.r_[np.zeros(T - 2, int), [1, 2]]                              # one huge class
+    return [(K1, rng.permutation(tc1)), (K2, tc2), (K3, tc3)]
+
+
+@pytest.mark.parametrize("family", ["perfect", "ragged"])
+@pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "16", "BRIDGER_ROWS": "64"},
+                                 {"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "8", "BRIDGER_ROWS": "32"}],
+                         ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
+def test_global_class_slots(family, env, monkeypatch):
+    """Global-node kernels with 16 lane groups on several classes: each group sums the classes
+    its contiguous tree range touches, the groups' partials are added in group order; SUM
+    (with empty classes: base score only) and MEAN (every class non-empty), softmax and
+    identity."""
+    import dataclasses
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    rng = np.random.default_rng(2024)
+    T, F = 64, 9
+    X = rng.standard_normal((3 * 64 + 29, F)).astype(np.float32)
+    if family == "perfect":
+        trees = [perfect_tree_arrays(5, rng.integers(0, F, 31), rng.standard_normal(31).astype(np.float32),
+                                     rng.standard_normal(32).astype(np.float32)) for _ in range(T)]
+        base_model = concat_trees(trees, F)
+        kernel = B.BRIDGER_KERNEL_PERFECT
+    else:
+        base_model = random_tiny_forest(rng, T, F, max_depth=9)
+        kernel = B.BRIDGER_KERNEL_RAGGED
+    for K, tc in _class_layouts(T, rng):
+        empty = len(np.unique(tc)) < K
+        for agg, xform in ((AGG_SUM, XFORM_SOFTMAX), (AGG_MEAN, XFORM_IDENTITY)):
+            if agg == AGG_MEAN and empty:
+                continue  # MEAN over an empty class is rejected at create
+            model = dataclasses.replace(base_model, n_classes=K, tree_class=np.asarray(tc, np.int32),
+                                        aggregate=agg, transform=xform,
+                                        base_score=rng.standard_normal(K).astype(np.float32))
+            with B.Forest(model) as f:
+                if not supported(f, kernel):
+                    continue
+                p = f.plan(X.shape[0])
+                print(f"[slots] {family} {env} K={K} agg={agg} plan={p}", flush=True)
+                R = int(env["BRIDGER_ROWS"])
+                G = 64 * int(env["BRIDGER_WAVES"]) // R
+                # the global-node plan: the row tile and G x K class slots per row
+                assert p["rows_per_wg"] == R and p["chunk_bytes"] == 0
+                assert p["lds_bytes"] == F * R * 4 + G * K * R * 8
+                check_parity(model, X, kernel, f"{family} K={K} agg={agg} {env}", forest=f)
+
+
 @pytest.mark.parametrize("env", VARIANT_ENVS, ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
 def test_perfect_kernel_variants(env, monkeypatch):
     for k, v in env.items():
