@@ -225,7 +225,7 @@ def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}); "
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); "
               "the forest is replicated and rows are independent, so N GPUs would each run this "
               "same kernel on n/N rows. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
