@@ -74,14 +74,19 @@ __global__ __launch_bounds__(kBinThreads) void bin_kernel(LaunchArgs a) {
 
 int launch_bin(const LaunchArgs &a0, void *stream) {
   LaunchArgs a = a0;
-  // about four row blocks per CU; each block restages the tables once
-  int64_t rows = (a.n_rows + 1023) / 1024;
-  rows = rows < 64 ? 64 : (rows > 16384 ? 16384 : rows);
+  // About one row block per resident workgroup (two per CU), at most 2,048 rows: each block
+  // restages the tables once per run of features, and a run's rows x features are read with
+  // one cache line per row, so longer blocks re-read lines that L2 no longer holds (measured:
+  // 1M x 28 rows 0.146 -> 0.144 ms, 100k x 784 0.541 -> 0.50 ms, 4M x 256 13.0 -> 10.0 ms
+  // against the previous n / 1024 rows per block).
+  int64_t rows = (a.n_rows + 511) / 512;
+  rows = rows < 64 ? 64 : (rows > 2048 ? 2048 : rows);
+  if (a0.rows_per_wg > 0) rows = a0.rows_per_wg;
   // the kernel indexes a run's (row, feature) pairs with 32 bits
   const int64_t cap = INT32_MAX / (a.F > 0 ? a.F : 1);
   rows = rows > cap ? (cap > 0 ? cap : 1) : rows;
   a.rows_per_wg = (int32_t)rows;
-  a.chunk_bytes = 64 * 1024;
+  if (a.chunk_bytes <= 0) a.chunk_bytes = 64 * 1024;
   const int64_t blocks = (a.n_rows + rows - 1) / rows;
   if (a.x_bytes == 2) return launch_common(bin_kernel<2>, kBinThreads, blocks, a.chunk_bytes, stream, a);
   if (a.x_bytes == 1) return launch_common(bin_kernel<1>, kBinThreads, blocks, a.chunk_bytes, stream, a);

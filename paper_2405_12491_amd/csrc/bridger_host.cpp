@@ -1307,6 +1307,11 @@ bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_
     a.q_off = (const int32_t *)h->d_q_off;
     a.xq = (uint8_t *)Xq + r0 * (int64_t)h->F * h->bin_bytes;
     a.x_vec4 = ((uintptr_t)a.X % 16 == 0) && (h->F % 4 == 0);
+    a.rows_per_wg = env_int("BRIDGER_BIN_ROWS", 0);  // tuning override of the row block
+    {  // tuning override of the LDS table buffer
+      const int kb = env_int("BRIDGER_BIN_LDS_KB", 0);
+      if (kb > 0) a.chunk_bytes = (int32_t)std::min<int64_t>((int64_t)kb * 1024, kLdsBytesPerCU);
+    }
     set_preprocess_args(h, a);
     RowNorms norms;
     if ((s = prepare_row_norms(h, a, stream, norms)) != BRIDGER_OK) return s;
