@@ -223,12 +223,20 @@ bridger_status validate_tree(int32_t t, int64_t n, const int32_t *feat, const fl
 }
 
 // -------------------------------------------------------------------- packing
+// Vector leaves of at most 4 classes are read by the chunked PERFECT kernel from LDS: their
+// class rows sit in the tree blocks in place of the scalar leaves (measured 4-8% faster for
+// K = 2..4; with 8-float rows the larger blocks pushed the plan to one workgroup per CU and
+// the 8-class GBDT forest ran 6% slower, so 5..8 classes keep their rows in global memory).
+bool perfect_vec_rows(const bridger_forest *h) { return h->vec && h->K <= 4; }
+
 void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *feat,
                   const float *thr, const int32_t *left, const int32_t *right,
                   const float *value) {
   const int n_int = (1 << D) - 1, n_leaf = 1 << D;
   const int leaf_off = 8 * (n_int + 1);   // 1-based heap: slots 1 .. 2^D - 1, slot 0 unused
-  const int tb = perfect_tree_bytes(D);
+  // vector leaves (K <= 4): the leaf block holds class rows, filled by build_vector_leaves
+  const bool rows = perfect_vec_rows(h);
+  const int tb = rows ? (8 + 4 * vec_stride(h->K)) << D : perfect_tree_bytes(D);
   h->perfect_tree_bytes = tb;
   h->perfect_blob.assign((size_t)tb * h->n_trees, 0);
   h->perfect_leaf_map.assign((size_t)n_leaf * h->n_trees, -1);
@@ -254,7 +262,7 @@ void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *
     for (int j = 0; j < n_leaf; ++j) {
       const int32_t nd = heap_to_node[n_leaf + j];
       const float v = value[a + nd];
-      std::memcpy(blk + leaf_off + 4 * j, &v, 4);
+      if (!rows) std::memcpy(blk + leaf_off + 4 * j, &v, 4);
       h->perfect_leaf_map[(size_t)k * n_leaf + j] = nd;
     }
   }
@@ -385,6 +393,15 @@ void build_vector_leaves(bridger_forest *h, const int64_t *offs, const int32_t *
     for (int32_t k = 0; k < h->n_trees; ++k)
       for (size_t j = 0; j < n_leaf; ++j)
         put(h->vec_perfect, k * n_leaf + j, h->tree_order[k], h->perfect_leaf_map[k * n_leaf + j]);
+    if (perfect_vec_rows(h)) {  // the rows also go into every copy of the tree blocks
+      const size_t tb = (size_t)h->perfect_tree_bytes, row = 4 * (size_t)KS;
+      for (std::vector<uint8_t> *blob : {&h->perfect_blob, &h->perfect_trav, &h->perfect_btrav}) {
+        if (blob->empty()) continue;
+        for (int32_t k = 0; k < h->n_trees; ++k)
+          std::memcpy(blob->data() + k * tb + 8 * n_leaf, &h->vec_perfect[k * n_leaf * KS],
+                      n_leaf * row);
+      }
+    }
   }
   if (!h->ragged_rec.empty()) {
     h->vec_ragged.assign(h->ragged_rec.size() * KS, 0.0f);

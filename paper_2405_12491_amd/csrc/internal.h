@@ -12,6 +12,9 @@
 //                             last-level slot m form an 8-byte pair 4*2^D bytes past that
 //                             slot's record
 //   Every level's records and the leaf block start 16-byte aligned.
+//   Vector leaves with K <= 4 classes: the leaf block holds the leaves' class rows instead,
+//   4 floats each (leaf j at 8 * 2^D + 16 j), so the tree chunks bring them to LDS with the
+//   records; tree_bytes = 24 * 2^D.
 //   The PERFECT kernel reads a traversal copy of this layout in which each record holds
 //   {threshold with -0 stored as +0; byte offset feature * 4R of the feature's row in the
 //   LDS tile of R rows}; the copy is rebuilt whenever the launch plan (and so R) is chosen.

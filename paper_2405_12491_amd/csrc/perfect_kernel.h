@@ -7,8 +7,9 @@
 
 namespace bridger {
 
-// VK: 0 scalar leaves; 4 or 8 vector leaves (K <= VK) with the class sums in registers; 64
-// vector leaves with the class sums in LDS.
+// VK: 0 scalar leaves; 4 or 8 vector leaves (K <= VK) with the class sums in registers (for
+// VK = 4 the leaf rows come with the staged tree blocks, for VK = 8 from global memory); 64
+// vector leaves with the class sums in LDS and the rows from global memory.
 template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -62,6 +63,13 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
               a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
         }
       }
+    } else if (VK == 4) {
+      // the leaf rows (4 floats) follow the records in the staged tree blocks
+      uint32_t addr[N];
+#pragma unroll
+      for (int u = 0; u < N; ++u)
+        addr[u] = b0 + (uint32_t)u * tb + (8u << D) + (m[u] - kFirstLeaf) * (4u * VK);
+      vec_add_lds(vacc, addr);
     } else if (VK) {
       int64_t leaf[N];
 #pragma unroll

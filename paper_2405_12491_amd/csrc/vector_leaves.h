@@ -68,6 +68,24 @@ __device__ __forceinline__ void vec_add_reg(const LaunchArgs &a, double (&acc)[V
   }
 }
 
+// The same with the leaf rows in LDS (the chunked PERFECT kernel stages them with the tree
+// blocks): addr[u] is the byte address of tree u's leaf row, VK floats, 16-byte aligned.
+template <int N, int VK>
+__device__ __forceinline__ void vec_add_lds(double (&acc)[VK], const uint32_t (&addr)[N]) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+#pragma unroll
+    for (int g = 0; g < VK / 4; ++g) {
+      const f4 w = *(const __attribute__((address_space(3))) f4 *)(uintptr_t)(addr[u] + 16u * g);
+      acc[4 * g + 0] += (double)w.x;
+      acc[4 * g + 1] += (double)w.y;
+      acc[4 * g + 2] += (double)w.z;
+      acc[4 * g + 3] += (double)w.w;
+    }
+  }
+}
+
 template <int VK>
 __device__ __forceinline__ void vec_store_reg(const LaunchArgs &a, const double (&acc)[VK],
                                               double *acc_lds, int slot_stride) {
