@@ -7,13 +7,13 @@
 
 namespace bridger {
 
-// VK: 0 scalar leaves; 4 or 8 vector leaves (K <= VK) with the class sums in registers (for
-// VK = 4 the leaf rows come with the staged tree blocks, for VK = 8 from global memory); 64
-// vector leaves with the class sums in LDS and the rows from global memory.
+// VK: 0 scalar leaves; 2, 4 or 8 vector leaves (K <= VK) with the class sums in registers (for
+// VK = 2 and 4 the leaf rows come with the staged tree blocks, for VK = 8 from global memory);
+// 64 vector leaves with the class sums in LDS and the rows from global memory.
 template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, int VK = 0>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
+  constexpr bool VK_REG = VK == 2 || VK == 4 || VK == 8;  // vector leaves, sums in registers
   constexpr int VR = VK_REG ? VK : 4;
   const int tid = threadIdx.x;
   const int R = a.rows_per_wg, G = a.groups;
@@ -63,12 +63,12 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
               a.leaf_map[(int64_t)t * (1 << D) + (m[u] - kFirstLeaf)];
         }
       }
-    } else if (VK == 4) {
-      // the leaf rows (4 floats) follow the records in the staged tree blocks
+    } else if (VK == 2 || VK == 4) {
+      // the leaf rows (16 bytes) follow the records in the staged tree blocks
       uint32_t addr[N];
 #pragma unroll
       for (int u = 0; u < N; ++u)
-        addr[u] = b0 + (uint32_t)u * tb + (8u << D) + (m[u] - kFirstLeaf) * (4u * VK);
+        addr[u] = b0 + (uint32_t)u * tb + (8u << D) + (m[u] - kFirstLeaf) * 16u;
       vec_add_lds(vacc, addr);
     } else if (VK) {
       int64_t leaf[N];
@@ -145,7 +145,9 @@ static int launch_perfect_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int 
   const int threads = 64 * (waves + 1);  // + the staging wave
   if (a.out_leaf)
     return launch_common(perfect_kernel<D, 4, true, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
-  if (a.vec && a.K <= 4)  // vector leaves: K >= 2, so never the simple variant
+  if (a.vec && a.K == 2)  // vector leaves: K >= 2, so never the simple variant
+    return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, 2>, threads, n_wg, lds_bytes, stream, a);
+  if (a.vec && a.K <= 4)
     return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, 4>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec && a.K <= 8)  // two trees per lane: the rows of four would cost occupancy
     return launch_common(perfect_kernel<D, 2, false, false, FIN, XB, 8>, threads, n_wg, lds_bytes, stream, a);

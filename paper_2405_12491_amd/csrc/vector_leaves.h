@@ -39,7 +39,7 @@ __device__ __forceinline__ void vec_add(const LaunchArgs &a, double *acc_lds, in
   }
 }
 
-// Class sums in registers for K <= VK (vector kernels with VK = 4 or 8, one or two 16-byte
+// Class sums in registers for K <= VK (vector kernels with VK = 2, 4 or 8, one or two 16-byte
 // groups per leaf row): every class of the padded row is added, so the padding's zeros land
 // in accumulators past K, which are never stored.  Per class the trees are added in order.
 // (Deferring each group's adds until after the next group's walk, to hide the L2 round trip,
@@ -73,8 +73,15 @@ __device__ __forceinline__ void vec_add_reg(const LaunchArgs &a, double (&acc)[V
 template <int N, int VK>
 __device__ __forceinline__ void vec_add_lds(double (&acc)[VK], const uint32_t (&addr)[N]) {
   typedef float f4 __attribute__((ext_vector_type(4)));
+  typedef float f2 __attribute__((ext_vector_type(2)));
 #pragma unroll
   for (int u = 0; u < N; ++u) {
+    if constexpr (VK == 2) {  // two classes: the first half of the 16-byte row
+      const f2 w = *(const __attribute__((address_space(3))) f2 *)(uintptr_t)addr[u];
+      acc[0] += (double)w.x;
+      acc[1] += (double)w.y;
+      continue;
+    }
 #pragma unroll
     for (int g = 0; g < VK / 4; ++g) {
       const f4 w = *(const __attribute__((address_space(3))) f4 *)(uintptr_t)(addr[u] + 16u * g);

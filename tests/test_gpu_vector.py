@@ -32,14 +32,15 @@ def _case(name, rng):
         X = rng.standard_normal((1300, 9)).astype(np.float32)
         X[5, 3] = np.nan
         return with_vector_leaves(base, 4, rng), X
+    # K = 2 and 3: class rows staged with the tree blocks; 5 and 10: rows read from L2
     K, n = {"rf_d8": (5, 1200), "mc_gbdt_d8": (10, 200), "ragged_d12": (3, 200),
-            "gbdt_d6": (2, 1500)}[name]
-    w = make_workload(name, n)
+            "gbdt_d6": (2, 1500), "rf_d8_k3": (3, 1100)}[name]
+    w = make_workload(name.split("_k")[0], n)
     return with_vector_leaves(w.forest, K, rng), w.X()
 
 
-@pytest.mark.parametrize("name", ["rf_d8", "mc_gbdt_d8", "ragged_d12", "gbdt_d6", "tiny_ragged",
-                                  "tiny_ragged_chunked"])
+@pytest.mark.parametrize("name", ["rf_d8", "rf_d8_k3", "mc_gbdt_d8", "ragged_d12", "gbdt_d6",
+                                  "tiny_ragged", "tiny_ragged_chunked"])
 def test_vector_forest(name, monkeypatch):
     import torch
     if name.endswith("_chunked"):   # ragged trees through LDS chunks instead of global records
