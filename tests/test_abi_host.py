@@ -104,6 +104,39 @@ def test_vector_leaf_forest_on_host():
         B.load_library().bridger_forest_destroy(h)
 
 
+def test_vector_leaf_rows_in_perfect_blocks():
+    """Vector leaves of at most 4 classes: each perfect tree block holds its leaves' class rows
+    (16 bytes, zero-padded) in place of the scalar values, 24 * 2^D bytes per tree, so that the
+    tree chunks bring them to LDS; more classes keep the 12 * 2^D block."""
+    rng = np.random.default_rng(5)
+    D, T, n_leaf = 3, 3, 8
+    trees = [perfect_tree_arrays(D, rng.integers(0, 4, 7), rng.standard_normal(7).astype(np.float32),
+                                 rng.standard_normal(8).astype(np.float32)) for _ in range(T)]
+    base = concat_trees(trees, 4)
+    for K in (2, 3, 4, 5):
+        v = rng.standard_normal((base.value.size, K)).astype(np.float32)
+        h = B.bridger_forest_create(base.n_trees, base.tree_offsets, base.feature, base.threshold,
+                                    base.left, base.right, v, 4, K, None, AGG_MEAN, 0, None,
+                                    B.BRIDGER_CREATE_HOST_ONLY)
+        try:
+            blob = B.bridger_forest_packed(h, 0, np.uint8)
+            leaf_map = B.bridger_forest_packed(h, 2, np.int32)
+            order = B.bridger_forest_packed(h, 3, np.int32)
+            tb = blob.size // T
+            if K > 4:
+                assert tb == 12 << D
+                continue
+            assert tb == 24 << D
+            for k in range(T):
+                rows = blob[k * tb + 8 * n_leaf:(k + 1) * tb].view(np.float32).reshape(n_leaf, 4)
+                for j in range(n_leaf):
+                    node = base.tree_offsets[order[k]] + leaf_map[k * n_leaf + j]
+                    np.testing.assert_array_equal(rows[j, :K], v[node])
+                    assert not rows[j, K:].any()
+        finally:
+            B.load_library().bridger_forest_destroy(h)
+
+
 def test_null_pointer_arguments():
     lib = B.load_library()
     h = ctypes.c_void_p()
