@@ -238,7 +238,9 @@ bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, c
  * values[indptr[i] .. indptr[i+1]) at features indices[same range]; every feature
  * not stored reads 0.0 (then goes through the fused preprocessing like any value).
  * Device pointers: indptr int64 [n_rows + 1] (non-decreasing), indices int32 and
- * values float [indptr[n_rows]].  Indices within a row must be distinct (a repeated
+ * values float [indptr[n_rows]]; indices and values are read only inside the rows'
+ * ranges and may be null when no entry is stored (a null indptr with n_rows > 0 is
+ * BRIDGER_ERR_INVALID_ARGUMENT).  Indices within a row must be distinct (a repeated
  * index gives one of its values, unspecified which); indices outside
  * [0, n_features) are ignored.  Same outputs and rules as predict /
  * predict_leaves; runs on the perfect and ragged kernel families

@@ -859,7 +859,8 @@ int32_t resolve_auto(const bridger_forest *h) {
 }
 
 bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_rows,
-                             int32_t n_features, const void *out, int x_align = 4) {
+                             int32_t n_features, const void *out, int x_align = 4,
+                             bool x_may_be_null = false) {
   if (!h) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null handle");
   if (h->host_only) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "handle was created host-only");
   if (n_rows < 0) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "n_rows < 0");
@@ -867,7 +868,8 @@ bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_r
     return fail(BRIDGER_ERR_INVALID_ARGUMENT,
                 "n_features " + std::to_string(n_features) + " != forest's " + std::to_string(h->F));
   if (n_rows == 0) return BRIDGER_OK;
-  if (!X || !out) return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null X or output pointer");
+  if ((!X && !x_may_be_null) || !out)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null X or output pointer");
   if (((uintptr_t)X % (uintptr_t)x_align) || ((uintptr_t)out & 3))
     return fail(BRIDGER_ERR_INVALID_ARGUMENT,
                 "X must be aligned to its element size and the output to 4 bytes");
@@ -992,8 +994,10 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   g_last_error.clear();
   if (csr && h && !(h->kernel_active == kPerfect || h->kernel_active == kRagged))
     return fail(BRIDGER_ERR_UNSUPPORTED, "CSR rows run on the perfect and ragged kernels only");
-  if (csr && n_rows > 0 && (!csr->indptr || !csr->indices))
-    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null CSR array");
+  // CSR: indptr is always read; indices and values only inside the rows' ranges, so they may
+  // be null when no entry is stored
+  if (csr && n_rows > 0 && !csr->indptr)
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT, "null CSR indptr");
   if (out_label && h && h->K == 1 && h->transform != BRIDGER_XFORM_SIGMOID)
     return fail(BRIDGER_ERR_UNSUPPORTED,
                 "labels need several classes or a sigmoid output (a classifier)");
@@ -1001,7 +1005,7 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
     return fail(BRIDGER_ERR_UNSUPPORTED, "a feature has 65536 or more distinct thresholds");
   const int xsz = binned && h ? h->bin_bytes : 4;
   void *dst = out ? (void *)out : (out_leaf ? (void *)out_leaf : (void *)out_label);
-  bridger_status s = check_predict(h, X, n_rows, n_features, dst, xsz);
+  bridger_status s = check_predict(h, X, n_rows, n_features, dst, xsz, csr != nullptr);
   if (s != BRIDGER_OK || n_rows == 0) return s;
   if (binned && !((h->kernel_active == kPerfect && h->perfect_bok) ||
                   (h->kernel_active == kRagged && h->ragged_bok)))

@@ -67,7 +67,7 @@ def _random_case(seed):
     return model, X, vector
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(200))
 def test_random_forests(seed):
     import torch
     model, X, vector = _random_case(seed)

@@ -102,3 +102,30 @@ def test_csr_prediction(case, monkeypatch):
         with pytest.raises(B.BridgerError) as e:
             f.predict_csr(d(ip), d(ix), d(v), n, out=out)
         assert e.value.status == B.BRIDGER_ERR_UNSUPPORTED
+
+
+@pytest.mark.gpu
+def test_csr_rows_without_entries():
+    """Rows that store no entry (every feature reads 0.0): the index and value arrays are empty
+    and may be null; the result is the prediction of all-zero rows."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rng = np.random.default_rng(115)
+    model = random_tiny_forest(rng, 12, 3, max_depth=6)
+    n = 70
+    X = np.zeros((n, 3), np.float32)
+    ref, ref_lv = oracle_predict(model, X, leaves=True)
+    ip = torch.zeros(n + 1, dtype=torch.int64, device="cuda")
+    ix = torch.empty(0, dtype=torch.int32, device="cuda")
+    v = torch.empty(0, dtype=torch.float32, device="cuda")
+    with B.Forest(model) as f:
+        out = f.predict_csr(ip, ix, v, n)
+        lv = f.predict_csr(ip, ix, v, n, leaves=True)
+        torch.cuda.synchronize()
+        assert_scores(out.cpu().numpy().astype(np.float64), ref, "empty csr")
+        assert_leaves(lv.cpu().numpy(), ref_lv, "empty csr")
+        with pytest.raises(B.BridgerError) as e:  # indptr is always needed
+            B.bridger_forest_predict_csr(f._h, 0, 0, 0, n, 3, out.data_ptr(),
+                                         torch.cuda.current_stream().cuda_stream)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
