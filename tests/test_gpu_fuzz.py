@@ -30,18 +30,21 @@ def _cuda():
     yield
 
 
-def _random_case(seed):
-    rng = np.random.default_rng(1000 + seed)
-    F = int(rng.integers(1, 10))
-    K = int(rng.integers(1, 5))
+def _random_case(seed, wide=False):
+    """Narrow rows (1-9 features, 1-4 classes), or wide ones (100-900 features, 1-8 classes,
+    up to 160 trees: the global-node kernels with lane groups, class slots and 8-class vector
+    leaves)."""
+    rng = np.random.default_rng((5000 if wide else 1000) + seed)
+    F = int(rng.integers(100, 901)) if wide else int(rng.integers(1, 10))
+    K = int(rng.integers(1, 9 if wide else 5))
     agg = AGG_MEAN if rng.random() < 0.4 else AGG_SUM
     if K == 1:
         xform = XFORM_SIGMOID if rng.random() < 0.5 else XFORM_IDENTITY
     else:
         xform = XFORM_SOFTMAX if rng.random() < 0.5 else XFORM_IDENTITY
-    T = int(rng.integers(K, 3 * K + 20))
+    T = int(rng.integers(K, 160)) if wide else int(rng.integers(K, 3 * K + 20))
     if rng.random() < 0.4:   # perfect trees of one depth
-        D = int(rng.integers(1, 7))
+        D = int(rng.integers(1, 9 if wide else 7))
         trees = [perfect_tree_arrays(D, rng.integers(0, F, (1 << D) - 1),
                                      GRID[rng.integers(0, len(GRID), (1 << D) - 1)],
                                      rng.standard_normal(1 << D).astype(np.float32)) for _ in range(T)]
@@ -58,7 +61,7 @@ def _random_case(seed):
     vector = K > 1 and xform != XFORM_SIGMOID and rng.random() < 0.3
     if vector:
         model = with_vector_leaves(model, K, rng, aggregate=agg, transform=xform)
-    n = int(rng.integers(1, 1500))
+    n = int(rng.integers(1, 400 if wide else 1500))
     X = GRID[rng.integers(0, len(GRID), (n, F))] + (rng.random((n, F)) < 0.3) * rng.standard_normal((n, F))
     X = X.astype(np.float32)
     X[rng.random((n, F)) < 0.02] = np.nan
@@ -69,8 +72,16 @@ def _random_case(seed):
 
 @pytest.mark.parametrize("seed", range(200))
 def test_random_forests(seed):
+    _check_case(seed, *_random_case(seed))
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_wide_forests(seed):
+    _check_case(f"wide {seed}", *_random_case(seed, wide=True))
+
+
+def _check_case(seed, model, X, vector):
     import torch
-    model, X, vector = _random_case(seed)
     if vector:
         ref, ref_lv = V.predict(model, X)
     else:
