@@ -1,13 +1,15 @@
 """Randomized differential parity: seeded random forests of many shapes (ragged and perfect,
 1-9 features, 1-4 classes, sum/mean, identity/sigmoid/softmax, thresholds on a coarse grid so
 ties are common, NaN and infinite inputs, scalar and vector leaves) on every kernel family that
-takes them, against the oracles: scores, leaf ids and labels; binned and CSR rows too."""
+takes them, against the oracles: scores, leaf ids and labels; binned and CSR rows too; wide
+rows (global-node kernels) and fused preprocessing as well."""
 import dataclasses
 
 import numpy as np
 import pytest
 
 import paper_2405_12491_amd as B
+from oracle import preprocess as P
 from oracle import sparse as S
 from oracle import vector as V
 from parity_util import assert_leaves, assert_scores, check_labels, oracle_predict, to_dev
@@ -80,16 +82,37 @@ def test_random_wide_forests(seed):
     _check_case(f"wide {seed}", *_random_case(seed, wide=True))
 
 
-def _check_case(seed, model, X, vector):
+@pytest.mark.parametrize("seed", range(40))
+def test_random_preprocessed(seed):
+    """Random forests behind a random fused preprocessing step (scaler, Binarizer or Normalizer)
+    with random parameters; narrow rows for even seeds, wide ones for odd."""
+    model, X, vector = _random_case(300 + seed, wide=seed % 2 == 1)
+    rng = np.random.default_rng(9000 + seed)
+    F = X.shape[1]
+    kind = [P.MINMAX, P.CENTER_SCALE, P.BINARIZE, P.NORMALIZE][seed % 4]
+    a = b = None
+    if kind == P.MINMAX:
+        a, b = rng.uniform(-3, 3, F), rng.uniform(-2, 2, F)
+    elif kind == P.CENTER_SCALE:
+        a, b = rng.standard_normal(F), rng.uniform(0.1, 4, F) * rng.choice([-1, 1], F)
+    elif kind == P.BINARIZE:
+        a = GRID[rng.integers(0, len(GRID), F)].astype(np.float64)
+    _check_case(f"pre {seed}", model, X, vector, (kind, a, b))
+
+
+def _check_case(seed, model, X, vector, pre=None):
     import torch
+    Xp = X if pre is None else P.apply(pre[0], pre[1], pre[2], X)
     if vector:
-        ref, ref_lv = V.predict(model, X)
+        ref, ref_lv = V.predict(model, Xp)
     else:
-        ref, ref_lv = oracle_predict(model, X, leaves=True)
+        ref, ref_lv = oracle_predict(model, Xp, leaves=True)
     Xd = to_dev(X)
     K = model.n_classes
     classifier = K > 1 or model.transform == XFORM_SIGMOID
     with B.Forest(model) as f:
+        if pre is not None:
+            f.set_preprocess(*pre)
         ran = 0
         for k in KERNELS:
             try:
