@@ -100,6 +100,24 @@ def test_random_preprocessed(seed):
     _check_case(f"pre {seed}", model, X, vector, (kind, a, b))
 
 
+# planner overrides (read when a forest is created): every forced shape still passes the
+# planner's capacity checks, and a family without a feasible plan reports unsupported
+PLAN_OVERRIDES = [("BRIDGER_GLOBAL", ["0", "1"]), ("BRIDGER_ILP", ["1", "2", "4"]),
+                  ("BRIDGER_WAVES", ["1", "2", "4", "8"]), ("BRIDGER_ROWS", ["64", "128", "256"]),
+                  ("BRIDGER_CHUNK_TREES", ["4", "8", "32"]), ("BRIDGER_NO_FIXED", ["1"])]
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_plans(seed, monkeypatch):
+    """Random forests under random launch-shape overrides (global or chunked records, trees
+    per lane, waves and rows per workgroup, trees per chunk)."""
+    rng = np.random.default_rng(7000 + seed)
+    for key, values in PLAN_OVERRIDES:
+        if rng.random() < 0.4:
+            monkeypatch.setenv(key, str(values[rng.integers(0, len(values))]))
+    _check_case(f"plan {seed}", *_random_case(600 + seed, wide=seed % 3 == 2))
+
+
 def _check_case(seed, model, X, vector, pre=None):
     import torch
     Xp = X if pre is None else P.apply(pre[0], pre[1], pre[2], X)
@@ -134,9 +152,14 @@ def _check_case(seed, model, X, vector, pre=None):
         f.kernel = B.BRIDGER_KERNEL_AUTO
         if f.kernel in (B.BRIDGER_KERNEL_PERFECT, B.BRIDGER_KERNEL_RAGGED):
             if f.bin_info()["bin_bytes"]:
-                out = f.predict_binned(f.bin(Xd))
-                torch.cuda.synchronize()
-                assert_scores(out.cpu().numpy(), ref, f"seed {seed} binned")
+                q = f.bin(Xd)
+                try:
+                    out = f.predict_binned(q)
+                except B.BridgerError as e:  # a forced shape can leave the bins no plan
+                    assert e.status == B.BRIDGER_ERR_UNSUPPORTED and "plan" in str(seed)
+                else:
+                    torch.cuda.synchronize()
+                    assert_scores(out.cpu().numpy(), ref, f"seed {seed} binned")
             nz = np.nonzero(np.where(np.isnan(X), 1.0, X))
             ip = np.concatenate([[0], np.cumsum(np.bincount(nz[0], minlength=X.shape[0]))]).astype(np.int64)
             d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
