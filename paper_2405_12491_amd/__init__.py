@@ -40,6 +40,17 @@ BRIDGER_PRE_NORMALIZE = 4
 _lib = None
 
 
+def _launch_stream(device) -> int:
+    """Raw handle of torch's current stream on ``device`` (where the kernels are launched).
+    torch's raw-stream query costs about 0.1 us against about 2 us for the stream object, which
+    matters for small batches; the public query serves if the raw one is absent."""
+    import torch
+    try:
+        return torch._C._cuda_getCurrentRawStream(device.index)
+    except AttributeError:
+        return torch.cuda.current_stream(device).cuda_stream
+
+
 class BridgerError(RuntimeError):
     def __init__(self, status: int, where: str, message: str):
         super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {message}")
@@ -286,7 +297,7 @@ class Forest:
         self._check_x(X)
         if out is None:
             out = torch.empty((X.shape[0], self.n_classes), dtype=torch.float32, device=X.device)
-        stream = torch.cuda.current_stream(X.device).cuda_stream
+        stream = _launch_stream(X.device)
         bridger_forest_predict(self._h, X.data_ptr(), X.shape[0], self.n_features, out.data_ptr(),
                                stream)
         return out
@@ -301,7 +312,7 @@ class Forest:
             cols = self.n_trees if leaves else self.n_classes
             out = torch.empty((n_rows, cols), dtype=torch.int32 if leaves else torch.float32,
                               device=values.device)
-        stream = torch.cuda.current_stream(values.device).cuda_stream
+        stream = _launch_stream(values.device)
         bridger_forest_predict_csr(self._h, indptr.data_ptr(), indices.data_ptr(), values.data_ptr(),
                                    n_rows, self.n_features, out.data_ptr(), stream, leaves)
         return out
@@ -311,7 +322,7 @@ class Forest:
         self._check_x(X)
         if out is None:
             out = torch.empty((X.shape[0],), dtype=torch.int32, device=X.device)
-        stream = torch.cuda.current_stream(X.device).cuda_stream
+        stream = _launch_stream(X.device)
         bridger_forest_predict_labels(self._h, X.data_ptr(), X.shape[0], self.n_features,
                                       out.data_ptr(), stream)
         return out
@@ -321,7 +332,7 @@ class Forest:
         self._check_x(X)
         if out is None:
             out = torch.empty((X.shape[0], self.n_trees), dtype=torch.int32, device=X.device)
-        stream = torch.cuda.current_stream(X.device).cuda_stream
+        stream = _launch_stream(X.device)
         bridger_forest_predict_leaves(self._h, X.data_ptr(), X.shape[0], self.n_features,
                                       out.data_ptr(), stream)
         return out
@@ -345,7 +356,7 @@ class Forest:
         if out is None:
             out = torch.empty((X.shape[0], self.n_features),
                               dtype=torch.uint8 if bb == 1 else torch.int16, device=X.device)
-        stream = torch.cuda.current_stream(X.device).cuda_stream
+        stream = _launch_stream(X.device)
         bridger_forest_bin(self._h, X.data_ptr(), X.shape[0], self.n_features, out.data_ptr(), stream)
         return out
 
@@ -363,7 +374,7 @@ class Forest:
         self._check_q(Xq)
         if out is None:
             out = torch.empty((Xq.shape[0], self.n_classes), dtype=torch.float32, device=Xq.device)
-        stream = torch.cuda.current_stream(Xq.device).cuda_stream
+        stream = _launch_stream(Xq.device)
         bridger_forest_predict_binned(self._h, Xq.data_ptr(), Xq.shape[0], self.n_features,
                                       out.data_ptr(), stream)
         return out
@@ -373,7 +384,7 @@ class Forest:
         self._check_q(Xq)
         if out is None:
             out = torch.empty((Xq.shape[0], self.n_trees), dtype=torch.int32, device=Xq.device)
-        stream = torch.cuda.current_stream(Xq.device).cuda_stream
+        stream = _launch_stream(Xq.device)
         bridger_forest_predict_binned_leaves(self._h, Xq.data_ptr(), Xq.shape[0], self.n_features,
                                              out.data_ptr(), stream)
         return out
