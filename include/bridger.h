@@ -256,8 +256,9 @@ bridger_status bridger_forest_predict_csr_leaves(bridger_forest_t h, const int64
                                                  int32_t *out_leaf, void *stream);
 
 /*
- * Classifier labels (int32 [n_rows], device): with several classes the class of
- * largest value (the first on ties), taken on the double-precision class values
+ * Classifier labels (int32 [n_rows], device; the index operators of Table 4, an
+ * argmax over the class values): with several classes the class of largest value
+ * (the first on ties), taken on the double-precision class values
  * before the link function (softmax keeps their order); with one output and a
  * sigmoid link, 1 when the value is above zero (probability above one half), else
  * 0.  BRIDGER_ERR_UNSUPPORTED for one output without a sigmoid (a regressor).
