@@ -95,3 +95,39 @@ def test_normalizer_in_graph():
             torch.cuda.synchronize()
             ref, _ = oracle_predict(w.forest, P.apply(P.NORMALIZE, None, None, X))
             assert_scores(out.cpu().numpy(), ref, f"normalized replay {rep}")
+
+
+@pytest.mark.parametrize("name,n", [("gbdt_d6", 3000), ("mc_gbdt_d8", 200)])
+def test_binning_and_binned_predict_in_graph(name, n):
+    """A serving pipeline in one graph: the binning pass writes the bins of the captured input,
+    then the binned prediction reads them (two kernels, no allocation); replays with new rows
+    match the oracle and an eager run bit for bit."""
+    import torch
+    rng = np.random.default_rng(21)
+    w = make_workload(name, n)
+    X0 = w.X(n)
+    Xd = torch.from_numpy(X0).cuda()
+    out = torch.empty((n, w.forest.n_classes), dtype=torch.float32, device="cuda")
+    with B.Forest(w.forest) as f:
+        q = f.bin(Xd)
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            f.bin(Xd, q)
+            f.predict_binned(q, out)
+        s.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            f.bin(Xd, q)
+            f.predict_binned(q, out)
+        for rep in range(4):
+            X = (rng.standard_normal(X0.shape) * (rep + 1)).astype(np.float32) if rep else X0
+            Xd.copy_(torch.from_numpy(X))
+            torch.cuda.synchronize()
+            out.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            ref, _ = oracle_predict(w.forest, X)
+            assert_scores(out.cpu().numpy(), ref, f"{name} binned replay {rep}")
+            eager = f.predict_binned(f.bin(Xd))
+            torch.cuda.synchronize()
+            assert np.array_equal(eager.cpu().numpy().view(np.uint32), out.cpu().numpy().view(np.uint32))
