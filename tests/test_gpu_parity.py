@@ -386,6 +386,44 @@ def test_determinism_and_streams():
     assert np.array_equal(a.view(np.uint32), c.view(np.uint32))
 
 
+def test_concurrent_host_threads():
+    """One handle serving several host threads at once, each with its own stream and rows (the
+    C calls release the interpreter lock): every thread's scores, leaf ids and binned scores
+    match the single-threaded results bit for bit, over repeated rounds."""
+    import threading
+    import torch
+    w = make_workload("gbdt_d6", 4000)
+    Xs = [to_dev((w.X() * np.float32(1 + 0.25 * i)).astype(np.float32)) for i in range(4)]
+    with B.Forest(w.forest) as f:
+        want = []
+        for Xd in Xs:
+            want.append((gpu_predict(f, Xd), gpu_predict(f, Xd, leaves=True),
+                         f.predict_binned(f.bin(Xd)).cpu().numpy()))
+        errors = []
+
+        def worker(i):
+            try:
+                s = torch.cuda.Stream()
+                with torch.cuda.stream(s):
+                    for _ in range(20):
+                        out = f.predict(Xs[i])
+                        lv = f.predict_leaves(Xs[i])
+                        ob = f.predict_binned(f.bin(Xs[i]))
+                    s.synchronize()
+                assert np.array_equal(out.cpu().numpy().view(np.uint32), want[i][0].view(np.uint32))
+                assert np.array_equal(lv.cpu().numpy(), want[i][1])
+                assert np.array_equal(ob.cpu().numpy().view(np.uint32), want[i][2].view(np.uint32))
+            except Exception as e:  # reported on the main thread
+                errors.append((i, repr(e)))
+
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(4)]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        assert not errors, errors
+
+
 def test_argument_errors():
     import torch
     w = make_workload("gbdt_d6", 64)
