@@ -434,6 +434,7 @@ struct PlanInput {
   bool perfect;
   double visits_per_row;
   int32_t x_bytes = 4;     // element of the LDS tile: 4 (fp32) or 2 / 1 (bins)
+  bool vec = false;        // vector leaves
 };
 
 // Smallest tile: bins pack 4 / x_bytes rows per 32-bit word and a half-wave's 32 rows must
@@ -469,7 +470,11 @@ Plan choose_plan(const PlanInput &in) {
         if (G > 1 && !in.perfect && R < 64) continue;
         const bool acc_lds = in.K > 1 || G > 1;
         const int64_t x_tile = (int64_t)in.F * R * in.x_bytes;
-        const int64_t acc_bytes = acc_lds ? (int64_t)in.K * G * R * 8 : 0;
+        // PERFECT with vector leaves of at most 8 classes keeps the class sums in registers
+        // and writes them only after the walk, into the row tile's LDS
+        const bool alias = in.perfect && in.vec && in.K <= 8 &&
+                           (int64_t)in.K * G * R * 8 <= x_tile;
+        const int64_t acc_bytes = acc_lds && !alias ? (int64_t)in.K * G * R * 8 : 0;
         for (int m = 1; m <= kMaxWavesPerCU / (W + 1); ++m) {  // workgroups per CU
           if (force_wg_per_cu && m != force_wg_per_cu) continue;
           if (pass == 0 && m * W < kMinWavesPerCU) continue;
@@ -524,6 +529,7 @@ Plan choose_plan(const PlanInput &in) {
           c.p.n_chunks = n_chunks;
           c.p.lds_bytes = (int32_t)lds;
           c.p.acc_in_lds = acc_lds;
+          c.p.acc_alias = alias ? 1 : 0;
           c.p.ilp = ilp;
           c.p.hbm_bytes = hbm;
           c.p.stage_bytes = stage;
@@ -948,6 +954,10 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
     a.lds_x_off = p.global_nodes ? 0 : 2 * p.chunk_bytes;
     a.lds_acc_off = a.lds_x_off + h->F * p.rows_per_wg * xsz;
     a.acc_in_lds = p.acc_in_lds;
+    if (p.acc_alias && !p.global_nodes) {  // class sums written into the tile after the walk
+      a.acc_alias = 1;
+      a.lds_acc_off = a.lds_x_off;
+    }
     a.ilp = p.ilp;
     const int64_t n_wg = (n_rows + p.rows_per_wg - 1) / p.rows_per_wg;
     // (bins compare exactly whatever the thresholds; fp32 needs them finite)
@@ -1164,6 +1174,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       pack_perfect(h, D, tree_offsets, feature, threshold, left, right, value);
       PlanInput pin{1 << 20, n_features, n_classes, n_trees,
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
+      pin.vec = vec;
       h->perfect_plan = pick_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
       if (h->perfect_ok) build_perfect_trav(h);
@@ -1172,6 +1183,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
     if (ragged_packed) {
       PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
                     (int32_t)std::min<int64_t>(h->ragged_max_tree_bytes, INT32_MAX), false, visits};
+      pin.vec = vec;
       h->ragged_plan = pick_plan(pin);
       h->ragged_ok = h->ragged_plan.waves > 0;
       if (h->ragged_ok && !h->ragged_plan.global_nodes)
@@ -1183,6 +1195,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       if (h->perfect_ok) {
         PlanInput pin{1 << 20, n_features, n_classes, n_trees, (double)h->perfect_blob.size(),
                       h->perfect_tree_bytes, true, visits, h->bin_bytes};
+        pin.vec = vec;
         h->perfect_bplan = pick_plan(pin);
         h->perfect_bok = h->perfect_bplan.waves > 0;
         if (h->perfect_bok) build_perfect_btrav(h);
@@ -1191,6 +1204,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
                       (int32_t)std::min<int64_t>(h->ragged_max_tree_bytes, INT32_MAX), false,
                       visits, h->bin_bytes};
+        pin.vec = vec;
         h->ragged_bplan = pick_plan(pin);
         h->ragged_bok = h->ragged_bplan.waves > 0;
         if (h->ragged_bok) {

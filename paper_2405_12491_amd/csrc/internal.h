@@ -74,6 +74,7 @@ struct Plan {
                            // PERFECT 4 or 8; global RAGGED 1, 2, 4 or 8
   int32_t global_nodes;    // records read from global memory, LDS holds only the tile
   int32_t waves_per_cu;    // resident compute waves per CU
+  int32_t acc_alias;       // class sums written after the walk into the row tile's LDS
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
 };
 
@@ -109,6 +110,7 @@ struct LaunchArgs {
   int32_t chunk_bytes;
   int32_t lds_x_off;           // byte offset of the feature tile in dynamic LDS
   int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
+  int32_t acc_alias;           // that area is the row tile's, written only after the walk
   int32_t acc_in_lds;
   int32_t ilp;                 // trees walked at once per lane (the plan's ilp)
   int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)

@@ -119,6 +119,7 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     return;
   }
   if (VK_REG) {
+    if (a.acc_alias) __syncthreads();  // the sums go into the row tile: every group is done
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
