@@ -470,9 +470,10 @@ Plan choose_plan(const PlanInput &in) {
         if (G > 1 && !in.perfect && R < 64) continue;
         const bool acc_lds = in.K > 1 || G > 1;
         const int64_t x_tile = (int64_t)in.F * R * in.x_bytes;
-        // PERFECT with vector leaves of at most 8 classes keeps the class sums in registers
-        // and writes them only after the walk, into the row tile's LDS
-        const bool alias = in.perfect && in.vec && in.K <= 8 &&
+        // PERFECT with at most 8 classes (vector leaves, or scalar leaves walked 4 trees at a
+        // time) keeps the class sums in registers and writes them only after the walk, into
+        // the row tile's LDS
+        const bool alias = in.perfect && acc_lds && in.K <= 8 && (in.vec || ilp == 4) &&
                            (int64_t)in.K * G * R * 8 <= x_tile;
         const int64_t acc_bytes = acc_lds && !alias ? (int64_t)in.K * G * R * 8 : 0;
         for (int m = 1; m <= kMaxWavesPerCU / (W + 1); ++m) {  // workgroups per CU

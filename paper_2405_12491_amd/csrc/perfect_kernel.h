@@ -10,7 +10,10 @@ namespace bridger {
 // VK: 0 scalar leaves; 2, 4 or 8 vector leaves (K <= VK) with the class sums in registers (for
 // VK = 2 and 4 the leaf rows come with the staged tree blocks, for VK = 8 from global memory);
 // 64 vector leaves with the class sums in LDS and the rows from global memory.
-template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, int VK = 0>
+// KS: scalar leaves of at most KS classes with the lane group's finished class sums kept in
+// registers and written to LDS (into the row tile, whose LDS the plan then shares with them)
+// only after the walk.
+template <int D, int U, bool LEAVES, bool SIMPLE, bool FIN, int XB, int VK = 0, int KS = 0>
 __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr bool VK_REG = VK == 2 || VK == 4 || VK == 8;  // vector leaves, sums in registers
@@ -50,6 +53,28 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
   double vacc[VR];
   if (VK_REG) vec_init_reg(a, vacc, g == 0);
   if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
+  // KS: a group walks its trees in ascending (class-sorted) order, so each class is summed in
+  // one stretch: the running sum moves to cs[k] when the class changes (rarely)
+  double cs[KS > 0 ? KS : 1];
+  if (KS) {
+#pragma unroll
+    for (int c = 0; c < KS; ++c) cs[c] = c < a.K ? class_init(a, c, g == 0) : 0.0;
+  }
+  auto advance_reg = [&](int t) {
+    if (t < ca.next_b) return;
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c == ca.k) cs[c] = ca.acc;
+    while (t >= ca.next_b) {
+      ca.k += 1;
+      ca.next_b = a.class_begin[ca.k + 1];
+    }
+    double v = 0.0;
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c == ca.k) v = cs[c];
+    ca.acc = v;
+  };
 
   // leaf ids or leaf values of N walked trees, kernel trees q .. q + N - 1
   auto finish = [&](auto &m, int q, uint32_t b0) {
@@ -82,7 +107,8 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
       for (int u = 0; u < N; ++u) lv[u] = lds_f32(smem, (m[u] << 2) + b0 + (uint32_t)u * tb + kLeafOff);
 #pragma unroll
       for (int u = 0; u < N; ++u) {
-        if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+        if (KS) advance_reg(q + u);
+        else if (!SIMPLE) class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
         ca.acc += (double)lv[u];
       }
     }
@@ -118,7 +144,15 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     }
     return;
   }
-  if (VK_REG) {
+  if (KS) {
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c == ca.k) cs[c] = ca.acc;
+    if (a.acc_alias) __syncthreads();  // the sums go into the row tile: every group is done
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c < a.K) acc_lds[c * slot_stride] = cs[c];
+  } else if (VK_REG) {
     if (a.acc_alias) __syncthreads();  // the sums go into the row tile: every group is done
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
@@ -156,6 +190,8 @@ static int launch_perfect_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int 
     return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, 64>, threads, n_wg, lds_bytes, stream, a);
   if (simple)
     return launch_common(perfect_kernel<D, 4, false, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
+  if (a.acc_alias && a.K <= 8 && a.ilp == 4)  // class sums in registers, then into the tile
+    return launch_common(perfect_kernel<D, 4, false, false, FIN, XB, 0, 8>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 1)
     return launch_common(perfect_kernel<D, 1, false, false, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.ilp == 2)
