@@ -291,6 +291,27 @@ def test_packed_layouts_permuted_and_classes():
         assert np.array_equal(lv, ref_lv)
 
 
+@pytest.mark.parametrize("K", [1, 3, 8, 10])
+def test_class_sums_share_the_row_tile(K):
+    """Chunked PERFECT plans for at most 8 classes keep the class sums in registers and write
+    them into the row tile after the walk: the LDS is the tile plus two chunk buffers.  More
+    classes reserve K x G x R doubles of class slots on top."""
+    import dataclasses
+    w = make_workload("gbdt_d6", 1000)
+    model = w.forest if K == 1 else dataclasses.replace(
+        w.forest, n_classes=K, tree_class=(np.arange(w.forest.n_trees) % K).astype(np.int32),
+        transform=XFORM_SOFTMAX, base_score=np.zeros(K, np.float32))
+    with host(model) as f:
+        p = f.plan(1_000_000)
+        R, F = p["rows_per_wg"], w.n_features
+        assert p["chunk_bytes"] > 0
+        tile_and_chunks = 2 * p["chunk_bytes"] + R * F * 4
+        if K <= 8:
+            assert p["lds_bytes"] == tile_and_chunks
+        else:
+            assert p["lds_bytes"] >= tile_and_chunks + 8 * K * R
+
+
 @pytest.mark.parametrize("name", list(CONFIGS))
 def test_plan_respects_lds_capacity(name):
     w = make_workload(name, 1000)
