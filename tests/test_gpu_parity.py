@@ -258,7 +258,8 @@ VARIANT_ENVS = [
     {"BRIDGER_CHUNK_TREES": "32"},
     {"BRIDGER_ILP": "1", "BRIDGER_WAVES": "4", "BRIDGER_ROWS": "64"},   # 4 lane groups, 1 tree
     {"BRIDGER_ILP": "2", "BRIDGER_WAVES": "2", "BRIDGER_ROWS": "64"},   # 2 lane groups, 2 trees
-]
+    {"BRIDGER_ILP": "4", "BRIDGER_WAVES": "4", "BRIDGER_ROWS": "64"},   # 4 lane groups, 4 trees:
+]                                                                      # class sums in registers
 
 
 def _variant_models():
@@ -272,7 +273,12 @@ def _variant_models():
     X6 = rng.standard_normal((1100, 6)).astype(np.float32)
     g = make_workload("gbdt_d6", 1500)
     r = make_workload("rf_d8", 700)
-    return [("gbdt_d6", g.forest, g.X()), ("rf_d8", r.forest, r.X()), ("multiclass", multi, X6)]
+    import dataclasses
+    g3 = dataclasses.replace(g.forest, n_classes=3, aggregate=AGG_MEAN, transform=XFORM_SOFTMAX,
+                             tree_class=(np.arange(g.forest.n_trees) % 3).astype(np.int32),
+                             base_score=rng.standard_normal(3).astype(np.float32))
+    return [("gbdt_d6", g.forest, g.X()), ("rf_d8", r.forest, r.X()), ("multiclass", multi, X6),
+            ("multiclass28", g3, g.X())]
 
 
 @pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1"}, {"BRIDGER_GLOBAL": "1", "BRIDGER_ILP": "2"},
