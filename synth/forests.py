@@ -101,6 +101,30 @@ def x_rows(seed: int, kind: str, n_features: int, r0: int, r1: int, **kw) -> np.
     return out
 
 
+def x_rows_threaded(seed: int, kind: str, n_features: int, r0: int, r1: int, threads: int = 8,
+                    **kw) -> np.ndarray:
+    """Rows [r0, r1) as ``x_rows``, the blocks drawn on ``threads`` threads (each block has its
+    own generator, so the result does not depend on the thread count)."""
+    from concurrent.futures import ThreadPoolExecutor
+    out = np.empty((max(r1 - r0, 0), n_features), dtype=np.float32)
+    if r1 <= r0:
+        return out
+    spans = []
+    r = r0
+    while r < r1:
+        e = min(r1, (r // BLOCK_ROWS + 1) * BLOCK_ROWS)
+        spans.append((r, e))
+        r = e
+
+    def fill(span):
+        a, b = span
+        out[a - r0:b - r0] = x_rows(seed, kind, n_features, a, b, **kw)
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(fill, spans))
+    return out
+
+
 def x_take(seed: int, kind: str, n_features: int, rows, **kw) -> np.ndarray:
     """The given rows (any order) of the feature matrix, generating each needed block once."""
     rows = np.asarray(rows, np.int64)

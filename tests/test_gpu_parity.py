@@ -447,59 +447,8 @@ def test_argument_errors():
         assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
 
 
-# ------------------------------------------------------------- full-size workloads
-def _full_X_device(w):
-    """The full feature matrix on the device, built block by block."""
-    import torch
-    from synth import BLOCK_ROWS, x_rows
-    Xd = torch.empty((w.n_rows, w.n_features), dtype=torch.float32, device="cuda")
-    step = BLOCK_ROWS * 4
-    for r in range(0, w.n_rows, step):
-        blk = x_rows(w.seed, w.x_kind, w.n_features, r, min(r + step, w.n_rows), **w.x_params)
-        Xd[r:r + blk.shape[0]].copy_(torch.from_numpy(blk))
-        if (r // step) % 8 == 0:
-            print(f"[full] X rows {r}..{r + blk.shape[0]}", flush=True)
-    return Xd
-
-
-def _sample_rows(n, R, rng, k=1500):
-    idx = set(range(min(n, R + 3)))                 # the first tile and a bit
-    idx |= set(range(max(0, n - R - 3), n))          # the last (ragged) tile
-    idx |= set(rng.integers(0, n, k).tolist())
-    return np.array(sorted(idx))
-
-
-@pytest.mark.parametrize("name", list(CONFIGS))
-def test_workload_full_size_sampled(name):
-    """Full-size inputs in the benchmark's launch configuration; sampled rows against the
-    oracle, plus leaf ids on windows at the start, middle and end."""
-    import torch
-    from synth import x_rows, x_take
-    w = make_workload(name)
-    print(f"[full] {name}: building X {w.n_rows}x{w.n_features}", flush=True)
-    Xd = _full_X_device(w)
-    rng = np.random.default_rng(1234)
-    with B.Forest(w.forest) as f:
-        plan = f.plan(w.n_rows)
-        print(f"[full] {name}: kernel={B.KERNEL_NAMES[f.kernel]} plan={plan}", flush=True)
-        out = f.predict(Xd)
-        torch.cuda.synchronize()
-        got = out.cpu().numpy()
-        idx = _sample_rows(w.n_rows, plan["rows_per_wg"] or 256, rng)
-        print(f"[full] {name}: oracle on {len(idx)} sampled rows", flush=True)
-        Xs = x_take(w.seed, w.x_kind, w.n_features, idx, **w.x_params)
-        ref, _ = oracle_predict(w.forest, Xs)
-        assert_scores(got[idx], ref, f"{name} full-size sampled scores")
-        assert np.all(np.isfinite(got))
-        win = 256 if w.forest.n_trees * w.n_features < 300_000 else 64
-        for a in (0, w.n_rows // 2 + 13, w.n_rows - win):
-            print(f"[full] {name}: leaf ids for rows [{a}, {a + win})", flush=True)
-            lv = gpu_predict(f, Xd[a:a + win], leaves=True)
-            _, ref_lv = oracle_predict(w.forest, x_rows(w.seed, w.x_kind, w.n_features, a, a + win, **w.x_params),
-                                       leaves=True)
-            assert_leaves(lv, ref_lv, f"{name} full-size leaves @{a}")
-    del Xd
-    torch.cuda.empty_cache()
+# The full-size workloads are checked exhaustively (every score, every leaf id) in
+# test_gpu_full_parity.py.
 
 
 def _chain_tree(depth, F, rng):

@@ -10,6 +10,7 @@ import os
 import subprocess
 import tempfile
 
+import numpy as np
 import pytest
 
 import oracle
@@ -65,3 +66,19 @@ def test_pins_reject_mutant(name):
             except (AssertionError, oracle.OracleError, IndexError, ValueError) as e:  # noqa: PERF203
                 caught.append((pin.__name__, type(e).__name__))
         assert caught, f"no pin rejects mutant {name}"
+
+
+@pytest.mark.parametrize("name,n", [("gbdt_d6", 1003), ("mc_gbdt_d8", 353), ("ragged_d12", 351)])
+def test_oracle_thread_split(name, n):
+    """The wrapper's row split over threads: 7 threads on a row count that 7 does not divide
+    give the one-thread results bit for bit (scores and leaf ids), and both agree with the
+    independent vectorized traversal on every leaf id."""
+    from synth import make_workload
+    assert n % 7 != 0
+    w = make_workload(name, n)
+    X = w.X()
+    o1, l1, v1 = oracle.predict(w.forest, X, want_leaves=True, threads=1)
+    o7, l7, v7 = oracle.predict(w.forest, X, want_leaves=True, threads=7)
+    assert np.array_equal(o1, o7) and np.array_equal(l1, l7) and v1 == v7
+    _, lv = P.numpy_traverse(w.forest, X)
+    assert np.array_equal(l7, lv)
