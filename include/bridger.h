@@ -149,6 +149,25 @@ bridger_status bridger_forest_predict(bridger_forest_t h, const float *X, int64_
                                       int32_t n_features, float *out, void *stream);
 
 /*
+ * Allocation-free predict, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same arguments,
+ * outputs, rules and errors as bridger_forest_predict, except that:
+ *   - n_rows must be at most BRIDGER_NOALLOC_MAX_ROWS (BRIDGER_ERR_INVALID_ARGUMENT beyond,
+ *     checked first, before any other argument);
+ *   - the call allocates nothing: the Normalizer's row norms (BRIDGER_PRE_NORMALIZE, the only
+ *     scratch of a prediction) go to a fixed device array of the library, 16 MiB per GPU,
+ *     held by every GPU the library runs on until the process ends.  Its address is looked
+ *     up once per device, at the first call on that device.
+ * Every allocation-free call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (on other streams, or through other handles) race and must be serialized by the
+ * caller, e.g. by issuing them on one stream.  Nothing in the array needs clearing: every
+ * call writes its rows' norms before reading them.
+ */
+#define BRIDGER_NOALLOC_MAX_ROWS 2097152
+bridger_status bridger_forest_predict_noalloc(bridger_forest_t h, const float *X, int64_t n_rows,
+                                              int32_t n_features, float *out, void *stream);
+
+/*
  * Write, for every (row, tree), the id of the leaf the row reaches, in the
  * caller's tree-local node numbering: device int32 [n_rows, n_trees], row-major
  * (tree index in the caller's order).  Same arguments and rules as predict.

@@ -72,6 +72,7 @@ def load_library(path: Optional[str] = None):
     lib.bridger_forest_create_ex.argtypes = create_args + [U32, P]
     lib.bridger_forest_predict.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_predict_leaves.argtypes = [P, P, I64, I32, P, P]
+    lib.bridger_forest_predict_noalloc.argtypes = [P, P, I64, I32, P, P]
     lib.bridger_forest_info.argtypes = [P, P, P, P, P, P]
     lib.bridger_forest_bin_info.argtypes = [P, P, P]
     lib.bridger_forest_predict_labels.argtypes = [P, P, I64, I32, P, P]
@@ -142,6 +143,18 @@ def bridger_forest_predict(h, X_ptr: int, n_rows: int, n_features: int, out_ptr:
     _check(load_library().bridger_forest_predict(h, ctypes.c_void_p(X_ptr), int(n_rows),
                                                  int(n_features), ctypes.c_void_p(out_ptr),
                                                  ctypes.c_void_p(stream)), "bridger_forest_predict")
+
+
+NOALLOC_MAX_ROWS = 2097152   # BRIDGER_NOALLOC_MAX_ROWS
+
+
+def bridger_forest_predict_noalloc(h, X_ptr: int, n_rows: int, n_features: int, out_ptr: int,
+                                   stream: int = 0):
+    """The allocation-free predict (at most NOALLOC_MAX_ROWS rows per call)."""
+    _check(load_library().bridger_forest_predict_noalloc(h, ctypes.c_void_p(X_ptr), int(n_rows),
+                                                         int(n_features), ctypes.c_void_p(out_ptr),
+                                                         ctypes.c_void_p(stream)),
+           "bridger_forest_predict_noalloc")
 
 
 def bridger_forest_predict_leaves(h, X_ptr: int, n_rows: int, n_features: int, out_ptr: int,

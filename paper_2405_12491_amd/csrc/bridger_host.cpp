@@ -830,9 +830,18 @@ struct RowNorms {
   }
 };
 
+// `scratch` (the allocation-free entry point) replaces the pool allocation when given.
 bridger_status prepare_row_norms(const bridger_forest *h, LaunchArgs &a, void *stream,
-                                 RowNorms &rn) {
+                                 RowNorms &rn, double *scratch = nullptr) {
   if (h->pre_kind != BRIDGER_PRE_NORMALIZE) return BRIDGER_OK;
+  if (scratch) {
+    const int err = launch_row_norm(a, scratch, stream);
+    if (err != 0)
+      return fail(BRIDGER_ERR_DEVICE, std::string("row-norm launch failed: ") +
+                                          hipGetErrorString((hipError_t)err));
+    a.row_norm = scratch;
+    return BRIDGER_OK;
+  }
   if (hipMallocAsync((void **)&rn.p, (size_t)a.n_rows * sizeof(double), (hipStream_t)stream) !=
       hipSuccess) {
     (void)hipGetLastError();
@@ -898,7 +907,7 @@ struct CsrRows {
 // batches.
 bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, float *out,
                            int32_t *out_leaf, int32_t *out_label, const CsrRows *csr,
-                           void *stream, bool binned, int xsz) {
+                           void *stream, bool binned, int xsz, double *norm_scratch) {
   bridger_status s = BRIDGER_OK;
   LaunchArgs a{};
   a.X = (const float *)X;
@@ -925,7 +934,7 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
   RowNorms norms;
   if (!binned) {
     set_preprocess_args(h, a);
-    if ((s = prepare_row_norms(h, a, stream, norms)) != BRIDGER_OK) return s;
+    if ((s = prepare_row_norms(h, a, stream, norms, norm_scratch)) != BRIDGER_OK) return s;
   }
   int err = 0;
   if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
@@ -1001,7 +1010,8 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
 
 bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int32_t n_features,
                           float *out, int32_t *out_leaf, void *stream, bool binned,
-                          int32_t *out_label = nullptr, const CsrRows *csr = nullptr) {
+                          int32_t *out_label = nullptr, const CsrRows *csr = nullptr,
+                          bool no_alloc = false) {
   g_last_error.clear();
   if (csr && h && !(h->kernel_active == kPerfect || h->kernel_active == kRagged))
     return fail(BRIDGER_ERR_UNSUPPORTED, "CSR rows run on the perfect and ragged kernels only");
@@ -1029,6 +1039,20 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
   if (!csr && xb < ob + obytes && ob < xb + xbytes)
     return fail(BRIDGER_ERR_INVALID_ARGUMENT, "output overlaps X");
 
+  // The allocation-free entry point: the row norms go to the library's static scratch.
+  double *norm_scratch = nullptr;
+  if (no_alloc) {
+    if (n_rows > kNoAllocMaxRows)
+      return fail(BRIDGER_ERR_INVALID_ARGUMENT,
+                  "n_rows " + std::to_string(n_rows) + " exceeds the allocation-free limit of " +
+                      std::to_string(kNoAllocMaxRows) + " rows per call");
+    if (h->pre_kind == BRIDGER_PRE_NORMALIZE) {
+      const int err = noalloc_norm_scratch(&norm_scratch);
+      if (err != 0)
+        return fail(BRIDGER_ERR_DEVICE, std::string("scratch lookup failed: ") +
+                                            hipGetErrorString((hipError_t)err));
+    }
+  }
   // A dispatch counts its work-items in 32 bits: larger batches go out as several launches of
   // at most kMaxRowsPerLaunch rows each (tile boundaries are unaffected: every tile size divides
   // it).  CSR rows keep absolute entry offsets, so only indptr moves.
@@ -1040,7 +1064,7 @@ bridger_status do_predict(bridger_forest *h, const void *X, int64_t n_rows, int3
     s = launch_rows(h, xr, nr, out ? out + r0 * h->K : nullptr,
                     out_leaf ? out_leaf + r0 * h->n_trees : nullptr,
                     out_label ? out_label + r0 : nullptr, csr ? &part : nullptr, stream, binned,
-                    xsz);
+                    xsz, norm_scratch);
     if (s != BRIDGER_OK) return s;
   }
   return BRIDGER_OK;
@@ -1281,6 +1305,18 @@ bridger_status bridger_forest_create(int32_t n_trees, const int64_t *tree_offset
 bridger_status bridger_forest_predict(bridger_forest_t h, const float *X, int64_t n_rows,
                                       int32_t n_features, float *out, void *stream) {
   return do_predict(h, X, n_rows, n_features, out, nullptr, stream, false);
+}
+
+bridger_status bridger_forest_predict_noalloc(bridger_forest_t h, const float *X, int64_t n_rows,
+                                              int32_t n_features, float *out, void *stream) {
+  if (n_rows > kNoAllocMaxRows) {  // before any other check: a size error is the first answer
+    g_last_error.clear();
+    return fail(BRIDGER_ERR_INVALID_ARGUMENT,
+                "n_rows " + std::to_string(n_rows) + " exceeds the allocation-free limit of " +
+                    std::to_string(kNoAllocMaxRows) + " rows per call");
+  }
+  return do_predict(h, X, n_rows, n_features, out, nullptr, stream, false, nullptr, nullptr,
+                    true);
 }
 
 bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X, int64_t n_rows,

@@ -44,6 +44,9 @@ constexpr int kMaxRaggedFeatures = 0xFFFF;
 // dispatch; predictions over more rows are issued as several launches.
 constexpr int64_t kMaxRowsPerLaunch = int64_t(1) << 24;
 constexpr int kMaxClasses = 64;  // class sums of one 256-row block fit LDS in every kernel
+// Rows per call of the allocation-free predict (its row-norm scratch: one double per row, a
+// file-scope device array of 16 MiB per GPU).
+constexpr int64_t kNoAllocMaxRows = int64_t(1) << 21;
 
 enum Kernel { kAuto = 0, kPerfect = 1, kRagged = 2, kDirect = 3, kGemm = 4 };
 
@@ -139,6 +142,9 @@ int launch_perfect_binned(int depth, const LaunchArgs &a, int waves, int64_t n_w
                           void *stream);
 int launch_bin(const LaunchArgs &a, void *stream);
 int launch_row_norm(const LaunchArgs &a, double *norm, void *stream);
+// Device address of the allocation-free predict's row-norm scratch on the current device
+// (kNoAllocMaxRows doubles); looked up once per device.  Returns a hipError_t as int.
+int noalloc_norm_scratch(double **ptr);
 int launch_perfect_global(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                           void *stream);
 int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,

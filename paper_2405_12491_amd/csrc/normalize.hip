@@ -1,6 +1,8 @@
 // normalize.hip -- gfx950 row-norm pass for the fused Normalizer (unit L2 rows).
 #include "kernel_common.h"
 
+#include <mutex>
+
 namespace bridger {
 
 // ================================================================== ROW NORMS
@@ -70,6 +72,36 @@ int launch_row_norm(const LaunchArgs &a, double *norm, void *stream) {
   hipLaunchKernelGGL(row_norm_kernel, dim3((uint32_t)blocks), dim3(kNormRows), 0,
                      (hipStream_t)stream, a, norm);
   return (int)hipGetLastError();
+}
+
+// ================================================= scratch of the allocation-free predict
+// The row norms of bridger_forest_predict_noalloc live in this file-scope device array (every
+// GPU the library runs on holds its own copy until the process ends), so that call allocates
+// nothing.  Host code never passes the array's name to a kernel: in host code that name is a
+// host-side stand-in, not a device address.  The device address comes from hipGetSymbolAddress,
+// taken once per device with that device current, and is passed to the row-norm kernel like
+// the stream-ordered buffer of bridger_forest_predict.  The norms are written for every row
+// before any kernel reads them, so nothing needs clearing between calls; calls that overlap on
+// one GPU (other streams, other handles) share the array and race.
+static __device__ __align__(256) double scratch[kNoAllocMaxRows];
+
+int noalloc_norm_scratch(double **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static double *addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  if (dev < 0 || dev >= kMaxDevices) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return e != hipSuccess ? (int)e : (int)hipErrorInvalidSymbol;
+    addr[dev] = (double *)p;
+  }
+  *ptr = addr[dev];
+  return 0;
 }
 
 }  // namespace bridger

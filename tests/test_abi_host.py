@@ -168,6 +168,23 @@ def test_predict_on_host_only_handle_fails():
         assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
 
 
+def test_noalloc_size_limit():
+    """The allocation-free predict rejects more rows than its scratch holds, before anything
+    else is checked (so on a host-only handle too); the header and binding agree on the limit."""
+    text = open(HEADER).read()
+    m = re.search(r"#define BRIDGER_NOALLOC_MAX_ROWS (\d+)", text)
+    assert m and int(m.group(1)) == B.NOALLOC_MAX_ROWS
+    with host(_tiny()) as f:
+        with pytest.raises(B.BridgerError) as e:
+            B.bridger_forest_predict_noalloc(f.handle, 16, B.NOALLOC_MAX_ROWS + 1, 2, 64, 0)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
+        assert "allocation-free limit" in B.bridger_last_error()
+        with pytest.raises(B.BridgerError) as e:   # within the limit: the host-only handle
+            B.bridger_forest_predict_noalloc(f.handle, 16, 1, 2, 64, 0)
+        assert e.value.status == B.BRIDGER_ERR_INVALID_ARGUMENT
+        assert "host-only" in B.bridger_last_error()
+
+
 # ----------------------------------------------------- packed-layout interpreter
 def walk_perfect(f: B.Forest, model, X):
     """1-based heap: slot m at byte 8m (children 2m, 2m+1), leaves from byte 8*2^D."""
