@@ -109,7 +109,63 @@ def parse():
                         "then one replay; times are reported per prediction)")
     p.add_argument("--calib-copy", action="store_true",
                    help="time a plain device copy of X instead (counter calibration)")
+    p.add_argument("--calib-lds", action="store_true",
+                   help="run only the calibration microbenchmarks (per-lane LDS gathers of 4, 8 "
+                        "and 16 bytes, conflict-free and random; HBM copy) and print them")
+    p.add_argument("--clock-warm-ms", type=float, default=300.0,
+                   help="untimed launches for at least this long before the warmup steps, so "
+                        "that the GPU reaches its steady clock whatever --warmup is")
     return p.parse_args()
+
+
+def load_calib():
+    import ctypes
+    import paper_2405_12491_amd as B
+    path = os.path.join(os.path.dirname(B.LIB_PATH), "libbridger_calib.so")
+    if not os.path.exists(path):
+        raise OSError(f"{path} not found: build it with `python -m paper_2405_12491_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.bridger_calib_device.argtypes = [P, P, P]
+    lib.bridger_calib_lds_gather.argtypes = [I32, I32, I32, P, P]
+    lib.bridger_calib_copy.argtypes = [I64, I32, P, P]
+    return lib
+
+
+def calibrate(copy_bytes=512 << 20, reps=20):
+    """The calibration microbenchmarks (libbridger_calib.so): per-lane LDS gather rates (lanes
+    per clock per CU at the nominal clock) and the HBM copy rate on this device."""
+    import ctypes
+    lib = load_calib()
+    n_cu, clk, lds = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    assert lib.bridger_calib_device(ctypes.byref(n_cu), ctypes.byref(clk), ctypes.byref(lds)) == 0
+    out = {"n_cu": n_cu.value, "max_clock_khz": clk.value, "lds_bytes_per_cu": lds.value,
+           "nominal_clock_ghz": CLOCK_HZ / 1e9}
+    def gather(width, distinct):
+        ms, rate = ctypes.c_double(), ctypes.c_double()
+        rc = lib.bridger_calib_lds_gather(width, distinct, reps, ctypes.byref(ms),
+                                          ctypes.byref(rate))
+        if rc != 0:
+            raise RuntimeError(f"bridger_calib_lds_gather({width}, {distinct}) failed: {rc}")
+        return rate.value * 64 / (N_CU * CLOCK_HZ)
+
+    out["lds_gather_lanes_per_clk_per_cu"] = {
+        "b32": gather(4, 64), "b64": gather(8, 64), "b128": gather(16, 64),
+        "b32_random": gather(4, 0)}
+    # node-record reads (b64) when the wave's lanes share 1, 2, ..., 32 records
+    out["lds_b64_lanes_per_clk_per_cu_by_distinct"] = {
+        str(d): gather(8, d) for d in (1, 2, 4, 8, 16, 32)}
+    ms, rate = ctypes.c_double(), ctypes.c_double()
+    rc = lib.bridger_calib_copy(copy_bytes, reps, ctypes.byref(ms), ctypes.byref(rate))
+    if rc != 0:
+        raise RuntimeError(f"bridger_calib_copy failed: {rc}")
+    out["copy_GBps"] = rate.value / 1e9
+    out["copy_bytes"] = copy_bytes
+    out["what"] = ("per-lane LDS gathers at addresses held in registers, 32 waves per CU, 16 "
+                   "independent reads per lane in flight; lanes per clock per CU at the nominal "
+                   "clock (the peak rates the kernels against 32); copy: read + write bytes/s "
+                   "of a 16-byte-per-lane device copy")
+    return out
 
 
 def build_x(w, device):
@@ -179,6 +235,25 @@ def node_depths(f):
     return depth
 
 
+def host_threads():
+    """Threads for the CPU oracle: every core this process may use, up to the host's CPU share
+    per GPU (OMP_NUM_THREADS where the environment sets it); and a record of the host."""
+    affinity = len(os.sched_getaffinity(0))
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    threads = max(1, min(affinity, share) if share > 0 else affinity)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return threads, {"nproc": os.cpu_count(), "affinity": affinity,
+                     "cpu_share": share or None, "threads_used": threads, "cpu_model": model}
+
+
 def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False):
     """The CPU oracle (with the oracle's preprocessing first, when fused) timed on the host's
     cores over the first `sample_rows` rows; its outputs are also compared with the GPU's for
@@ -188,7 +263,7 @@ def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False
     from synth import x_rows
     n = min(sample_rows, w.n_rows)
     X = x_rows(w.seed, w.x_kind, w.n_features, 0, n, **w.x_params)
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    threads, host = host_threads()
     t0 = time.perf_counter()
     if pre[0] != "none":
         X = P.apply(PRE_KINDS[pre[0]], pre[1], pre[2], X)
@@ -214,7 +289,7 @@ def cpu_baseline(w, out_dev, sample_rows, pre=("none", None, None), labels=False
     else:
         got = got.astype(np.float64)
         ok = bool(np.all(np.abs(got - ref) <= 1e-6 + 1e-5 * np.abs(ref)))
-    return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+    return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle", "host": host,
             "sample": f"first {n:,} rows of the {w.n_rows:,}-row workload ({visits:,} node visits), "
                       f"{dt:.2f} s wall on {threads} threads",
             "visits_per_s": visits / dt, "agrees_with_gpu": ok,
@@ -235,6 +310,10 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calib_lds:
+        print(json.dumps({"calibration": calibrate()}), flush=True)
+        return
+    calib = calibrate()
     w = make_workload(args.workload, args.rows)
     if args.vector:
         import dataclasses
@@ -308,6 +387,16 @@ def main():
                 step()
         step = graph.replay   # replays on the current (timed) stream
         per_step = args.graph
+    # bring the GPU to its steady clock (it ramps over the first ~50 ms of back-to-back
+    # launches), then the W warmup steps
+    t_warm = time.perf_counter()
+    warm_launches = 0
+    while (time.perf_counter() - t_warm) * 1e3 < args.clock_warm_ms:
+        for _ in range(8):
+            step()
+        warm_launches += 8
+        torch.cuda.synchronize()
+    t_warm = time.perf_counter() - t_warm
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -404,14 +493,19 @@ def main():
             "traffic": measured_traffic(w.name, n),
             "what": "internal-node visits per second against the on-chip gather bound: each "
                     "visit needs 2 data-dependent per-lane LDS gathers (node, feature value); a "
-                    "CU's 32-bank LDS serves 32 lanes/clk; 256 CUs x 2.4 GHz. HBM is not the "
-                    "binding level (see hbm).",
+                    "CU's LDS serves 32 lanes/clk; 256 CUs x 2.4 GHz. The calibration object "
+                    "holds the gather rates measured on this device (conflict-free b32 and "
+                    "b64 gathers, which the kernels issue, stay below 32 lanes/clk). HBM is "
+                    "not the binding level (see hbm).",
         },
         "node_visits_per_s": visits_per_s,
         "visits_per_row": visits_per_row,
         "hbm": {"algorithmic_bytes": alg_bytes, "achieved_GBps": alg_bytes / s / 1e9,
                 "peak_GBps": HBM_PEAK_BYTES_PER_S / 1e9,
                 "frac": alg_bytes / s / HBM_PEAK_BYTES_PER_S},
+        "calibration": calib,
+        "clock_warm": {"ms": t_warm * 1e3, "launches": warm_launches,
+                       "note": "untimed launches before the warmup steps (clock ramp)"},
         "wall_s_timed_region": t_wall,
         "create_ms": create_s * 1e3,
         "launch_ms_median_of_20": float(np.median(one)),

@@ -17,8 +17,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "bridger.h")
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(bridger_\w+)\s*\(", text)))
 
@@ -33,6 +33,18 @@ def test_header_declares_the_entry_points():
 def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(B.LIB_PATH)
     missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_calibration_library_exports_its_symbols():
+    """include/bridger_calib.h is implemented by libbridger_calib.so; every header under
+    include/ is covered by one of the two libraries."""
+    headers = sorted(os.listdir(os.path.join(ROOT, "include")))
+    assert headers == ["bridger.h", "bridger_calib.h"]
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(B.LIB_PATH), "libbridger_calib.so"))
+    names = declared_functions(os.path.join(ROOT, "include", "bridger_calib.h"))
+    assert set(names) == {"bridger_calib_device", "bridger_calib_lds_gather", "bridger_calib_copy"}
+    missing = [n for n in names if not hasattr(lib, n)]
     assert not missing, missing
 
 
