@@ -82,7 +82,8 @@ enum {
   BRIDGER_CREATE_HOST_ONLY = 1u,
   /* Vector leaves (tree classifiers: decision, extra and random forests of
    * classification trees, whose leaves hold class probabilities; the aggregation
-   * category of Sec. 4.1): `value` holds n_classes floats per node, row-major
+   * category of the classical operator representation, Sec. 3.2 and Sec. 4.2, lowered
+   * to Table 4's sum/mean): `value` holds n_classes floats per node, row-major
    * [N, n_classes] (ignored at internal nodes), and every tree adds its leaf's
    * vector to all n_classes outputs, in ascending tree order per class.  MEAN
    * divides each class sum by n_trees (a random forest's averaged probabilities).
@@ -171,6 +172,8 @@ bridger_status bridger_forest_predict_noalloc(bridger_forest_t h, const float *X
  * Write, for every (row, tree), the id of the leaf the row reaches, in the
  * caller's tree-local node numbering: device int32 [n_rows, n_trees], row-major
  * (tree index in the caller's order).  Same arguments and rules as predict.
+ * This is the result of the comparison and conditional operators alone (Sec. 4.2;
+ * Table 4's less_equal and where, iterated by loop/while), before the aggregation.
  */
 bridger_status bridger_forest_predict_leaves(bridger_forest_t h, const float *X, int64_t n_rows,
                                              int32_t n_features, int32_t *out_leaf,
@@ -286,16 +289,18 @@ bridger_status bridger_forest_predict_csr_leaves(bridger_forest_t h, const int64
 bridger_status bridger_forest_predict_labels(bridger_forest_t h, const float *X, int64_t n_rows,
                                              int32_t n_features, int32_t *labels, void *stream);
 
-/* Shape facts.  Any output pointer may be NULL.  all_perfect = 1 when every tree
- * is perfect with one common depth (then max_depth is that depth). */
+/* Shape facts of the converted model (what the frontend handed over, Sec. 4.1).
+ * Any output pointer may be NULL.  all_perfect = 1 when every tree is perfect with
+ * one common depth (then max_depth is that depth). */
 bridger_status bridger_forest_info(bridger_forest_t h, int32_t *n_trees, int32_t *n_features,
                                    int32_t *n_outputs, int32_t *max_depth, int32_t *all_perfect);
 
-/* Select the kernel family (BRIDGER_KERNEL_*).  Returns BRIDGER_ERR_UNSUPPORTED
+/* Select the kernel family (BRIDGER_KERNEL_*): which generated code runs the lowered
+ * operators (the code generation step of Sec. 4.5).  Returns BRIDGER_ERR_UNSUPPORTED
  * (and keeps the current choice) when that family cannot evaluate this forest. */
 bridger_status bridger_forest_set_kernel(bridger_forest_t h, int32_t kernel);
 
-/* The kernel family predict will use (AUTO resolved). */
+/* The kernel family predict will use (AUTO resolved; Sec. 4.5's code generation). */
 bridger_status bridger_forest_get_kernel(bridger_forest_t h, int32_t *kernel);
 
 /*
@@ -311,7 +316,8 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
                                    double *stage_bytes, double *lds_read_bytes);
 
 /*
- * Read-only view of a host copy of the packed layout, for inspection and tests:
+ * Read-only view of a host copy of the packed layout (the node records after Table 2's
+ * data type rewriting and redundant operator elimination), for inspection and tests:
  * which = 0 node records of the active kernel family, 1 per-tree start offsets,
  * 2 leaf-id map (kernel leaf slot -> caller node id), 3 kernel tree order
  * (kernel position -> caller tree index), 4 chunk table, 5 the binning thresholds
@@ -321,10 +327,14 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
 bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
                                      int64_t *bytes);
 
-/* Free the handle and its device memory (device-synchronizing).  NULL is a no-op. */
+/* Free the handle and its device memory (device-synchronizing): the end of the
+ * runtime's hold on the converted model (Sec. 4.1).  NULL is a no-op. */
 void bridger_forest_destroy(bridger_forest_t h);
 
-/* Message for the calling thread's most recent failed call ("" if none). */
+/* Message for the calling thread's most recent failed call ("" if none).  The
+ * paper states no error interface; this is the library's own, so that nothing
+ * throws across the C ABI (thread-local storage, valid until the thread's next
+ * call into the library). */
 const char *bridger_last_error(void);
 
 #ifdef __cplusplus

@@ -6,7 +6,8 @@ import this module; the library never does and shares no code with it.
 Tree classifiers of the paper's CML suite (decision, extra and random forests of trees; its
 evaluation names ExtraTreeClassifier) store a class-probability vector in every leaf, and a
 forest of them averages the vectors of the leaves a row reaches (the aggregation category of
-the operator representation, Sec. 4.1; Table 1's sum/mean).  Written from that definition:
+the classical operator representation, Sec. 3.2 and Sec. 4.2; Table 4's sum/mean).  Written
+from that definition:
 
   leaf(r, t)  the leaf row r reaches in tree t (the scalar oracle's walk: left iff x <= t)
   acc[k]      = base[k] (SUM) or 0 (MEAN); then for t = 0, 1, ..., T-1 in turn

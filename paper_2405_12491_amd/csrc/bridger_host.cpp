@@ -733,10 +733,20 @@ void build_ragged_brec(bridger_forest *h) {
 }
 
 // ------------------------------------------------------------------- device io
+// Test hook: with BRIDGER_TEST_ALLOC_LIMIT=<bytes> in the environment, every device allocation
+// of the library larger than <bytes> fails as an exhausted device would (read at each
+// allocation), so that the out-of-memory paths of create, set_preprocess and the Normalizer's
+// scratch can be exercised.
+bool alloc_refused(size_t bytes) {
+  const char *v = std::getenv("BRIDGER_TEST_ALLOC_LIMIT");
+  if (!v || !*v) return false;
+  return bytes > (size_t)std::strtoull(v, nullptr, 10);
+}
+
 template <class T>
 bridger_status upload(void **dst, const std::vector<T> &src, size_t pad = 0) {
   const size_t bytes = src.size() * sizeof(T);
-  if (hipMalloc(dst, bytes + pad + 16) != hipSuccess) {
+  if (alloc_refused(bytes + pad + 16) || hipMalloc(dst, bytes + pad + 16) != hipSuccess) {
     *dst = nullptr;
     (void)hipGetLastError();
     return fail(BRIDGER_ERR_OUT_OF_MEMORY, "device allocation failed");
@@ -842,8 +852,9 @@ bridger_status prepare_row_norms(const bridger_forest *h, LaunchArgs &a, void *s
     a.row_norm = scratch;
     return BRIDGER_OK;
   }
-  if (hipMallocAsync((void **)&rn.p, (size_t)a.n_rows * sizeof(double), (hipStream_t)stream) !=
-      hipSuccess) {
+  if (alloc_refused((size_t)a.n_rows * sizeof(double)) ||
+      hipMallocAsync((void **)&rn.p, (size_t)a.n_rows * sizeof(double), (hipStream_t)stream) !=
+          hipSuccess) {
     (void)hipGetLastError();
     rn.p = nullptr;
     return fail(BRIDGER_ERR_OUT_OF_MEMORY, "no stream-ordered scratch for the row norms");
@@ -1425,7 +1436,10 @@ bridger_status bridger_forest_set_preprocess(bridger_forest_t h, int32_t kind, c
     if (!h->d_pre_a) {
       bridger_status s = upload(&h->d_pre_a, va);
       if (s != BRIDGER_OK) return s;
-      if ((s = upload(&h->d_pre_b, vb)) != BRIDGER_OK) return s;
+      if ((s = upload(&h->d_pre_b, vb)) != BRIDGER_OK) {
+        free_dev(h->d_pre_a);  // both or neither: a later call uploads both again
+        return s;
+      }
     } else if (hipMemcpy(h->d_pre_a, va.data(), 8 * va.size(), hipMemcpyHostToDevice) !=
                    hipSuccess ||
                hipMemcpy(h->d_pre_b, vb.data(), 8 * vb.size(), hipMemcpyHostToDevice) !=
