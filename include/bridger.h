@@ -322,7 +322,9 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
  * 2 leaf-id map (kernel leaf slot -> caller node id), 3 kernel tree order
  * (kernel position -> caller tree index), 4 chunk table, 5 the binning thresholds
  * (float, feature after feature, each ascending), 6 their per-feature offsets
- * (int32 [n_features + 1]).  *ptr stays valid until destroy or set_kernel.
+ * (int32 [n_features + 1]), 7 the ragged trees' top-level heaps (16 records per tree: the
+ * root's record index, then the records of the first four levels as a 1-based heap; absent
+ * when the plan does not use them).  *ptr stays valid until destroy or set_kernel.
  */
 bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
                                      int64_t *bytes);

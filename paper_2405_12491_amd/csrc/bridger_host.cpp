@@ -111,6 +111,7 @@ struct bridger_forest {
   std::vector<uint8_t> perfect_btrav;   // PERFECT traversal copy for bins: {rank, f * R * bytes}
   std::vector<uint32_t> perfect_broots;  // per tree: the binned copy's root record
   std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
+  std::vector<uint64_t> ragged_tops, ragged_btops;  // top-level heaps (fp32 / binned records)
   std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
 
   // fused preprocessing (BRIDGER_PRE_*)
@@ -136,7 +137,8 @@ struct bridger_forest {
   DevArrays d_perfect, d_ragged, d_direct;
   void *d_perfect_trav = nullptr, *d_perfect_roots = nullptr, *d_perfect_broots = nullptr;
   void *d_q_values = nullptr, *d_q_off = nullptr, *d_perfect_btrav = nullptr,
-       *d_ragged_brec = nullptr, *d_ragged_bchunk_first = nullptr,
+       *d_ragged_brec = nullptr, *d_ragged_bchunk_first = nullptr, *d_ragged_tops = nullptr,
+       *d_ragged_btops = nullptr,
        *d_ragged_bchunk_rec = nullptr;
   double visits_per_row_est = 0;  // for the model: mean internal visits per row (all trees)
 };
@@ -586,7 +588,18 @@ Plan choose_plan(const PlanInput &in) {
 // tile and the per-group class sums only; G lane groups split the trees; up to 16 waves per
 // workgroup (no staging wave).  Picks the most resident waves (every wave hides L2 round
 // trips), then fewer lane groups, then more rows per tile.
-Plan choose_global_plan(const PlanInput &in) {
+// Top levels of the RAGGED lockstep kernel read from LDS: 5 (4 trees per batch) measured at
+// least as fast as 4 (8 trees per batch) on the ragged forests, fp32 and binned, and 6 (2 trees
+// per batch) slower; BRIDGER_TOP_LEVELS=4 overrides.
+int top_levels_default() {
+  const int l = env_int("BRIDGER_TOP_LEVELS", kTopLevelsDefault);
+  return (l == 4 || l == 5) ? l : kTopLevelsDefault;
+}
+
+// tops: the RAGGED variant whose top levels come from per-wave LDS copies (one class, scalar
+// leaves, lane groups of whole waves): the LDS holds the row tile and kTopWaveBytes per wave,
+// which also take the group sums at the end.
+Plan choose_global_plan(const PlanInput &in, bool tops = false) {
   Plan best{};
   const int force_waves = env_int("BRIDGER_WAVES", 0);
   const int force_rows = env_int("BRIDGER_ROWS", 0);
@@ -600,7 +613,9 @@ Plan choose_global_plan(const PlanInput &in) {
       if (force_rows && R != force_rows) continue;
       const int G = 64 * W / R;
       if (G > 1 && (int64_t)G * 4 > in.n_trees) continue;  // a few trees per lane group
-      const int64_t lds = (int64_t)in.F * R * in.x_bytes + (int64_t)in.K * G * R * 8;
+      if (tops && R < 64) continue;                        // a group is whole waves
+      const int64_t lds = (int64_t)in.F * R * in.x_bytes +
+                          (tops ? (int64_t)W * kTopWaveBytes : (int64_t)in.K * G * R * 8);
       if (lds > kLdsBytesPerCU) continue;
       const int m = (int)std::min<int64_t>(kLdsBytesPerCU / lds, kMaxWavesPerCU / W);
       if (m < 1) continue;
@@ -612,6 +627,7 @@ Plan choose_global_plan(const PlanInput &in) {
       p.acc_in_lds = 1;
       p.ilp = env_int("BRIDGER_ILP", 8) == 4 ? 4 : 8;  // L2 round trips: keep 8 in flight
       p.global_nodes = 1;
+      p.tops = tops ? top_levels_default() : 0;
       p.waves_per_cu = m * W;
       const double n = (double)std::max<int64_t>(in.n_rows, 1);
       p.hbm_bytes = n * in.F * 4 + n * in.K * 4 + in.forest_bytes;
@@ -654,6 +670,16 @@ Plan pick_plan(const PlanInput &pin) {
   if (!pin.perfect) {  // trees walked at once per lane (8: 3% faster than 4 on ragged forests)
     const int u = env_int("BRIDGER_ILP", 8);
     g.ilp = (u == 1 || u == 2 || u == 4) ? u : 8;
+    // one class with scalar leaves: the top levels from per-wave LDS copies when that keeps as
+    // many resident waves (BRIDGER_TOPS=0 turns it off)
+    if (pin.K == 1 && !pin.vec && pin.forest_bytes < 2147483648.0 &&
+        env_int("BRIDGER_TOPS", 1) != 0 && !env_int("BRIDGER_ILP", 0)) {
+      Plan t = choose_global_plan(pin, true);
+      if (t.waves && t.waves_per_cu >= g.waves_per_cu) {
+        t.ilp = top_batch(t.tops);
+        g = t;
+      }
+    }
   }
   // Ragged trees: the global-node kernel, whose lanes walk their trees in lockstep with no
   // barrier inside the walk, measured as fast or faster than the LDS-chunked state machine on
@@ -732,6 +758,33 @@ void build_ragged_brec(bridger_forest *h) {
   }
 }
 
+// Top-level heaps of the RAGGED trees (layout in internal.h): per kernel tree the records of its
+// first L levels at heap slots 1 .. 2^L - 1 (copies of the packed records `rec`, found by
+// following each internal record's left_rel), slot 0 the root's record index; slots under a
+// leaf, and top_batch(L) trailing trees, hold a leaf record.
+void build_ragged_tops(const std::vector<uint64_t> &rec, const std::vector<int32_t> &start,
+                       int32_t n_trees, int L, std::vector<uint64_t> &tops) {
+  const uint64_t leaf = (uint64_t)kLeafFlag << 32;
+  const int slots = 1 << L;
+  tops.assign((size_t)(n_trees + top_batch(L)) * slots, leaf);
+  std::vector<int64_t> idx(slots);
+  for (int32_t k = 0; k < n_trees; ++k) {
+    uint64_t *t = &tops[(size_t)k * slots];
+    t[0] = (uint64_t)(uint32_t)start[k];
+    idx[1] = start[k];
+    for (int m = 2; m < slots; ++m) idx[m] = -1;
+    for (int m = 1; m < slots; ++m) {
+      if (idx[m] < 0) continue;
+      t[m] = rec[idx[m]];
+      const uint32_t meta = (uint32_t)(rec[idx[m]] >> 32);
+      if (2 * m + 1 < slots && !(meta & (uint32_t)kLeafFlag)) {
+        idx[2 * m] = idx[m] + (meta & (uint32_t)kMaxRel);
+        idx[2 * m + 1] = idx[2 * m] + 1;
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------- device io
 // Test hook: with BRIDGER_TEST_ALLOC_LIMIT=<bytes> in the environment, every device allocation
 // of the library larger than <bytes> fails as an exhausted device would (read at each
@@ -771,7 +824,8 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_perfect_trav);
   free_dev(h->d_perfect_roots);
   free_dev(h->d_perfect_broots);
-  for (void **q : {&h->d_q_values, &h->d_q_off, &h->d_perfect_btrav, &h->d_ragged_brec,
+  for (void **q : {&h->d_ragged_tops, &h->d_ragged_btops, &h->d_q_values, &h->d_q_off,
+                   &h->d_perfect_btrav, &h->d_ragged_brec,
                    &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b,
                    &h->d_vec_perfect, &h->d_vec_ragged, &h->d_vec_direct})
     free_dev(*q);
@@ -802,6 +856,8 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_ragged.chunk_first, h->ragged_chunk_first)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_ragged.chunk_rec, h->ragged_chunk_rec)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_ragged.leaf_map, h->ragged_rec_node)) != BRIDGER_OK) return s;
+    if (!h->ragged_tops.empty() && (s = upload(&h->d_ragged_tops, h->ragged_tops)) != BRIDGER_OK)
+      return s;
   }
   if (h->bin_bytes) {
     if ((s = upload(&h->d_q_values, h->q_values)) != BRIDGER_OK) return s;
@@ -815,6 +871,9 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_ragged_brec, h->ragged_brec, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_ragged_bchunk_first, h->ragged_bchunk_first)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_ragged_bchunk_rec, h->ragged_bchunk_rec)) != BRIDGER_OK) return s;
+    if (!h->ragged_btops.empty() &&
+        (s = upload(&h->d_ragged_btops, h->ragged_btops)) != BRIDGER_OK)
+      return s;
   }
   if ((s = upload(&h->d_direct.nodes, h->direct_rec)) != BRIDGER_OK) return s;
   if ((s = upload(&h->d_direct.tree_start, h->direct_root)) != BRIDGER_OK) return s;
@@ -994,7 +1053,13 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
       err = launch_perfect_fixed(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else if (h->kernel_active == kPerfect)
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
-    else if (p.global_nodes)
+    else if (p.global_nodes && p.tops) {
+      a.tops = (const uint64_t *)(binned ? h->d_ragged_btops : h->d_ragged_tops);
+      a.nodes_bytes = (uint32_t)(8 * h->ragged_rec.size());
+      a.top_levels = p.tops;
+      a.lds_top_off = h->F * p.rows_per_wg * xsz;
+      err = launch_ragged_top(a, p.waves, n_wg, p.lds_bytes, stream);
+    } else if (p.global_nodes)
       err = launch_ragged_global(a, p.waves, n_wg, p.lds_bytes, stream);
     else
       err = launch_ragged(a, p.waves, n_wg, p.lds_bytes, stream);
@@ -1225,6 +1290,9 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       if (h->ragged_ok && !h->ragged_plan.global_nodes)
         h->ragged_plan.n_chunks = ragged_chunks(h, h->ragged_plan.chunk_bytes,
                                                 h->ragged_chunk_first, h->ragged_chunk_rec);
+      if (h->ragged_ok && h->ragged_plan.tops)
+        build_ragged_tops(h->ragged_rec, h->ragged_tree_start, h->n_trees, h->ragged_plan.tops,
+                          h->ragged_tops);
     }
     // binned variants of the same layouts (used by bridger_forest_predict_binned)
     if (build_quantization(h, feature, threshold, left)) {
@@ -1245,6 +1313,9 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         h->ragged_bok = h->ragged_bplan.waves > 0;
         if (h->ragged_bok) {
           build_ragged_brec(h);
+          if (h->ragged_bplan.tops)
+            build_ragged_tops(h->ragged_brec, h->ragged_tree_start, h->n_trees,
+                              h->ragged_bplan.tops, h->ragged_btops);
           if (!h->ragged_bplan.global_nodes)
             h->ragged_bplan.n_chunks = ragged_chunks(h, h->ragged_bplan.chunk_bytes,
                                                      h->ragged_bchunk_first, h->ragged_bchunk_rec);
@@ -1567,6 +1638,8 @@ bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const vo
       if (which == 1) return give(h->ragged_tree_start.data(), h->ragged_tree_start.size() * 4);
       if (which == 2) return give(h->ragged_rec_node.data(), h->ragged_rec_node.size() * 4);
       if (which == 4) return give(h->ragged_chunk_first.data(), h->ragged_chunk_first.size() * 4);
+      if (which == 7 && !h->ragged_tops.empty())
+        return give(h->ragged_tops.data(), h->ragged_tops.size() * 8);
       break;
     default:
       if (which == 0) return give(h->direct_rec.data(), h->direct_rec.size() * 4);

@@ -27,6 +27,11 @@
 //     leaf    : w = value bits,     meta = 0x8000 | next_rel           (next_rel = records to the
 //               next tree's root, i.e. to the end of this tree)
 //   Trees are grouped into chunks of at most chunk_bytes; a chunk is staged to LDS whole.
+//   Top levels (for the lockstep kernel with one tree per wave in every slot), L = 4 or 5: per
+//   kernel tree 2^L records of 8 bytes, a 1-based heap of the tree's first L levels (slot 1 the
+//   root, the children of slot m at 2m and 2m + 1, each a copy of the node's packed record;
+//   slots under a leaf hold a leaf record) with slot 0 holding the root's record index in its
+//   low word; then top_batch(L) empty trees, so that a batch copy never reads past the end.
 //
 // DIRECT (any forest): 16-byte records {float w; int32 feature (-1 at a leaf); int32 left;
 //   int32 right} with absolute record indices; kernel tree t starts at record root[t].
@@ -40,6 +45,12 @@ constexpr int kLdsBytesPerCU = 163840;
 constexpr int kLeafFlag = 0x8000;
 constexpr int kMaxRel = 0x7FFF;
 constexpr int kMaxRaggedFeatures = 0xFFFF;
+// RAGGED top-level heaps: a wave's LDS copy holds one batch of top_batch(L) trees' heaps, 1 KB
+// (one 16-byte load per lane); L top levels per tree.
+constexpr int kTopWaveBytes = 1024;
+constexpr int kTopLevelsDefault = 5;
+constexpr int top_bytes(int L) { return 8 << L; }
+constexpr int top_batch(int L) { return kTopWaveBytes / top_bytes(L); }
 // Rows per dispatch: every launch shape then stays far below the 32-bit work-item count of a
 // dispatch; predictions over more rows are issued as several launches.
 constexpr int64_t kMaxRowsPerLaunch = int64_t(1) << 24;
@@ -78,6 +89,9 @@ struct Plan {
   int32_t global_nodes;    // records read from global memory, LDS holds only the tile
   int32_t waves_per_cu;    // resident compute waves per CU
   int32_t acc_alias;       // class sums written after the walk into the row tile's LDS
+  int32_t tops;            // RAGGED global: 0, or L, the top levels read from a per-wave LDS
+                           // copy (after the row tile, kTopWaveBytes per wave, which then
+                           // holds the group sums)
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
 };
 
@@ -130,6 +144,10 @@ struct LaunchArgs {
   const double *row_norm;      // NORMALIZE: each row's L2 norm in double (1 for a zero row)
   int32_t vec;                 // vector leaves: K class values per leaf in leaf_vec
   const float *leaf_vec;       // [leaf index][vec_stride(K)], as the family numbers leaves
+  const uint64_t *tops;        // RAGGED top-level heaps ([n_trees + top_batch(L)][2^L])
+  int32_t top_levels;          // L
+  uint32_t nodes_bytes;        // bytes of `nodes` (RAGGED top-level kernel: < 2^31)
+  int32_t lds_top_off;         // byte offset of the per-wave top-level copies in dynamic LDS
 };
 
 // Vector leaves: floats per leaf in leaf_vec, K rounded up to whole 16-byte groups.
@@ -152,6 +170,7 @@ int launch_perfect_fixed(int depth, const LaunchArgs &a, int waves, int64_t n_wg
 int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
 int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                          void *stream);
+int launch_ragged_top(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
 int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream);
 int launch_gemm(int depth, const LaunchArgs &a, int64_t n_wg, void *stream);
 

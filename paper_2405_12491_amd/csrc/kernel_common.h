@@ -36,6 +36,9 @@ namespace bridger {
 
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
 
+// Fourth word of a raw (untyped, unswizzled) buffer resource on gfx9-family CDNA parts.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+
 // The kernels declare no static LDS, so dynamic LDS starts at LDS address 0 and a byte
 // offset into it is directly an LDS address (no base add on every access).
 __device__ __forceinline__ float lds_f32(const uint8_t *, uint32_t addr) {

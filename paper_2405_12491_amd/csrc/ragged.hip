@@ -232,7 +232,191 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   }
 }
 
+// The same lockstep walk for one output class with scalar leaves (or leaf ids), when every
+// lane group is a whole number of waves (R >= 64): all lanes of a wave then walk the same
+// batch of U = top_batch(L) trees, so each tree's first L levels come from a per-wave LDS copy
+// of the trees' top-level heaps (layout in internal.h) instead of one wave-wide global load per
+// level.  One 16-byte-per-lane global->LDS load copies a whole batch's heaps (1 KB); the next
+// batch's copy is issued as soon as the current batch has left its top levels, so it lands
+// while the deeper levels are walked.  The texture addresser, which resolves every wave-wide
+// global load and bounds the walk, sees L fewer loads per tree.  A batch is always U slots;
+// slots past the group's last tree start at a leaf and are never added.  Leaves are added in
+// tree order; the G groups' partial sums meet in the waves' copy buffers at the end.
+template <bool LEAVES, int XB, int L>
+__global__ __launch_bounds__(1024) void ragged_top_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr int U = top_batch(L);
+  constexpr int kTopLevels = L;
+  constexpr uint32_t kTopBytes = (uint32_t)top_bytes(L);
+  const int tid = threadIdx.x;
+  const int R = a.rows_per_wg, G = a.groups;
+  const int r = tid & (R - 1);
+  const int g = __builtin_amdgcn_readfirstlane(tid / R);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
+  const int shift = a.log2_row_bytes;
+  const int T = a.n_trees;
+  const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * kTopWaveBytes;
+
+  load_tile_any<XB, false>(smem, a, r, row, row_ok, g, G);
+  __syncthreads();
+
+  const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
+  const uint8_t *tops = reinterpret_cast<const uint8_t *>(a.tops);
+  const uint8_t *recs = a.nodes;
+  // the heaps of trees q .. q + U - 1 (one 16-byte load per lane) into this wave's buffer
+  auto copy_tops = [&](int q) {
+    __builtin_amdgcn_global_load_lds(
+        (const void *)(tops + (size_t)q * kTopBytes + (size_t)lane * 16),
+        (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf), 16, 0, 0);
+  };
+  // record i through a buffer resource: a 32-bit byte offset (one shift per load), and a read
+  // outside the records returns zeros instead of faulting
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)recs, (short)0, (int)a.nodes_bytes, kBufferRsrcWord3);
+  auto load_rec = [&](uint32_t i) {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rsrc, i * 8u, 0, 0);
+    return make_uint2(v.x, v.y);
+  };
+  double acc = (!LEAVES && a.aggregate == 0 && g == 0) ? (double)a.base[0] : 0.0;
+  if (ga < gb) copy_tops(ga);
+  for (int q = ga; q < gb; q += U) {
+    const int nvalid = gb - q < U ? gb - q : U;
+    wait_stage();  // this batch's heaps have landed
+    uint32_t idx[U], m[U];
+    uint2 rec[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t tb = buf + (uint32_t)u * kTopBytes;
+      idx[u] = lds_u64(smem, tb).x;
+      rec[u] = u < nvalid ? lds_u64(smem, tb + 8) : make_uint2(0u, (uint32_t)kLeafFlag);
+      m[u] = 1u;
+    }
+    // levels 0 .. kTopLevels - 1: every record from the copy, the last level's children from
+    // global memory
+    // One level of all U slots: gather every slot's feature value (a slot at a leaf reads
+    // feature 0 harmlessly), then step the slots that sit on an internal node.  Returns
+    // whether any slot of this lane was internal.
+    bool inner[U];
+    auto step = [&]() {
+      bool any = false;
+      uint32_t xv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        xv[u] = gather_x<false, XB>(smem, ((rec[u].y >> 16) << shift) + lane_off);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        // branch-free: keep = all ones on an internal node, zero at a leaf
+        const uint32_t meta = rec[u].y;
+        const uint32_t keep = ((meta >> 15) & 1u) - 1u;
+        inner[u] = keep != 0u;
+        any = any || inner[u];
+        const uint32_t right = (goes_right<XB>(xv[u], rec[u].x) ? 1u : 0u) & keep;
+        idx[u] += ((meta & (uint32_t)kMaxRel) + right) & keep;
+        m[u] += (m[u] + right) & keep;
+      }
+      return any;
+    };
+    // levels 0 .. kTopLevels - 2 read the next record from the copy (slots at a leaf re-read
+    // their own); the last top level reads the children from global memory
+    bool live = true;
+#pragma unroll
+    for (int level = 0; level + 1 < kTopLevels; ++level) {
+      if (live) {
+        live = step();
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          rec[u] = lds_u64(smem, buf + (uint32_t)u * kTopBytes + 8u * m[u]);
+      }
+    }
+    if (live) {
+      live = step();
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (inner[u]) rec[u] = load_rec(idx[u]);
+    }
+    // the top levels are read: the next batch's heaps can land while the deeper levels run
+    if (q + U < gb) copy_tops(q + U);
+    // deeper levels: a slot whose lanes all sit at leaves skips its work (the branch is taken
+    // on the slot's own lane mask), so a finished tree costs neither loads nor arithmetic
+    // validated trees are at most 64 deep; the bound keeps the loop finite regardless
+    for (int level = kTopLevels; live && level <= 64; ++level) {
+      bool any = false;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        inner[u] = (rec[u].y & (uint32_t)kLeafFlag) == 0;
+        any = any || inner[u];
+      }
+      if (!any) break;
+      uint32_t xv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        xv[u] = gather_x<false, XB>(smem, ((rec[u].y >> 16) << shift) + lane_off);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (inner[u]) {
+          idx[u] += (rec[u].y & (uint32_t)kMaxRel) + (goes_right<XB>(xv[u], rec[u].x) ? 1u : 0u);
+          rec[u] = load_rec(idx[u]);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u < nvalid) {
+        if (LEAVES) {
+          if (row_ok) a.out_leaf[row * (int64_t)T + a.tree_order[q + u]] = a.leaf_map[idx[u]];
+        } else {
+          acc += (double)__uint_as_float(rec[u].x);
+        }
+      }
+    }
+  }
+  if (LEAVES) return;
+  // group sums: each thread's partial in its own wave's copy buffer (free once no copy is in
+  // flight), then group 0 adds the groups' partials of its row in group order
+  wait_stage();
+  auto slot = [&](int t) {
+    return reinterpret_cast<double *>(smem + a.lds_top_off + (t >> 6) * kTopWaveBytes +
+                                      (t & 63) * 8);
+  };
+  *slot(tid) = acc;
+  __syncthreads();
+  if (g == 0 && row_ok) {
+    double z = *slot(r);
+    for (int gg = 1; gg < G; ++gg) z += *slot(gg * R + r);
+    if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
+    store_one(a, row, z);
+  }
+}
+
 // ---------------------------------------------------------------------- launchers
+template <int XB, int L>
+static int launch_ragged_top_xl(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                                void *stream) {
+  const int threads = 64 * waves;
+  if (a.out_leaf)
+    return launch_common(ragged_top_kernel<true, XB, L>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_top_kernel<false, XB, L>, threads, n_wg, lds_bytes, stream, a);
+}
+
+template <int XB>
+static int launch_ragged_top_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                               void *stream) {
+  if (a.top_levels == 5) return launch_ragged_top_xl<XB, 5>(a, waves, n_wg, lds_bytes, stream);
+  if (a.top_levels == 4) return launch_ragged_top_xl<XB, 4>(a, waves, n_wg, lds_bytes, stream);
+  return (int)hipErrorInvalidValue;
+}
+
+int launch_ragged_top(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {
+  if (a.x_bytes == 2) return launch_ragged_top_x<2>(a, waves, n_wg, lds_bytes, stream);
+  if (a.x_bytes == 1) return launch_ragged_top_x<1>(a, waves, n_wg, lds_bytes, stream);
+  return launch_ragged_top_x<4>(a, waves, n_wg, lds_bytes, stream);
+}
+
 template <int XB, int U>
 static int launch_ragged_global_xu(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                                    void *stream) {

@@ -252,6 +252,50 @@ def walk_ragged(f: B.Forest, X):
     return leaves, vals
 
 
+def has_tops(f: B.Forest) -> bool:
+    try:
+        B.bridger_forest_packed(f.handle, 7, np.uint32)
+        return True
+    except B.BridgerError:
+        return False
+
+
+def walk_ragged_tops(f: B.Forest, X):
+    """The lockstep kernel's walk: levels 0-3 from the top-level heaps (slot 0 the root's record
+    index, slot m's children at 2m and 2m + 1), deeper levels from the packed records.  Every
+    heap record must equal the packed record at the index the walk tracks."""
+    rec = B.bridger_forest_packed(f.handle, 0, np.uint32).reshape(-1, 2)
+    tops = B.bridger_forest_packed(f.handle, 7, np.uint32).reshape(-1, 2)
+    rec_node = B.bridger_forest_packed(f.handle, 2, np.int32)
+    order = B.bridger_forest_packed(f.handle, 3, np.int32)
+    T = f.n_trees
+    # L top levels: 2^L records per tree, then 1024 / (8 * 2^L) empty trees
+    L = [l for l in (4, 5) if tops.shape[0] == (T + 1024 // (8 << l)) << l]
+    assert len(L) == 1
+    L = L[0]
+    tops = tops.reshape(-1, 1 << L, 2)
+    assert np.all(tops[T:, 1:, 1] == 0x8000)
+    leaves = np.empty((X.shape[0], T), np.int32)
+    rows = np.arange(X.shape[0])
+    for k in range(T):
+        a = np.full(X.shape[0], tops[k, 0, 0], np.int64)
+        m = np.ones(X.shape[0], np.int64)
+        r = tops[k, 1][None, :].repeat(X.shape[0], 0)
+        for level in range(70):
+            assert np.array_equal(r, rec[a])
+            meta = r[:, 1]
+            leaf = (meta & 0x8000) != 0
+            if leaf.all():
+                break
+            feat = (meta >> 16).astype(np.int64)
+            right = (~(X[rows, feat] <= r[:, 0].view(np.float32)) & ~leaf).astype(np.int64)
+            a = np.where(leaf, a, a + (meta & 0x7FFF) + right)
+            m = np.where(leaf, m, 2 * m + right)
+            r = tops[k][m] if level + 1 < L else rec[a]
+        leaves[:, order[k]] = rec_node[a]
+    return leaves
+
+
 def walk_direct(f: B.Forest, X):
     rec = B.bridger_forest_packed(f.handle, 0, np.int32).reshape(-1, 4)
     root = B.bridger_forest_packed(f.handle, 1, np.int32)
@@ -288,9 +332,31 @@ def test_packed_layouts_reproduce_oracle_leaves(name):
                 lv, _ = walk_perfect(f, w.forest, X)
             elif k == B.BRIDGER_KERNEL_RAGGED:
                 lv, _ = walk_ragged(f, X)
+                if has_tops(f):
+                    assert np.array_equal(walk_ragged_tops(f, X), ref_lv), name
             else:
                 lv = walk_direct(f, X)
             assert np.array_equal(lv, ref_lv), (name, k)
+
+
+@pytest.mark.parametrize("levels", ["4", "5"])
+@pytest.mark.parametrize("seed", range(6))
+def test_ragged_top_heaps(seed, levels, monkeypatch):
+    """Random ragged one-class forests (leaves at every top level, single-leaf trees, trees
+    shallower than the heap) get top-level heaps, and walking them reproduces the oracle."""
+    monkeypatch.setenv("BRIDGER_TOP_LEVELS", levels)
+    rng = np.random.default_rng(100 + seed)
+    F = int(rng.integers(1, 9))
+    model = random_tiny_forest(rng, int(rng.integers(1, 40)), F, max_depth=int(rng.integers(0, 9)),
+                               p_split=float(rng.uniform(0.3, 0.95)), thr_grid=[-1.0, 0.0, 0.5, 1.0])
+    model = permute_nodes(model, rng)
+    X = rng.choice(np.array([-1.0, 0.0, 0.5, 1.0, 2.0, np.nan], np.float32), (64, F))
+    _, ref_lv, _ = oracle.predict(model, X, want_leaves=True)
+    with host(model) as f:
+        if f.kernel != B.BRIDGER_KERNEL_RAGGED:
+            f.kernel = B.BRIDGER_KERNEL_RAGGED
+        assert has_tops(f)
+        assert np.array_equal(walk_ragged_tops(f, X), ref_lv)
 
 
 def test_packed_layouts_permuted_and_classes():
