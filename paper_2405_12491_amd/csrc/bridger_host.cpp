@@ -437,6 +437,7 @@ struct PlanInput {
   double visits_per_row;
   int32_t x_bytes = 4;     // element of the LDS tile: 4 (fp32) or 2 / 1 (bins)
   bool vec = false;        // vector leaves
+  int32_t depth = 0;       // PERFECT: the trees' depth
 };
 
 // Smallest tile: bins pack 4 / x_bytes rows per 32-bit word and a half-wave's 32 rows must
@@ -596,6 +597,14 @@ int top_levels_default() {
   return (l == 4 || l == 5) ? l : kTopLevelsDefault;
 }
 
+// Top levels of the PERFECT global-node kernel read from LDS: 3 (16 trees per lane: 0.629 ms
+// on the 10-class 784-feature forest) or 4 (8 trees per lane: 0.685 ms; 2 levels with 32
+// trees per lane spill registers); BRIDGER_PERFECT_TOP_LEVELS overrides.
+int perfect_top_levels() {
+  const int l = env_int("BRIDGER_PERFECT_TOP_LEVELS", kPerfectTopLevels);
+  return (l == 3 || l == 4) ? l : kPerfectTopLevels;
+}
+
 // tops: the RAGGED variant whose top levels come from per-wave LDS copies (one class, scalar
 // leaves, lane groups of whole waves): the LDS holds the row tile and kTopWaveBytes per wave,
 // which also take the group sums at the end.
@@ -613,9 +622,14 @@ Plan choose_global_plan(const PlanInput &in, bool tops = false) {
       if (force_rows && R != force_rows) continue;
       const int G = 64 * W / R;
       if (G > 1 && (int64_t)G * 4 > in.n_trees) continue;  // a few trees per lane group
-      if (tops && R < 64) continue;                        // a group is whole waves
-      const int64_t lds = (int64_t)in.F * R * in.x_bytes +
-                          (tops ? (int64_t)W * kTopWaveBytes : (int64_t)in.K * G * R * 8);
+      if (tops && !in.perfect && R < 64) continue;         // a group is whole waves
+      // PERFECT top levels: 1 KB per lane group of each wave (a wave holds 64 / R groups when
+      // R < 64), besides the class sums
+      const int64_t top_bytes_wg =
+          !tops ? 0 : in.perfect ? (int64_t)W * std::max(1, 64 / R) * 1024
+                                 : (int64_t)W * kTopWaveBytes;
+      const int64_t lds = (int64_t)in.F * R * in.x_bytes + top_bytes_wg +
+                          (tops && !in.perfect ? 0 : (int64_t)in.K * G * R * 8);
       if (lds > kLdsBytesPerCU) continue;
       const int m = (int)std::min<int64_t>(kLdsBytesPerCU / lds, kMaxWavesPerCU / W);
       if (m < 1) continue;
@@ -627,7 +641,7 @@ Plan choose_global_plan(const PlanInput &in, bool tops = false) {
       p.acc_in_lds = 1;
       p.ilp = env_int("BRIDGER_ILP", 8) == 4 ? 4 : 8;  // L2 round trips: keep 8 in flight
       p.global_nodes = 1;
-      p.tops = tops ? top_levels_default() : 0;
+      p.tops = !tops ? 0 : in.perfect ? perfect_top_levels() : top_levels_default();
       p.waves_per_cu = m * W;
       const double n = (double)std::max<int64_t>(in.n_rows, 1);
       p.hbm_bytes = n * in.F * 4 + n * in.K * 4 + in.forest_bytes;
@@ -687,6 +701,16 @@ Plan pick_plan(const PlanInput &pin) {
   // and every chunk's barrier waits for its deepest path); a forest larger than L2 would
   // moreover be restaged from memory for every row tile.
   if (!pin.perfect) return g;
+  // PERFECT trees deeper than the copied levels, scalar leaves, eight trees per lane: the top
+  // levels from per-wave LDS copies when that keeps as many resident waves
+  if (!pin.vec && pin.depth > perfect_top_levels() && g.ilp == 8 &&
+      env_int("BRIDGER_TOPS", 1) != 0) {
+    Plan t = choose_global_plan(pin, true);
+    if (t.waves && t.waves_per_cu >= g.waves_per_cu) {
+      t.ilp = 1024 / (8 << t.tops);
+      g = t;
+    }
+  }
   const bool few = p.waves == 0 || p.waves_per_cu < kMinWavesPerCU;
   const bool fits = pin.forest_bytes <= kL2BytesPerXcd;
   if (gmode == 1 || (few && fits && g.waves_per_cu > p.waves_per_cu)) return g;
@@ -1047,8 +1071,13 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
                        perfect_fixed_ok(h->perfect_depth, p.trees_per_chunk) &&
                        p.chunk_bytes == p.trees_per_chunk * h->perfect_tree_bytes &&
                        h->fixed_chunks;
-    if (h->kernel_active == kPerfect && p.global_nodes)
+    if (h->kernel_active == kPerfect && p.global_nodes) {
+      if (p.tops) {  // after the row tile and the class sums
+        a.top_levels = p.tops;
+        a.lds_top_off = a.lds_acc_off + h->K * p.groups * p.rows_per_wg * 8;
+      }
       err = launch_perfect_global(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
+    }
     else if (fixed)
       err = launch_perfect_fixed(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else if (h->kernel_active == kPerfect)
@@ -1276,6 +1305,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       PlanInput pin{1 << 20, n_features, n_classes, n_trees,
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
       pin.vec = vec;
+      pin.depth = D;
       h->perfect_plan = pick_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
       if (h->perfect_ok) build_perfect_trav(h);
@@ -1300,6 +1330,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         PlanInput pin{1 << 20, n_features, n_classes, n_trees, (double)h->perfect_blob.size(),
                       h->perfect_tree_bytes, true, visits, h->bin_bytes};
         pin.vec = vec;
+        pin.depth = D;
         h->perfect_bplan = pick_plan(pin);
         h->perfect_bok = h->perfect_bplan.waves > 0;
         if (h->perfect_bok) build_perfect_btrav(h);

@@ -13,8 +13,11 @@
 namespace bridger {
 
 // VK: 0 scalar leaves; 4 or 8 (K <= VK) or 64 vector leaves (class sums in registers / LDS).
-template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0>
+// TL: 0, or the number of top levels read from per-wave LDS copies (scalar leaves only).
+template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0>
 __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
+  static_assert(TL == 0 || (VK == 0 && U * (8 << TL) == 1024 && TL < D),
+                "top levels: scalar leaves, one lane group's batch in 1 KB");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
   constexpr int VR = VK_REG ? VK : 4;
@@ -75,16 +78,105 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
     }
   };
 
-  int q = t_begin;
-  for (; q + U <= t_end; q += U) {
-    uint32_t m[U];
-    walk_trees_global<D, U, FIN, XB>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
-    finish(m, q);
-  }
-  for (; q < t_end; ++q) {
-    uint32_t m[1];
-    walk_trees_global<D, 1, FIN, XB>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
-    finish(m, q);
+  if constexpr (TL > 0) {
+    // Top levels from LDS: every wave copies the first TL levels (records of heap slots 1 ..
+    // 2^TL - 1, 8 << TL bytes from the start of each tree block) of the next U trees of each of
+    // its lane groups into its own LDS buffer with 16-byte global->LDS loads (1 KB per
+    // instruction), issued as soon as the current batch has left its top levels.  The batch
+    // loop is wave-uniform: batch j covers trees t_begin + jU .. + U - 1 of every group, slots
+    // past a group's last tree walk that tree again and are not added.
+    constexpr uint32_t TBT = 8u << TL;  // bytes of one tree's top levels
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int gpw = R < 64 ? 64 / R : 1;              // lane groups per wave
+    const int gi = R < 64 ? lane / R : 0;             // this lane's group within the wave
+    const int gw0 = __builtin_amdgcn_readfirstlane((wave * 64) / R);  // the wave's first group
+    const uint32_t wave_bytes = (uint32_t)gpw * U * TBT;
+    const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * wave_bytes;
+    static_assert(U * TBT == 1024, "one lane group's batch is one 16-byte-per-lane load");
+    const int NB = ((T + G - 1) / G + U - 1) / U;     // batches of the largest group
+    // the tree ranges of the wave's (at most two) lane groups
+    int cb0[2], cb1[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int gc = gw0 + (i < gpw ? i : 0);
+      cb0[i] = (int)(((int64_t)T * gc) / G);
+      cb1[i] = (int)(((int64_t)T * (gc + 1)) / G);
+    }
+    constexpr int LPT = (int)TBT / 16;                 // lanes per tree of the copy
+    const int cu = lane / LPT;                         // tree of the batch this lane copies
+    const uint32_t cpos = (uint32_t)(lane % LPT) * 16; // and its 16 bytes of that tree's levels
+    auto copy_batch = [&](int j) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        if (i < gpw) {
+          const int t = min(cb0[i] + j * U + cu, cb1[i] - 1);
+          __builtin_amdgcn_global_load_lds(
+              (const void *)(a.nodes + (size_t)t * tb + cpos),
+              (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf + i * 1024u), 16,
+              0, 0);
+        }
+      }
+    };
+    copy_batch(0);
+    for (int j = 0; j < NB; ++j) {
+      const int q = t_begin + j * U;
+      wait_stage();  // this batch's top levels have landed
+      uint32_t m[U];
+      size_t base[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        m[u] = 1u;
+        base[u] = (size_t)min(q + u, t_end - 1) * tb;
+      }
+      const uint32_t lbuf = buf + (uint32_t)gi * U * TBT;
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        uint2 rec[U];
+        uint32_t xv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          rec[u] = d < TL ? lds_u64(smem, lbuf + (uint32_t)u * TBT + (m[u] << 3))
+                          : *reinterpret_cast<const uint2 *>(a.nodes + base[u] + (m[u] << 3));
+#pragma unroll
+        for (int u = 0; u < U; ++u) xv[u] = gather_x<FIN, XB>(smem, rec[u].y + lane_off);
+#pragma unroll
+        for (int u = 0; u < U; ++u) m[u] = step_slot<FIN, XB>(m[u], rec[u].x, xv[u]);
+        if (d == TL - 1 && j + 1 < NB) copy_batch(j + 1);
+      }
+      if (LEAVES) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (row_ok && q + u < t_end)
+            a.out_leaf[row * (int64_t)T + a.tree_order[q + u]] =
+                a.leaf_map[(int64_t)(q + u) * (1 << D) + (m[u] - kFirstLeaf)];
+        }
+      } else {
+        float lv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          lv[u] = *reinterpret_cast<const float *>(a.nodes + base[u] + kLeafOff + (m[u] << 2));
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (q + u < t_end) {
+            class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+            ca.acc += (double)lv[u];
+          }
+        }
+      }
+    }
+  } else {
+    int q = t_begin;
+    for (; q + U <= t_end; q += U) {
+      uint32_t m[U];
+      walk_trees_global<D, U, FIN, XB>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
+      finish(m, q);
+    }
+    for (; q < t_end; ++q) {
+      uint32_t m[1];
+      walk_trees_global<D, 1, FIN, XB>(smem, a.nodes, (size_t)q * tb, tb, lane_off, m);
+      finish(m, q);
+    }
   }
   if (LEAVES) return;
   if (VK_REG) {
@@ -109,6 +201,24 @@ template <int D, bool FIN, int XB>
 static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                              void *stream) {
   const int threads = 64 * waves;
+  if constexpr (D > 4) {
+    if (a.top_levels == 4 && !a.vec) {  // 8 trees per lane
+      if (a.out_leaf)
+        return launch_common(perfect_global_kernel<D, 8, true, FIN, XB, 0, 4>, threads, n_wg,
+                             lds_bytes, stream, a);
+      return launch_common(perfect_global_kernel<D, 8, false, FIN, XB, 0, 4>, threads, n_wg,
+                           lds_bytes, stream, a);
+    }
+  }
+  if constexpr (D > 3) {
+    if (a.top_levels == 3 && !a.vec) {  // 16 trees per lane
+      if (a.out_leaf)
+        return launch_common(perfect_global_kernel<D, 16, true, FIN, XB, 0, 3>, threads, n_wg,
+                             lds_bytes, stream, a);
+      return launch_common(perfect_global_kernel<D, 16, false, FIN, XB, 0, 3>, threads, n_wg,
+                           lds_bytes, stream, a);
+    }
+  }
   if (a.out_leaf)
     return launch_common(perfect_global_kernel<D, 4, true, FIN, XB>, threads, n_wg, lds_bytes, stream, a);
   if (a.vec && a.K <= 4)
