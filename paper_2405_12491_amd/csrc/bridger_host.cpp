@@ -1492,10 +1492,30 @@ bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_
     a.q_off = (const int32_t *)h->d_q_off;
     a.xq = (uint8_t *)Xq + r0 * (int64_t)h->F * h->bin_bytes;
     a.x_vec4 = ((uintptr_t)a.X % 16 == 0) && (h->F % 4 == 0);
-    a.rows_per_wg = env_int("BRIDGER_BIN_ROWS", 0);  // tuning override of the row block
+    a.rows_per_wg = env_int("BRIDGER_BIN_ROWS", 0);  // tuning overrides: stream kernel's rows
+    a.trees_per_chunk = env_int("BRIDGER_BIN_CHUNKS", 0);  // and row kernel's 512-row chunks
     {  // tuning override of the LDS table buffer
       const int kb = env_int("BRIDGER_BIN_LDS_KB", 0);
       if (kb > 0) a.chunk_bytes = (int32_t)std::min<int64_t>((int64_t)kb * 1024, kLdsBytesPerCU);
+    }
+    // the largest number of LDS loads of tables (runs of whole tables within 64 KB, or the
+    // override) any group of 32 features needs; it picks the binning kernel
+    {
+      const int cap = (a.chunk_bytes > 0 ? a.chunk_bytes : 65536) / 4;
+      int max_runs = 0;
+      for (int f0 = 0; f0 < h->F; f0 += 32) {
+        const int f1 = std::min(h->F, f0 + 32);
+        int runs = 0;
+        for (int f = f0; f < f1;) {
+          int fe = f;
+          while (fe < f1 && h->q_off[fe + 1] - h->q_off[f] <= cap) ++fe;
+          f = fe > f ? fe : f + 1;
+          ++runs;
+        }
+        max_runs = std::max(max_runs, runs);
+      }
+      a.n_chunks = env_int("BRIDGER_BIN_KERNEL", 0) == 1 ? 3
+                   : env_int("BRIDGER_BIN_KERNEL", 0) == 2 ? 1 : max_runs;
     }
     set_preprocess_args(h, a);
     RowNorms norms;

@@ -81,7 +81,13 @@ def test_binned_adversarial(F):
 
 
 @pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1"}, {"BRIDGER_GLOBAL": "0"},
-                                 {"BRIDGER_ILP": "1", "BRIDGER_WAVES": "4", "BRIDGER_ROWS": "128"}],
+                                 {"BRIDGER_ILP": "1", "BRIDGER_WAVES": "4", "BRIDGER_ROWS": "128"},
+                                 # the binning pass: row kernel, stream kernel, small LDS buffers
+                                 # (many runs; tables larger than the buffer searched in place)
+                                 {"BRIDGER_BIN_KERNEL": "1"}, {"BRIDGER_BIN_KERNEL": "2"},
+                                 {"BRIDGER_BIN_KERNEL": "1", "BRIDGER_BIN_LDS_KB": "1"},
+                                 {"BRIDGER_BIN_KERNEL": "1", "BRIDGER_BIN_CHUNKS": "3"},
+                                 {"BRIDGER_BIN_KERNEL": "2", "BRIDGER_BIN_LDS_KB": "1"}],
                          ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
 def test_binned_kernel_variants(env, monkeypatch):
     for k, v in env.items():
