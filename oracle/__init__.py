@@ -31,9 +31,10 @@ _lock = threading.Lock()
 
 def build(src: str = _SRC, out: str = _LIB_PATH) -> str:
     """Compile the oracle with gcc (no FMA contraction, no fast-math)."""
-    cmd = ["gcc", *GCC_FLAGS, "-o", out + ".tmp", src, "-lm"]
+    tmp = f"{out}.{os.getpid()}.tmp"  # one per process: parallel test workers build at once
+    cmd = ["gcc", *GCC_FLAGS, "-o", tmp, src, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(out + ".tmp", out)
+    os.replace(tmp, out)
     return out
 
 

@@ -45,6 +45,18 @@ constexpr double kLdsInstrPerSec = 0.44 * 256 * 2.4e9;
 constexpr int kMaxWavesPerCU = 32;
 constexpr double kL2BytesPerXcd = 4.0 * 1024 * 1024;
 constexpr int kMinWavesPerCU = 8;
+constexpr int kNumCUs = 256;
+// Latency terms for small batches, where a workgroup's walk over its share of the trees, not
+// the throughput of the LDS, sets the time: one dependent LDS gather (two per level, and the
+// leaf), and the barrier and L2 round trip of a chunk.  Fitted by least squares to batches
+// that take one round of workgroups (the 500-tree depth-6 and 100-tree depth-8 forests, one to
+// sixteen lane groups, 7 to 32 chunks; 15 to 81 us): 35 ns and 0.63 us.
+constexpr double kLdsLatencySec = 35e-9;
+constexpr double kChunkLatencySec = 0.63e-6;
+// Batch-size classes: besides the plan for large batches, each forest keeps plans made for
+// batches of at most these many rows (a predict takes the smallest class that holds it).
+constexpr int64_t kSizeClasses[] = {int64_t(1) << 13, int64_t(1) << 15, int64_t(1) << 17,
+                                    int64_t(1) << 19};
 
 int env_int(const char *name, int dflt) {
   const char *v = std::getenv(name);
@@ -110,6 +122,21 @@ struct bridger_forest {
   bool perfect_bok = false, ragged_bok = false;
   std::vector<uint8_t> perfect_btrav;   // PERFECT traversal copy for bins: {rank, f * R * bytes}
   std::vector<uint32_t> perfect_broots;  // per tree: the binned copy's root record
+  // PERFECT plans for small batches (kSizeClasses; the plans above serve larger batches), with
+  // the traversal copies for their row tiles (copy -1: the one above serves)
+  struct TravCopy {
+    int32_t R;
+    std::vector<uint8_t> trav;
+    std::vector<uint32_t> roots;
+    void *d_trav = nullptr, *d_roots = nullptr;
+  };
+  struct SizedPlan {
+    int64_t max_rows;
+    Plan plan;
+    int copy;
+  };
+  std::vector<SizedPlan> perfect_sized, perfect_bsized;
+  std::deque<TravCopy> perfect_copies, perfect_bcopies;
   std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
   std::vector<uint64_t> ragged_tops, ragged_btops;  // top-level heaps (fp32 / binned records)
   std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
@@ -273,13 +300,14 @@ void pack_perfect(bridger_forest *h, int D, const int64_t *offs, const int32_t *
 // Records of the PERFECT kernel: the feature index becomes the byte offset of the feature's
 // row in the LDS tile of the chosen plan (row stride 4R bytes), and a threshold of -0 is
 // stored as +0 (equal under <=; the sign-of-difference step needs the +0).
-void build_perfect_trav(bridger_forest *h) {
+void make_perfect_trav(const bridger_forest *h, int32_t R, std::vector<uint8_t> &trav,
+                       std::vector<uint32_t> &roots) {
   const int D = h->perfect_depth;
   const int tb = h->perfect_tree_bytes;
-  const uint32_t row_bytes = 4u * (uint32_t)h->perfect_plan.rows_per_wg;
-  h->perfect_trav = h->perfect_blob;
+  const uint32_t row_bytes = 4u * (uint32_t)R;
+  trav = h->perfect_blob;
   for (int32_t k = 0; k < h->n_trees; ++k) {
-    uint8_t *blk = h->perfect_trav.data() + (size_t)k * tb;
+    uint8_t *blk = trav.data() + (size_t)k * tb;
     for (int m = 1; m < (1 << D); ++m) {
       float th;
       uint32_t f;
@@ -291,9 +319,13 @@ void build_perfect_trav(bridger_forest *h) {
       std::memcpy(blk + 8 * m + 4, &f, 4);
     }
   }
-  h->perfect_roots.assign((size_t)2 * h->n_trees, 0);
+  roots.assign((size_t)2 * h->n_trees, 0);
   for (int32_t k = 0; k < h->n_trees; ++k)
-    std::memcpy(&h->perfect_roots[2 * (size_t)k], h->perfect_trav.data() + (size_t)k * tb + 8, 8);
+    std::memcpy(&roots[2 * (size_t)k], trav.data() + (size_t)k * tb + 8, 8);
+}
+
+void build_perfect_trav(bridger_forest *h) {
+  make_perfect_trav(h, h->perfect_plan.rows_per_wg, h->perfect_trav, h->perfect_roots);
 }
 
 // Breadth-first record order with adjacent children; returns false if a tree cannot be
@@ -397,7 +429,11 @@ void build_vector_leaves(bridger_forest *h, const int64_t *offs, const int32_t *
         put(h->vec_perfect, k * n_leaf + j, h->tree_order[k], h->perfect_leaf_map[k * n_leaf + j]);
     if (perfect_vec_rows(h)) {  // the rows also go into every copy of the tree blocks
       const size_t tb = (size_t)h->perfect_tree_bytes, row = 4 * (size_t)KS;
-      for (std::vector<uint8_t> *blob : {&h->perfect_blob, &h->perfect_trav, &h->perfect_btrav}) {
+      std::vector<std::vector<uint8_t> *> blobs{&h->perfect_blob, &h->perfect_trav,
+                                                &h->perfect_btrav};
+      for (auto *cs : {&h->perfect_copies, &h->perfect_bcopies})
+        for (auto &c : *cs) blobs.push_back(&c.trav);
+      for (std::vector<uint8_t> *blob : blobs) {
         if (blob->empty()) continue;
         for (int32_t k = 0; k < h->n_trees; ++k)
           std::memcpy(blob->data() + k * tb + 8 * n_leaf, &h->vec_perfect[k * n_leaf * KS],
@@ -524,6 +560,16 @@ Plan choose_plan(const PlanInput &in) {
           const double lds_instr =
               (double)n / 64.0 * (2.0 * in.visits_per_row + in.n_trees) +
               n_wg * (in.forest_bytes / 1024.0);
+          // fewer workgroups than resident slots leave CUs idle; and a workgroup cannot finish
+          // before its lanes' dependent gathers over their share of the trees, once per round
+          // of resident workgroups
+          const double slots = (double)kNumCUs * m;
+          const double fill = std::min(1.0, n_wg / slots);
+          const double rounds = std::ceil(n_wg / slots);
+          const double per_tree_visits = in.visits_per_row / std::max(in.n_trees, 1);
+          const double chain = rounds * (std::ceil((double)in.n_trees / ((double)G * ilp)) *
+                                             (2.0 * per_tree_visits + 1.0) * kLdsLatencySec +
+                                         n_chunks * kChunkLatencySec);
           Cand c{};
           c.p.waves = W;
           c.p.rows_per_wg = R;
@@ -539,7 +585,8 @@ Plan choose_plan(const PlanInput &in) {
           c.p.stage_bytes = stage;
           c.p.lds_read_bytes = lds_instr * 256.0;
           c.p.est_seconds = std::max({hbm / kHbmBytesPerSec, stage / kL2BytesPerSec,
-                                      lds_instr / kLdsInstrPerSec});
+                                      lds_instr / kLdsInstrPerSec}) / fill;
+          c.p.est_seconds = std::max(c.p.est_seconds, chain);
           c.waves_cu = m * W;
           c.p.waves_per_cu = m * W;
           c.single = G == 1;
@@ -747,13 +794,14 @@ uint32_t rank_of(const bridger_forest *h, int32_t f, float t) {
 }
 
 // PERFECT traversal copy for bins: {rank, byte offset f * R * bin_bytes of the feature's row}.
-void build_perfect_btrav(bridger_forest *h) {
+void make_perfect_btrav(const bridger_forest *h, int32_t R, std::vector<uint8_t> &trav,
+                        std::vector<uint32_t> &roots) {
   const int D = h->perfect_depth;
   const int tb = h->perfect_tree_bytes;
-  const uint32_t row_bytes = (uint32_t)h->perfect_bplan.rows_per_wg * (uint32_t)h->bin_bytes;
-  h->perfect_btrav = h->perfect_blob;
+  const uint32_t row_bytes = (uint32_t)R * (uint32_t)h->bin_bytes;
+  trav = h->perfect_blob;
   for (int32_t k = 0; k < h->n_trees; ++k) {
-    uint8_t *blk = h->perfect_btrav.data() + (size_t)k * tb;
+    uint8_t *blk = trav.data() + (size_t)k * tb;
     for (int m = 1; m < (1 << D); ++m) {
       float th;
       uint32_t f;
@@ -764,9 +812,48 @@ void build_perfect_btrav(bridger_forest *h) {
       std::memcpy(blk + 8 * m + 4, &off, 4);
     }
   }
-  h->perfect_broots.assign((size_t)2 * h->n_trees, 0);
+  roots.assign((size_t)2 * h->n_trees, 0);
   for (int32_t k = 0; k < h->n_trees; ++k)
-    std::memcpy(&h->perfect_broots[2 * (size_t)k], h->perfect_btrav.data() + (size_t)k * tb + 8, 8);
+    std::memcpy(&roots[2 * (size_t)k], trav.data() + (size_t)k * tb + 8, 8);
+}
+
+void build_perfect_btrav(bridger_forest *h) {
+  make_perfect_btrav(h, h->perfect_bplan.rows_per_wg, h->perfect_btrav, h->perfect_broots);
+}
+
+bool same_plan(const Plan &a, const Plan &b) {
+  return a.waves == b.waves && a.rows_per_wg == b.rows_per_wg && a.groups == b.groups &&
+         a.chunk_bytes == b.chunk_bytes && a.trees_per_chunk == b.trees_per_chunk &&
+         a.n_chunks == b.n_chunks && a.lds_bytes == b.lds_bytes && a.ilp == b.ilp &&
+         a.global_nodes == b.global_nodes && a.acc_alias == b.acc_alias && a.tops == b.tops;
+}
+
+// PERFECT plans for the batch-size classes that differ from the large-batch plan `big`, each
+// with a traversal copy for its row tile unless `big`'s serves (binned: bin copies).
+void build_sized_plans(bridger_forest *h, PlanInput pin, const Plan &big, bool binned) {
+  auto &sized = binned ? h->perfect_bsized : h->perfect_sized;
+  auto &copies = binned ? h->perfect_bcopies : h->perfect_copies;
+  sized.clear();
+  copies.clear();
+  if (env_int("BRIDGER_SIZED_PLANS", 1) == 0) return;
+  for (const int64_t n : kSizeClasses) {
+    pin.n_rows = n;
+    const Plan p = pick_plan(pin);
+    if (p.waves == 0 || same_plan(p, big)) continue;
+    int copy = -1;
+    if (p.rows_per_wg != big.rows_per_wg) {
+      for (size_t i = 0; i < copies.size(); ++i)
+        if (copies[i].R == p.rows_per_wg) copy = (int)i;
+      if (copy < 0) {
+        copies.emplace_back();
+        copies.back().R = p.rows_per_wg;
+        if (binned) make_perfect_btrav(h, p.rows_per_wg, copies.back().trav, copies.back().roots);
+        else make_perfect_trav(h, p.rows_per_wg, copies.back().trav, copies.back().roots);
+        copy = (int)copies.size() - 1;
+      }
+    }
+    sized.push_back({n, p, copy});
+  }
 }
 
 // RAGGED records for bins: an internal record's threshold becomes its rank.
@@ -848,6 +935,11 @@ void free_all(bridger_forest *h) {
   free_dev(h->d_perfect_trav);
   free_dev(h->d_perfect_roots);
   free_dev(h->d_perfect_broots);
+  for (auto *cs : {&h->perfect_copies, &h->perfect_bcopies})
+    for (auto &c : *cs) {
+      free_dev(c.d_trav);
+      free_dev(c.d_roots);
+    }
   for (void **q : {&h->d_ragged_tops, &h->d_ragged_btops, &h->d_q_values, &h->d_q_off,
                    &h->d_perfect_btrav, &h->d_ragged_brec,
                    &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b,
@@ -872,6 +964,10 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_perfect.nodes, h->perfect_blob, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_perfect_trav, h->perfect_trav, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_perfect_roots, h->perfect_roots)) != BRIDGER_OK) return s;
+    for (auto &c : h->perfect_copies) {
+      if ((s = upload(&c.d_trav, c.trav, 1024)) != BRIDGER_OK) return s;
+      if ((s = upload(&c.d_roots, c.roots)) != BRIDGER_OK) return s;
+    }
     if ((s = upload(&h->d_perfect.leaf_map, h->perfect_leaf_map)) != BRIDGER_OK) return s;
   }
   if (h->ragged_ok) {
@@ -890,6 +986,10 @@ bridger_status upload_all(bridger_forest *h) {
   if (h->perfect_bok) {
     if ((s = upload(&h->d_perfect_btrav, h->perfect_btrav, 1024)) != BRIDGER_OK) return s;
     if ((s = upload(&h->d_perfect_broots, h->perfect_broots)) != BRIDGER_OK) return s;
+    for (auto &c : h->perfect_bcopies) {
+      if ((s = upload(&c.d_trav, c.trav, 1024)) != BRIDGER_OK) return s;
+      if ((s = upload(&c.d_roots, c.roots)) != BRIDGER_OK) return s;
+    }
   }
   if (h->ragged_bok) {
     if ((s = upload(&h->d_ragged_brec, h->ragged_brec, 1024)) != BRIDGER_OK) return s;
@@ -991,6 +1091,15 @@ bridger_status check_predict(const bridger_forest *h, const void *X, int64_t n_r
   return BRIDGER_OK;
 }
 
+// The PERFECT plan made for the smallest batch-size class holding n_rows, or null (the plan
+// for large batches serves).
+const bridger_forest::SizedPlan *sized_plan(const bridger_forest *h, int64_t n_rows,
+                                            bool binned) {
+  for (const auto &sp : binned ? h->perfect_bsized : h->perfect_sized)
+    if (n_rows <= sp.max_rows) return &sp;
+  return nullptr;
+}
+
 // X is fp32 rows, or (binned) rows of bin_bytes-wide bins from bridger_forest_bin.
 struct CsrRows {
   const int64_t *indptr = nullptr;
@@ -1033,8 +1142,10 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
   int err = 0;
   if (h->kernel_active == kPerfect || h->kernel_active == kRagged) {
     const bool perfect = h->kernel_active == kPerfect;
-    const Plan &p = perfect ? (binned ? h->perfect_bplan : h->perfect_plan)
-                            : (binned ? h->ragged_bplan : h->ragged_plan);
+    const bridger_forest::SizedPlan *sp = perfect ? sized_plan(h, n_rows, binned) : nullptr;
+    const Plan &p = sp ? sp->plan
+                       : perfect ? (binned ? h->perfect_bplan : h->perfect_plan)
+                                 : (binned ? h->ragged_bplan : h->ragged_plan);
     const DevArrays &d = perfect ? h->d_perfect : h->d_ragged;
     if (perfect)
       a.nodes = (const uint8_t *)(binned ? h->d_perfect_btrav : h->d_perfect_trav);
@@ -1042,6 +1153,11 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
       a.nodes = (const uint8_t *)(binned ? h->d_ragged_brec : d.nodes);
     a.finite_thresholds = h->finite_thresholds ? 1 : 0;
     a.roots = (const uint32_t *)(binned ? h->d_perfect_broots : h->d_perfect_roots);
+    if (sp && sp->copy >= 0) {  // the small-batch plan's own row tile
+      const auto &c = (binned ? h->perfect_bcopies : h->perfect_copies)[sp->copy];
+      a.nodes = (const uint8_t *)c.d_trav;
+      a.roots = (const uint32_t *)c.d_roots;
+    }
     a.tree_start = (const int32_t *)d.tree_start;
     a.chunk_first = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_first : d.chunk_first);
     a.chunk_rec = (const int32_t *)(binned && !perfect ? h->d_ragged_bchunk_rec : d.chunk_rec);
@@ -1308,7 +1424,10 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       pin.depth = D;
       h->perfect_plan = pick_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
-      if (h->perfect_ok) build_perfect_trav(h);
+      if (h->perfect_ok) {
+        build_perfect_trav(h);
+        build_sized_plans(h, pin, h->perfect_plan, false);
+      }
     }
     const bool ragged_packed = pack_ragged(h, tree_offsets, feature, threshold, left, right, value);
     if (ragged_packed) {
@@ -1333,7 +1452,10 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         pin.depth = D;
         h->perfect_bplan = pick_plan(pin);
         h->perfect_bok = h->perfect_bplan.waves > 0;
-        if (h->perfect_bok) build_perfect_btrav(h);
+        if (h->perfect_bok) {
+          build_perfect_btrav(h);
+          build_sized_plans(h, pin, h->perfect_bplan, true);
+        }
       }
       if (ragged_packed) {
         PlanInput pin{1 << 20, n_features, n_classes, n_trees, 8.0 * h->ragged_rec.size(),
@@ -1367,6 +1489,14 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       show("perfect binned", h->perfect_bplan);
       show("ragged", h->ragged_plan);
       show("ragged binned", h->ragged_bplan);
+      for (const auto &sp : h->perfect_sized) {
+        const std::string what = "perfect <= " + std::to_string(sp.max_rows) + " rows";
+        show(what.c_str(), sp.plan);
+      }
+      for (const auto &sp : h->perfect_bsized) {
+        const std::string what = "perfect binned <= " + std::to_string(sp.max_rows) + " rows";
+        show(what.c_str(), sp.plan);
+      }
     }
     h->kernel_active = resolve_auto(h);
     const int forced = env_int("BRIDGER_KERNEL", 0);
@@ -1631,7 +1761,8 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
   Plan p{};
   double forest_bytes = 0;
   if (h->kernel_active == kPerfect) {
-    p = h->perfect_plan;
+    const bridger_forest::SizedPlan *sp = sized_plan(h, n_rows, false);
+    p = sp ? sp->plan : h->perfect_plan;
     forest_bytes = (double)h->perfect_blob.size();
   } else if (h->kernel_active == kRagged) {
     p = h->ragged_plan;

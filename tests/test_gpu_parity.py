@@ -257,6 +257,7 @@ VARIANT_ENVS = [
     {"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "8", "BRIDGER_ROWS": "32"},    # 2 groups a wave
     {"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "8", "BRIDGER_ROWS": "128"},   # groups of 2 waves
     {"BRIDGER_NO_FIXED": "1"},                                 # run-time chunk geometry
+    {"BRIDGER_SIZED_PLANS": "0"},                              # the large-batch plan on small n
     {"BRIDGER_CHUNK_TREES": "4"},                              # compile-time chunks of 4, 8, 32
     {"BRIDGER_CHUNK_TREES": "8"},
     {"BRIDGER_CHUNK_TREES": "32"},
@@ -390,6 +391,59 @@ def test_perfect_kernel_variants(env, monkeypatch):
                 continue
             print(f"[variant] {env} {name} plan={f.plan(X.shape[0])}", flush=True)
             check_parity(model, X, B.BRIDGER_KERNEL_PERFECT, f"{name} {env}", forest=f)
+
+
+# batch sizes in each of the planner's size classes (up to 8192, 32768, 131072 and 524288 rows;
+# larger batches take the large-batch plan)
+SIZE_CLASS_ROWS = [1, 325, 5000, 20000, 100000]
+
+
+def _size_class_models():
+    from synth import with_vector_leaves
+    rng = np.random.default_rng(91)
+    F, T = 9, 22
+    trees = [perfect_tree_arrays(6, rng.integers(0, F, 63), rng.standard_normal(63).astype(np.float32),
+                                 rng.standard_normal(64).astype(np.float32)) for _ in range(T)]
+    one = concat_trees(trees, F, 1, None, AGG_SUM, XFORM_SIGMOID, np.zeros(1, np.float32))
+    tc = np.arange(T) % 3
+    multi = concat_trees(trees, F, 3, tc, AGG_SUM, XFORM_SOFTMAX, rng.standard_normal(3).astype(np.float32))
+    models = [("K=1", one), ("K=3", multi)]
+    for K in (2, 3, 8):
+        models.append((f"vector K={K}", with_vector_leaves(one, K, rng, AGG_MEAN, XFORM_SOFTMAX)))
+    X = rng.standard_normal((max(SIZE_CLASS_ROWS), F)).astype(np.float32)
+    return models, X
+
+
+def test_batch_size_classes():
+    """Every batch-size class's plan (each with its own row tile and traversal copy) against
+    the oracle, for scalar and vector leaves, on fp32 rows and on bins."""
+    import torch
+    models, X = _size_class_models()
+    Xd = to_dev(X)
+    from oracle import vector as V
+    for name, model in models:
+        if np.ndim(model.value) == 2:
+            ref, ref_lv = V.predict(model, X, threads=8)
+        else:
+            ref, ref_lv = oracle_predict(model, X, leaves=True)
+        with B.Forest(model) as f:
+            f.kernel = B.BRIDGER_KERNEL_PERFECT
+            q = f.bin(Xd)
+            plans = set()
+            for n in SIZE_CLASS_ROWS:
+                p = f.plan(n)
+                plans.add((p["rows_per_wg"], p["chunk_bytes"], p["lds_bytes"]))
+                print(f"[sized] {name} n={n} plan={p}", flush=True)
+                what = f"{name} n={n}"
+                assert_scores(gpu_predict(f, Xd[:n]), ref[:n], what + " scores")
+                assert_leaves(gpu_predict(f, Xd[:n], leaves=True), ref_lv[:n], what + " leaves")
+                out = f.predict_binned(q[:n])
+                lv = f.predict_binned_leaves(q[:n])
+                torch.cuda.synchronize()
+                assert_scores(out.cpu().numpy().astype(np.float64), ref[:n], what + " binned scores")
+                assert_leaves(lv.cpu().numpy(), ref_lv[:n], what + " binned leaves")
+            # small batches get plans of their own (more, smaller workgroups)
+            assert len(plans) >= 2, (name, plans)
 
 
 def test_determinism_and_streams():
