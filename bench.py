@@ -130,6 +130,7 @@ def load_calib():
     lib.bridger_calib_device.argtypes = [P, P, P]
     lib.bridger_calib_lds_gather.argtypes = [I32, I32, I32, P, P]
     lib.bridger_calib_copy.argtypes = [I64, I32, P, P]
+    lib.bridger_calib_global_gather.argtypes = [I32, I32, I32, I32, P, P]
     return lib
 
 
@@ -156,6 +157,19 @@ def calibrate(copy_bytes=512 << 20, reps=20):
     # node-record reads (b64) when the wave's lanes share 1, 2, ..., 32 records
     out["lds_b64_lanes_per_clk_per_cu_by_distinct"] = {
         str(d): gather(8, d) for d in (1, 2, 4, 8, 16, 32)}
+    # wave-wide loads from an L2-resident buffer of 2 MiB: clocks per load instruction per CU
+    def global_gather(width, distinct):
+        ms, rate = ctypes.c_double(), ctypes.c_double()
+        rc = lib.bridger_calib_global_gather(width, distinct, 21, reps, ctypes.byref(ms),
+                                             ctypes.byref(rate))
+        if rc != 0:
+            raise RuntimeError(f"bridger_calib_global_gather({width}, {distinct}) failed: {rc}")
+        return N_CU * CLOCK_HZ / rate.value
+
+    out["l2_gather_clk_per_wave_load_per_cu"] = {
+        "b32": global_gather(4, 64), "b64": global_gather(8, 64), "b128": global_gather(16, 64)}
+    out["l2_b64_clk_per_wave_load_per_cu_by_distinct_lines"] = {
+        str(d): global_gather(8, d) for d in (1, 4, 16)}
     ms, rate = ctypes.c_double(), ctypes.c_double()
     rc = lib.bridger_calib_copy(copy_bytes, reps, ctypes.byref(ms), ctypes.byref(rate))
     if rc != 0:
@@ -164,8 +178,9 @@ def calibrate(copy_bytes=512 << 20, reps=20):
     out["copy_bytes"] = copy_bytes
     out["what"] = ("per-lane LDS gathers at addresses held in registers, 32 waves per CU, 16 "
                    "independent reads per lane in flight; lanes per clock per CU at the nominal "
-                   "clock (the peak rates the kernels against 32); copy: read + write bytes/s "
-                   "of a 16-byte-per-lane device copy")
+                   "clock (the peak rates the kernels against 32); L2 gathers: clocks per "
+                   "wave-wide load per CU, each lane on its own 128-byte line unless shared; "
+                   "copy: read + write bytes/s of a 16-byte-per-lane device copy")
     return out
 
 

@@ -322,9 +322,15 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
  * 2 leaf-id map (kernel leaf slot -> caller node id), 3 kernel tree order
  * (kernel position -> caller tree index), 4 chunk table, 5 the binning thresholds
  * (float, feature after feature, each ascending), 6 their per-feature offsets
- * (int32 [n_features + 1]), 7 the ragged trees' top-level heaps (16 records per tree: the
- * root's record index, then the records of the first four levels as a 1-based heap; absent
- * when the plan does not use them).  *ptr stays valid until destroy or set_kernel.
+ * (int32 [n_features + 1]), 7 the ragged trees' top-level heaps (2^L records per tree, L = 4
+ * or 5 levels: the root's record index, then the records of the first L levels as a 1-based
+ * heap; absent when the plan does not use them), 8 and 9 the perfect trees' deep blocks below
+ * their first 3 (or 4) levels, with the thresholds' bits (8) or their ranks among the binning
+ * thresholds (9): per kernel tree, levels taken in pairs, one 16-byte block {w(m), w(2m),
+ * w(2m + 1), f(m) | f(2m) << 10 | f(2m + 1) << 20} per node m of a pair's upper level, then
+ * either one block {w(m), f(m), leaf value of 2m, of 2m + 1} per node of the last level or
+ * the 2^D leaf values (absent with vector leaves or more than 1024 features).  *ptr stays
+ * valid until destroy or set_kernel.
  */
 bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
                                      int64_t *bytes);

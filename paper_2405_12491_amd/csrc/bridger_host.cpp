@@ -137,6 +137,11 @@ struct bridger_forest {
   };
   std::vector<SizedPlan> perfect_sized, perfect_bsized;
   std::deque<TravCopy> perfect_copies, perfect_bcopies;
+  // PERFECT deep blocks (layout in internal.h) below deep_tl top levels: thresholds' bits,
+  // and ranks for bins; empty when the forest has more than kDeepMaxFeatures features
+  std::vector<uint8_t> perfect_deep, perfect_bdeep;
+  int32_t deep_tl = 0;
+  void *d_perfect_deep = nullptr, *d_perfect_bdeep = nullptr;
   std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
   std::vector<uint64_t> ragged_tops, ragged_btops;  // top-level heaps (fp32 / binned records)
   std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
@@ -821,6 +826,63 @@ void build_perfect_btrav(bridger_forest *h) {
   make_perfect_btrav(h, h->perfect_bplan.rows_per_wg, h->perfect_btrav, h->perfect_broots);
 }
 
+// Deep blocks of the PERFECT trees below TL top levels (layout in internal.h) from the packed
+// blocks: thresholds as stored (-0 as +0, as in the traversal copy), or their ranks (binned).
+void make_perfect_deep(const bridger_forest *h, int TL, bool binned, std::vector<uint8_t> &deep) {
+  const int D = h->perfect_depth, tb = h->perfect_tree_bytes;
+  const int dtb = deep_tree_bytes(D, TL), ND = D - TL, NP = ND / 2;
+  deep.assign((size_t)dtb * h->n_trees, 0);
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const uint8_t *blk = h->perfect_blob.data() + (size_t)k * tb;
+    uint8_t *out = deep.data() + (size_t)k * dtb;
+    auto rec = [&](int m, uint32_t &w, uint32_t &f) {
+      float th;
+      std::memcpy(&th, blk + 8 * m, 4);
+      std::memcpy(&f, blk + 8 * m + 4, 4);
+      if (th == 0.0f) th = 0.0f;
+      if (binned) w = rank_of(h, (int32_t)f, th);
+      else std::memcpy(&w, &th, 4);
+    };
+    auto leaf = [&](int j) {
+      uint32_t v;
+      std::memcpy(&v, blk + (8 << D) + 4 * j, 4);
+      return v;
+    };
+    for (int i = 0; i < NP; ++i) {
+      const int d = TL + 2 * i;
+      for (int m = 1 << d; m < (2 << d); ++m) {
+        uint32_t w[3], f[3];
+        rec(m, w[0], f[0]);
+        rec(2 * m, w[1], f[1]);
+        rec(2 * m + 1, w[2], f[2]);
+        const uint32_t q[4] = {w[0], w[1], w[2], f[0] | f[1] << 10 | f[2] << 20};
+        std::memcpy(out + deep_pair_off(TL, i) + 16 * (m - (1 << d)), q, 16);
+      }
+    }
+    uint8_t *tail = out + deep_pair_off(TL, NP);
+    if (ND & 1) {
+      for (int m = 1 << (D - 1); m < (1 << D); ++m) {
+        uint32_t q[4];
+        rec(m, q[0], q[1]);
+        q[2] = leaf(2 * m - (1 << D));
+        q[3] = leaf(2 * m + 1 - (1 << D));
+        std::memcpy(tail + 16 * (m - (1 << (D - 1))), q, 16);
+      }
+    } else {
+      for (int j = 0; j < (1 << D); ++j) {
+        const uint32_t v = leaf(j);
+        std::memcpy(tail + 4 * j, &v, 4);
+      }
+    }
+  }
+}
+
+// The deep blocks serve the wide-row plans whose top levels come from LDS copies.
+bool deep_wanted(const bridger_forest *h) {
+  return env_int("BRIDGER_DEEP", 1) != 0 && !h->vec && h->F <= kDeepMaxFeatures &&
+         h->perfect_depth > perfect_top_levels();
+}
+
 bool same_plan(const Plan &a, const Plan &b) {
   return a.waves == b.waves && a.rows_per_wg == b.rows_per_wg && a.groups == b.groups &&
          a.chunk_bytes == b.chunk_bytes && a.trees_per_chunk == b.trees_per_chunk &&
@@ -940,7 +1002,8 @@ void free_all(bridger_forest *h) {
       free_dev(c.d_trav);
       free_dev(c.d_roots);
     }
-  for (void **q : {&h->d_ragged_tops, &h->d_ragged_btops, &h->d_q_values, &h->d_q_off,
+  for (void **q : {&h->d_perfect_deep, &h->d_perfect_bdeep, &h->d_ragged_tops,
+                   &h->d_ragged_btops, &h->d_q_values, &h->d_q_off,
                    &h->d_perfect_btrav, &h->d_ragged_brec,
                    &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b,
                    &h->d_vec_perfect, &h->d_vec_ragged, &h->d_vec_direct})
@@ -969,6 +1032,9 @@ bridger_status upload_all(bridger_forest *h) {
       if ((s = upload(&c.d_roots, c.roots)) != BRIDGER_OK) return s;
     }
     if ((s = upload(&h->d_perfect.leaf_map, h->perfect_leaf_map)) != BRIDGER_OK) return s;
+    if (!h->perfect_deep.empty() &&
+        (s = upload(&h->d_perfect_deep, h->perfect_deep, 1024)) != BRIDGER_OK)
+      return s;
   }
   if (h->ragged_ok) {
     if ((s = upload(&h->d_ragged.nodes, h->ragged_rec, 1024)) != BRIDGER_OK) return s;
@@ -990,6 +1056,9 @@ bridger_status upload_all(bridger_forest *h) {
       if ((s = upload(&c.d_trav, c.trav, 1024)) != BRIDGER_OK) return s;
       if ((s = upload(&c.d_roots, c.roots)) != BRIDGER_OK) return s;
     }
+    if (!h->perfect_bdeep.empty() &&
+        (s = upload(&h->d_perfect_bdeep, h->perfect_bdeep, 1024)) != BRIDGER_OK)
+      return s;
   }
   if (h->ragged_bok) {
     if ((s = upload(&h->d_ragged_brec, h->ragged_brec, 1024)) != BRIDGER_OK) return s;
@@ -1191,6 +1260,11 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
       if (p.tops) {  // after the row tile and the class sums
         a.top_levels = p.tops;
         a.lds_top_off = a.lds_acc_off + h->K * p.groups * p.rows_per_wg * 8;
+        void *deep = binned ? h->d_perfect_bdeep : h->d_perfect_deep;
+        if (deep && p.tops == h->deep_tl) {
+          a.deep = (const uint8_t *)deep;
+          a.deep_tree_bytes = deep_tree_bytes(h->perfect_depth, p.tops);
+        }
       }
       err = launch_perfect_global(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     }
@@ -1427,6 +1501,10 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       if (h->perfect_ok) {
         build_perfect_trav(h);
         build_sized_plans(h, pin, h->perfect_plan, false);
+        if (deep_wanted(h)) {
+          h->deep_tl = perfect_top_levels();
+          make_perfect_deep(h, h->deep_tl, false, h->perfect_deep);
+        }
       }
     }
     const bool ragged_packed = pack_ragged(h, tree_offsets, feature, threshold, left, right, value);
@@ -1455,6 +1533,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         if (h->perfect_bok) {
           build_perfect_btrav(h);
           build_sized_plans(h, pin, h->perfect_bplan, true);
+          if (!h->perfect_deep.empty()) make_perfect_deep(h, h->deep_tl, true, h->perfect_bdeep);
         }
       }
       if (ragged_packed) {
@@ -1814,6 +1893,10 @@ bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const vo
     case kGemm:
       if (which == 0) return give(h->perfect_blob.data(), h->perfect_blob.size());
       if (which == 2) return give(h->perfect_leaf_map.data(), h->perfect_leaf_map.size() * 4);
+      if (which == 8 && !h->perfect_deep.empty())
+        return give(h->perfect_deep.data(), h->perfect_deep.size());
+      if (which == 9 && !h->perfect_bdeep.empty())
+        return give(h->perfect_bdeep.data(), h->perfect_bdeep.size());
       break;
     case kRagged:
       if (which == 0) return give(h->ragged_rec.data(), h->ragged_rec.size() * 8);

@@ -54,6 +54,41 @@ __global__ __launch_bounds__(kThreads) void lds_gather_kernel(const uint32_t *la
   if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;  // keeps the reads alive; practically never taken
 }
 
+// Per-lane global-memory gathers of W bytes from an L2-resident buffer of mask + 1 bytes: every
+// lane issues kReadsPerIter independent loads per iteration at byte (lane_addr[64 k + l] +
+// it * kGlobalStride) & mask, so each iteration touches new cache lines (the L1 holds few of
+// them) while the buffer stays in L2, as the node records of the global-node kernels do.
+// lane_addr entries are multiples of 128 plus a multiple of W below 128 - W + 1, so no load
+// crosses a line; with `distinct` < 64 lanes share that many lines.
+constexpr uint32_t kGlobalStride = 128u * 4099u;  // an odd number of lines per iteration
+template <int W>
+__global__ __launch_bounds__(kThreads) void global_gather_kernel(const uint8_t *__restrict__ buf,
+                                                                 uint32_t mask,
+                                                                 const uint32_t *lane_addr,
+                                                                 int iters, uint32_t *sink) {
+  uint32_t addr[kReadsPerIter];
+#pragma unroll
+  for (int k = 0; k < kReadsPerIter; ++k) addr[k] = lane_addr[64 * k + (threadIdx.x & 63)];
+  uint32_t acc = 0;
+  for (int it = 0; it < iters; ++it) {
+    const uint32_t shift = (uint32_t)it * kGlobalStride;
+#pragma unroll
+    for (int k = 0; k < kReadsPerIter; ++k) {
+      const uint8_t *q = buf + ((addr[k] + shift) & mask);
+      if constexpr (W == 4) {
+        acc ^= *reinterpret_cast<const uint32_t *>(q);
+      } else if constexpr (W == 8) {
+        const uint2 v = *reinterpret_cast<const uint2 *>(q);
+        acc ^= v.x ^ v.y;
+      } else {
+        const uint4 v = *reinterpret_cast<const uint4 *>(q);
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+      }
+    }
+  }
+  if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;  // keeps the loads alive; practically never taken
+}
+
 __global__ __launch_bounds__(kThreads) void copy_kernel(const uint4 *__restrict__ src,
                                                         uint4 *__restrict__ dst, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * kThreads;
@@ -156,6 +191,61 @@ int bridger_calib_lds_gather(int32_t width_bytes, int32_t distinct, int32_t reps
   const double wave_reads = (double)blocks * (kThreads / 64) * iters * kReadsPerIter;
   if (ms_per_launch) *ms_per_launch = ms;
   if (wave_reads_per_s) *wave_reads_per_s = wave_reads / (ms * 1e-3);
+  return 0;
+}
+
+int bridger_calib_global_gather(int32_t width_bytes, int32_t distinct, int32_t buffer_log2,
+                                int32_t reps, double *ms_per_launch, double *wave_loads_per_s) {
+  if (!(width_bytes == 4 || width_bytes == 8 || width_bytes == 16) || reps < 1 ||
+      distinct < 1 || distinct > 64 || (distinct & (distinct - 1)) != 0 || buffer_log2 < 16 ||
+      buffer_log2 > 30)
+    return (int)hipErrorInvalidValue;
+  int32_t n_cu = 0;
+  int e0 = bridger_calib_device(&n_cu, nullptr, nullptr);
+  if (e0 != 0) return e0;
+  const uint32_t bytes = 1u << buffer_log2;
+  // lane l, read k: line ((l mod distinct) * 16 + k) * 37 (mod the buffer's lines), at a
+  // position inside the line that is a multiple of W
+  uint32_t host[64 * kReadsPerIter];
+  const uint32_t w = (uint32_t)width_bytes, lines = bytes / 128u;
+  for (int k = 0; k < kReadsPerIter; ++k)
+    for (int l = 0; l < 64; ++l) {
+      const uint32_t src = (uint32_t)(l % distinct);
+      const uint32_t line = ((src * 16u + (uint32_t)k) * 37u) % lines;
+      host[64 * k + l] = line * 128u + ((src * w) % 128u);
+    }
+  uint8_t *d_buf = nullptr;
+  uint32_t *d_addr = nullptr, *d_sink = nullptr;
+  const int blocks = n_cu * kBlocksPerCU;
+  hipError_t e = hipMalloc(&d_buf, bytes);
+  if (e == hipSuccess) e = hipMalloc(&d_addr, sizeof(host));
+  if (e == hipSuccess) e = hipMalloc(&d_sink, sizeof(uint32_t) * (size_t)blocks);
+  if (e == hipSuccess) e = hipMemset(d_buf, 3, bytes);
+  if (e == hipSuccess) e = hipMemcpy(d_addr, host, sizeof(host), hipMemcpyHostToDevice);
+  const int iters = 256;
+  double ms = 0.0;
+  if (e == hipSuccess) {
+    const uint32_t mask = bytes - 1u;
+    auto launch = [&]() {
+      if (width_bytes == 4)
+        hipLaunchKernelGGL(global_gather_kernel<4>, dim3(blocks), dim3(kThreads), 0, nullptr,
+                           d_buf, mask, d_addr, iters, d_sink);
+      else if (width_bytes == 8)
+        hipLaunchKernelGGL(global_gather_kernel<8>, dim3(blocks), dim3(kThreads), 0, nullptr,
+                           d_buf, mask, d_addr, iters, d_sink);
+      else
+        hipLaunchKernelGGL(global_gather_kernel<16>, dim3(blocks), dim3(kThreads), 0, nullptr,
+                           d_buf, mask, d_addr, iters, d_sink);
+    };
+    e = time_ms(launch, reps, &ms);
+  }
+  if (d_buf) (void)hipFree(d_buf);
+  if (d_addr) (void)hipFree(d_addr);
+  if (d_sink) (void)hipFree(d_sink);
+  if (e != hipSuccess) return (int)e;
+  const double wave_loads = (double)blocks * (kThreads / 64) * iters * kReadsPerIter;
+  if (ms_per_launch) *ms_per_launch = ms;
+  if (wave_loads_per_s) *wave_loads_per_s = wave_loads / (ms * 1e-3);
   return 0;
 }
 

@@ -75,6 +75,22 @@ constexpr bool perfect_fixed_ok(int D, int CT) {
   return D >= 2 && D <= 9 && (CT == 4 || CT == 8 || CT == 16 || CT == 32) &&
          2 * CT * perfect_tree_bytes(D) <= 65536;
 }
+// PERFECT deep blocks, read from global memory by the wide-row kernel below its first TL levels
+// (which come from per-wave LDS copies): per kernel tree, for the deep levels TL, TL + 2, ...
+// taken in pairs, one 16-byte block per node m of the pair's upper level, {w(m), w(2m),
+// w(2m + 1), f(m) | f(2m) << 10 | f(2m + 1) << 20} (w: the threshold's bits, or its rank for
+// bins; f: the feature index, below kDeepMaxFeatures); then, when D - TL is odd, one block per
+// node m of level D - 1, {w(m), f(m), leaf value of 2m, leaf value of 2m + 1}, else the 2^D
+// leaf values.  Every block of a level is indexed by m - 2^level.
+constexpr int kDeepMaxFeatures = 1024;
+constexpr int deep_pair_off(int TL, int i) {
+  int o = 0;
+  for (int j = 0; j < i; ++j) o += 16 << (TL + 2 * j);
+  return o;
+}
+constexpr int deep_tree_bytes(int D, int TL) {
+  return deep_pair_off(TL, (D - TL) / 2) + (((D - TL) & 1) ? (16 << (D - 1)) : (4 << D));
+}
 constexpr int kMaxGemmDepth = 4;
 constexpr int kMaxGemmFeatures = 64;
 
@@ -152,6 +168,8 @@ struct LaunchArgs {
   int32_t top_levels;          // L
   uint32_t nodes_bytes;        // bytes of `nodes` (RAGGED top-level kernel: < 2^31)
   int32_t lds_top_off;         // byte offset of the per-wave top-level copies in dynamic LDS
+  const uint8_t *deep;         // PERFECT deep blocks of the top_levels plan, or nullptr
+  int32_t deep_tree_bytes;     // their bytes per kernel tree (deep_tree_bytes(D, top_levels))
 };
 
 // Vector leaves: floats per leaf in leaf_vec, K rounded up to whole 16-byte groups.

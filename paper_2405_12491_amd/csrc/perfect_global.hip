@@ -12,12 +12,25 @@
 
 namespace bridger {
 
+// Whether a row goes right at a node: the step bit of step_slot.
+template <bool FIN, int XB>
+__device__ __forceinline__ uint32_t go_right(uint32_t w, uint32_t x) {
+  if constexpr (XB != 4) return (w - x) >> 31;
+  else if constexpr (FIN) return __float_as_uint(__uint_as_float(w) - __uint_as_float(x)) >> 31;
+  else return (__uint_as_float(x) <= __uint_as_float(w)) ? 0u : 1u;
+}
+
 // VK: 0 scalar leaves; 4 or 8 (K <= VK) or 64 vector leaves (class sums in registers / LDS).
 // TL: 0, or the number of top levels read from per-wave LDS copies (scalar leaves only).
-template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0>
-__global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
+// DEEP: below the top levels the walk reads the deep blocks (layout in internal.h): one
+// 16-byte load per pair of levels, and the last level's block carries its two leaf values.
+// DEEP holds 16 blocks of 16 bytes per lane: workgroups of at most 8 waves, so that a lane may
+// use 256 registers.
+template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0, bool DEEP = false>
+__global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(LaunchArgs a) {
   static_assert(TL == 0 || (VK == 0 && U * (8 << TL) == 1024 && TL < D),
                 "top levels: scalar leaves, one lane group's batch in 1 KB");
+  static_assert(!DEEP || TL > 0, "deep blocks follow LDS top levels");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
   constexpr int VR = VK_REG ? VK : 4;
@@ -131,7 +144,7 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
       }
       const uint32_t lbuf = buf + (uint32_t)gi * U * TBT;
 #pragma unroll
-      for (int d = 0; d < D; ++d) {
+      for (int d = 0; d < (DEEP ? TL : D); ++d) {
         uint2 rec[U];
         uint32_t xv[U];
 #pragma unroll
@@ -144,6 +157,65 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
         for (int u = 0; u < U; ++u) m[u] = step_slot<FIN, XB>(m[u], rec[u].x, xv[u]);
         if (d == TL - 1 && j + 1 < NB) copy_batch(j + 1);
       }
+      float lv[U];
+      if constexpr (DEEP) {
+        constexpr int ND = D - TL, NP = ND / 2;
+        const uint32_t l2rb = (uint32_t)a.log2_row_bytes;
+        const uint8_t *dbase[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          dbase[u] = a.deep + (size_t)min(q + u, t_end - 1) * (uint32_t)a.deep_tree_bytes;
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+          // levels d and d + 1: node m's block holds both children's thresholds and features
+          const int d = TL + 2 * i;
+          const int off = deep_pair_off(TL, i) - (16 << d);
+          uint4 blk[U];
+          uint32_t xv[U], b[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            blk[u] = *reinterpret_cast<const uint4 *>(dbase[u] + off + (m[u] << 4));
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            xv[u] = gather_x<FIN, XB>(smem, ((blk[u].w & 1023u) << l2rb) + lane_off);
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            b[u] = go_right<FIN, XB>(blk[u].x, xv[u]);
+            const uint32_t f2 = (blk[u].w >> (b[u] ? 20 : 10)) & 1023u;
+            blk[u].x = b[u] ? blk[u].z : blk[u].y;  // the child's threshold
+            xv[u] = gather_x<FIN, XB>(smem, (f2 << l2rb) + lane_off);
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            m[u] = 4u * m[u] + 2u * b[u] + go_right<FIN, XB>(blk[u].x, xv[u]);
+        }
+        if constexpr (ND & 1) {
+          // level D - 1 with its two leaf values
+          constexpr int off = deep_pair_off(TL, NP) - (16 << (D - 1));
+          uint4 blk[U];
+          uint32_t xv[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            blk[u] = *reinterpret_cast<const uint4 *>(dbase[u] + off + (m[u] << 4));
+#pragma unroll
+          for (int u = 0; u < U; ++u) xv[u] = gather_x<FIN, XB>(smem, (blk[u].y << l2rb) + lane_off);
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const uint32_t bb = go_right<FIN, XB>(blk[u].x, xv[u]);
+            lv[u] = __uint_as_float(bb ? blk[u].w : blk[u].z);
+            m[u] = 2u * m[u] + bb;
+          }
+        } else if (!LEAVES) {
+          constexpr int off = deep_pair_off(TL, NP) - (4 << D);
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            lv[u] = *reinterpret_cast<const float *>(dbase[u] + off + (m[u] << 2));
+        }
+      } else if (!LEAVES) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          lv[u] = *reinterpret_cast<const float *>(a.nodes + base[u] + kLeafOff + (m[u] << 2));
+      }
       if (LEAVES) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -152,10 +224,6 @@ __global__ __launch_bounds__(1024) void perfect_global_kernel(LaunchArgs a) {
                 a.leaf_map[(int64_t)(q + u) * (1 << D) + (m[u] - kFirstLeaf)];
         }
       } else {
-        float lv[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          lv[u] = *reinterpret_cast<const float *>(a.nodes + base[u] + kLeafOff + (m[u] << 2));
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           if (q + u < t_end) {
@@ -202,6 +270,13 @@ static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int l
                              void *stream) {
   const int threads = 64 * waves;
   if constexpr (D > 4) {
+    if (a.top_levels == 4 && !a.vec && a.deep && waves <= 8) {  // 8 trees per lane, deep blocks
+      if (a.out_leaf)
+        return launch_common(perfect_global_kernel<D, 8, true, FIN, XB, 0, 4, true>, threads,
+                             n_wg, lds_bytes, stream, a);
+      return launch_common(perfect_global_kernel<D, 8, false, FIN, XB, 0, 4, true>, threads,
+                           n_wg, lds_bytes, stream, a);
+    }
     if (a.top_levels == 4 && !a.vec) {  // 8 trees per lane
       if (a.out_leaf)
         return launch_common(perfect_global_kernel<D, 8, true, FIN, XB, 0, 4>, threads, n_wg,
@@ -211,6 +286,13 @@ static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int l
     }
   }
   if constexpr (D > 3) {
+    if (a.top_levels == 3 && !a.vec && a.deep && waves <= 8) {  // 16 trees per lane, deep blocks
+      if (a.out_leaf)
+        return launch_common(perfect_global_kernel<D, 16, true, FIN, XB, 0, 3, true>, threads,
+                             n_wg, lds_bytes, stream, a);
+      return launch_common(perfect_global_kernel<D, 16, false, FIN, XB, 0, 3, true>, threads,
+                           n_wg, lds_bytes, stream, a);
+    }
     if (a.top_levels == 3 && !a.vec) {  // 16 trees per lane
       if (a.out_leaf)
         return launch_common(perfect_global_kernel<D, 16, true, FIN, XB, 0, 3>, threads, n_wg,

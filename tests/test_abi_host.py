@@ -450,3 +450,118 @@ def test_create_without_gpu_reports_device_error():
     with pytest.raises(B.BridgerError) as e:
         B.Forest(_tiny())
     assert e.value.status == B.BRIDGER_ERR_DEVICE
+
+
+def _deep_tree_bytes(D, TL):
+    pairs = sum(16 << (TL + 2 * j) for j in range((D - TL) // 2))
+    return pairs + ((16 << (D - 1)) if (D - TL) & 1 else (4 << D))
+
+
+def walk_perfect_deep(f: B.Forest, X, D, TL, bins=None):
+    """The wide-row perfect walk: the first TL levels from the packed records (the LDS copies
+    hold the same records), then the deep blocks (packed array 8; with bins, array 9, whose
+    w fields are ranks and a row goes right iff its bin exceeds the rank)."""
+    blob = B.bridger_forest_packed(f.handle, 0, np.uint8)
+    deep = B.bridger_forest_packed(f.handle, 9 if bins is not None else 8, np.uint8)
+    leaf_map = B.bridger_forest_packed(f.handle, 2, np.int32)
+    order = B.bridger_forest_packed(f.handle, 3, np.int32)
+    T = f.n_trees
+    tb, dtb = blob.size // T, deep.size // T
+    assert dtb == _deep_tree_bytes(D, TL), (D, TL, dtb)
+    n = X.shape[0]
+    rows = np.arange(n)
+    leaves = np.empty((n, T), np.int32)
+    vals = np.empty((n, T), np.float32)
+
+    def right(w, x_or_bin):
+        if bins is not None:
+            return (x_or_bin > w.astype(np.int64)).astype(np.int64)
+        return np.where(x_or_bin <= w.view(np.float32), 0, 1)
+
+    V = bins if bins is not None else X
+    for k in range(T):
+        blk = blob[k * tb:(k + 1) * tb]
+        thr = blk[:8 << D].view(np.float32)[0::2]
+        feat = blk[:8 << D].view(np.uint32)[1::2]
+        m = np.ones(n, np.int64)
+        for _ in range(TL):   # top levels: fp32 thresholds of the records (bins: ranks below)
+            if bins is None:
+                m = 2 * m + np.where(X[rows, feat[m]] <= thr[m], 0, 1)
+            else:
+                ranks = {i: _rank(f, int(feat[i]), thr[i]) for i in np.unique(m)}
+                w = np.array([ranks[i] for i in m], np.uint32)
+                m = 2 * m + right(w, bins[rows, feat[m]])
+        d_blk = deep[k * dtb:(k + 1) * dtb].view(np.uint32)
+        off = 0
+        d = TL
+        while D - d >= 2:
+            q = d_blk[off // 4:off // 4 + (4 << d)].reshape(-1, 4)[m - (1 << d)]
+            b1 = right(q[:, 0].copy(), V[rows, q[:, 3] & 1023])
+            w2 = np.where(b1 == 1, q[:, 2], q[:, 1]).astype(np.uint32)
+            f2 = (q[:, 3] >> np.where(b1 == 1, 20, 10).astype(np.uint32)) & 1023
+            b2 = right(w2, V[rows, f2])
+            m = 4 * m + 2 * b1 + b2
+            off += 16 << d
+            d += 2
+        if d == D - 1:
+            q = d_blk[off // 4:off // 4 + (4 << d)].reshape(-1, 4)[m - (1 << d)]
+            b = right(q[:, 0].copy(), V[rows, q[:, 1]])
+            lv = np.where(b == 1, q[:, 3], q[:, 2]).view(np.float32)
+            m = 2 * m + b
+        else:
+            assert d == D
+            lv = d_blk[off // 4:off // 4 + (1 << D)].view(np.float32)[m - (1 << D)]
+        leaves[:, order[k]] = leaf_map[k * (1 << D) + m - (1 << D)]
+        vals[:, order[k]] = lv
+    return leaves, vals
+
+
+def _rank(f: B.Forest, feat: int, t: float) -> int:
+    """A threshold's rank among its feature's binning thresholds (packed arrays 5 and 6)."""
+    q = B.bridger_forest_packed(f.handle, 5, np.float32)
+    qo = B.bridger_forest_packed(f.handle, 6, np.int32)
+    u = q[qo[feat]:qo[feat + 1]]
+    return int(np.searchsorted(u, np.float32(t) + np.float32(0.0), side="left"))
+
+
+@pytest.mark.parametrize("D,F,levels", [(4, 7, "3"), (5, 9, "3"), (6, 28, "3"), (7, 5, "3"),
+                                        (8, 784, "3"), (8, 1024, "4"), (9, 12, "4"), (10, 3, "3")])
+def test_perfect_deep_blocks(D, F, levels, monkeypatch):
+    """The deep blocks of the wide-row perfect kernel (pairs of levels in one 16-byte block,
+    the last level with its leaf values, or a leaf array) walked on the CPU reach the oracle's
+    leaves and values: fp32 rows with ties, signed zeros, infinities and NaN, and bins."""
+    monkeypatch.setenv("BRIDGER_PERFECT_TOP_LEVELS", levels)
+    rng = np.random.default_rng(D * 100 + F)
+    T = 9
+    n_int = (1 << D) - 1
+    grid = np.array([-1.0, -0.0, 0.0, 0.5, 1.0, np.inf], np.float32)
+    trees = [perfect_tree_arrays(D, rng.integers(0, F, n_int),
+                                 rng.choice(grid, n_int).astype(np.float32),
+                                 rng.standard_normal(1 << D).astype(np.float32))
+             for _ in range(T)]
+    model = permute_nodes(concat_trees(trees, F), rng)
+    X = rng.choice(np.array([-2.0, -1.0, -0.0, 0.0, 0.5, 1.0, 3.0, np.inf, -np.inf, np.nan],
+                            np.float32), (200, F))
+    _, ref_lv, _ = oracle.predict(model, X, want_leaves=True)
+    ref_val = model.value[model.tree_offsets[:-1][None, :] + ref_lv]
+    with host(model) as f:
+        assert f.kernel == B.BRIDGER_KERNEL_PERFECT
+        lv, vals = walk_perfect_deep(f, X, D, int(levels))
+        assert np.array_equal(lv, ref_lv)
+        assert np.array_equal(vals, ref_val.astype(np.float32))
+        from oracle import binning
+        bins = binning.bin_rows(binning.tables(model), X)
+        lv, vals = walk_perfect_deep(f, X, D, int(levels), bins=bins)
+        assert np.array_equal(lv, ref_lv)
+        assert np.array_equal(vals, ref_val.astype(np.float32))
+
+
+def test_perfect_deep_blocks_absent():
+    """More than 1024 features or vector leaves: no deep blocks (the kernel reads every level
+    from the records)."""
+    rng = np.random.default_rng(3)
+    trees = [perfect_tree_arrays(6, rng.integers(0, 1100, 63), rng.standard_normal(63).astype(np.float32),
+                                 rng.standard_normal(64).astype(np.float32)) for _ in range(3)]
+    with host(concat_trees(trees, 1100)) as f:
+        with pytest.raises(B.BridgerError):
+            B.bridger_forest_packed(f.handle, 8, np.uint8)

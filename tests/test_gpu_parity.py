@@ -254,6 +254,7 @@ VARIANT_ENVS = [
     {"BRIDGER_GLOBAL": "1", "BRIDGER_NO_SIGN_STEP": "1"},      # (top 3 levels from LDS copies)
     {"BRIDGER_GLOBAL": "1", "BRIDGER_PERFECT_TOP_LEVELS": "4"},  # top 4 levels, 8 trees a lane
     {"BRIDGER_GLOBAL": "1", "BRIDGER_TOPS": "0"},              # every level from global memory
+    {"BRIDGER_GLOBAL": "1", "BRIDGER_DEEP": "0"},              # top levels, then one record a level
     {"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "8", "BRIDGER_ROWS": "32"},    # 2 groups a wave
     {"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "8", "BRIDGER_ROWS": "128"},   # groups of 2 waves
     {"BRIDGER_NO_FIXED": "1"},                                 # run-time chunk geometry
