@@ -43,7 +43,8 @@ def test_calibration_library_exports_its_symbols():
     assert headers == ["bridger.h", "bridger_calib.h"]
     lib = ctypes.CDLL(os.path.join(os.path.dirname(B.LIB_PATH), "libbridger_calib.so"))
     names = declared_functions(os.path.join(ROOT, "include", "bridger_calib.h"))
-    assert set(names) == {"bridger_calib_device", "bridger_calib_lds_gather", "bridger_calib_copy"}
+    assert set(names) == {"bridger_calib_device", "bridger_calib_lds_gather",
+                          "bridger_calib_global_gather", "bridger_calib_copy"}
     missing = [n for n in names if not hasattr(lib, n)]
     assert not missing, missing
 
