@@ -308,10 +308,13 @@ static int launch_bin_stream(const LaunchArgs &a0, void *stream) {
 
 // Runs of table staging per feature group decide the kernel: with one or two runs the stream
 // kernel (1,024 lanes, many searches in flight, a second read of the rows from L2) is the
-// faster (16-bit bins of 1M x 28 rows: 0.138 against 0.276 ms); with more runs its re-reads of
-// X go to memory (7.3x the rows' bytes read and 4.0x the bins written for 4M x 256 rows with
-// about six runs a group), and the row kernel, which reads X and writes the bins once, is the
-// faster (8.7 against 9.5 ms).  a.n_chunks carries the largest number of runs of any group.
+// faster (16-bit bins of 1M x 28 rows: 0.138 against 0.276 ms), and so it is with more runs
+// while the rows fit the last-level cache that serves its re-reads (1M x 28 rows, five runs:
+// 0.167 against 0.323 ms); with more runs over larger rows its re-reads of X go to memory (7.3x
+// the rows' bytes read and 4.0x the bins written for 4M x 256 rows with seven runs a group),
+// and the row kernel, which reads X and writes the bins once, is the faster (8.7 against
+// 9.5 ms).  The host passes a.n_chunks = the largest number of runs of any group when it
+// wants the row kernel, else 1.
 int launch_bin(const LaunchArgs &a, void *stream) {
   return a.n_chunks > 2 ? launch_bin_rows(a, stream) : launch_bin_stream(a, stream);
 }

@@ -46,6 +46,7 @@ constexpr int kMaxWavesPerCU = 32;
 constexpr double kL2BytesPerXcd = 4.0 * 1024 * 1024;
 constexpr int kMinWavesPerCU = 8;
 constexpr int kNumCUs = 256;
+constexpr int64_t kLastLevelCacheBytes = int64_t(256) << 20;  // MI355X Infinity Cache
 // Latency terms for small batches, where a workgroup's walk over its share of the trees, not
 // the throughput of the LDS, sets the time: one dependent LDS gather (two per level, and the
 // leaf), and the barrier and L2 round trip of a chunk.  Fitted by least squares to batches
@@ -1723,8 +1724,12 @@ bridger_status bridger_forest_bin(bridger_forest_t h, const float *X, int64_t n_
         }
         max_runs = std::max(max_runs, runs);
       }
-      a.n_chunks = env_int("BRIDGER_BIN_KERNEL", 0) == 1 ? 3
-                   : env_int("BRIDGER_BIN_KERNEL", 0) == 2 ? 1 : max_runs;
+      // the row kernel when the stream kernel's re-reads of the rows (one per run) would miss
+      // the last-level cache: more than two runs and more row bytes than the cache holds
+      const bool rows_kernel = max_runs > 2 && nr * (int64_t)h->F * 4 > kLastLevelCacheBytes;
+      const int force = env_int("BRIDGER_BIN_KERNEL", 0);
+      a.n_chunks = force == 1 ? std::max(max_runs, 3)
+                   : force == 2 ? 1 : rows_kernel ? max_runs : 1;
     }
     set_preprocess_args(h, a);
     RowNorms norms;
