@@ -144,16 +144,16 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     }
     return;
   }
+  // With acc_alias the sums below go into the row tile: the last chunk's barrier above has
+  // already seen every group finish its walk, so the tile is free.
   if (KS) {
 #pragma unroll
     for (int c = 0; c < KS; ++c)
       if (c == ca.k) cs[c] = ca.acc;
-    if (a.acc_alias) __syncthreads();  // the sums go into the row tile: every group is done
 #pragma unroll
     for (int c = 0; c < KS; ++c)
       if (c < a.K) acc_lds[c * slot_stride] = cs[c];
   } else if (VK_REG) {
-    if (a.acc_alias) __syncthreads();  // the sums go into the row tile: every group is done
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
