@@ -480,6 +480,7 @@ struct PlanInput {
   int32_t x_bytes = 4;     // element of the LDS tile: 4 (fp32) or 2 / 1 (bins)
   bool vec = false;        // vector leaves
   int32_t depth = 0;       // PERFECT: the trees' depth
+  bool deep = false;       // PERFECT: deep blocks exist (wide-row plans may use them)
 };
 
 // Smallest tile: bins pack 4 / x_bytes rows per 32-bit word and a half-wave's 32 rows must
@@ -655,7 +656,21 @@ int top_levels_default() {
 // trees per lane spill registers); BRIDGER_PERFECT_TOP_LEVELS overrides.
 int perfect_top_levels() {
   const int l = env_int("BRIDGER_PERFECT_TOP_LEVELS", kPerfectTopLevels);
-  return (l == 3 || l == 4) ? l : kPerfectTopLevels;
+  return (l >= 3 && l <= 5) ? l : kPerfectTopLevels;
+}
+
+// Bytes of a lane group's copy of top levels: 1 KB (3 levels of 16 trees, 4 of 8), 2 KB (4
+// levels of 16 trees, 5 of 8; with deep blocks only).
+int perfect_top_group_bytes(int L, bool deep) {
+  if (!deep) return 1024;
+  if (L == 5) return 2048;
+  return env_int("BRIDGER_TOP_GROUP_KB", 1) == 2 ? 2048 : 1024;
+}
+
+// Deep blocks: scalar leaves, feature indices in 10 bits, trees deeper than the top levels.
+bool deep_possible(bool vec, int F, int depth) {
+  return env_int("BRIDGER_DEEP", 1) != 0 && !vec && F <= kDeepMaxFeatures &&
+         depth > perfect_top_levels();
 }
 
 // tops: the RAGGED variant whose top levels come from per-wave LDS copies (one class, scalar
@@ -676,13 +691,18 @@ Plan choose_global_plan(const PlanInput &in, bool tops = false) {
       const int G = 64 * W / R;
       if (G > 1 && (int64_t)G * 4 > in.n_trees) continue;  // a few trees per lane group
       if (tops && !in.perfect && R < 64) continue;         // a group is whole waves
-      // PERFECT top levels: 1 KB per lane group of each wave (a wave holds 64 / R groups when
-      // R < 64), besides the class sums
+      // PERFECT top levels: 1 or 2 KB per lane group of each wave (a wave holds 64 / R groups
+      // when R < 64), besides the class sums, which the deep-block kernel keeps in registers
+      // (at most 16 classes) and writes into the row tile after the walk
+      const bool deep = tops && in.perfect && in.deep && W <= 8;
+      const int gb = perfect_top_group_bytes(perfect_top_levels(), deep);
+      const int64_t tile = (int64_t)in.F * R * in.x_bytes;
+      const int64_t acc = (int64_t)in.K * G * R * 8;
+      const bool alias = deep && in.K <= 16 && acc <= tile && env_int("BRIDGER_REG_SUMS", 1) != 0;
       const int64_t top_bytes_wg =
-          !tops ? 0 : in.perfect ? (int64_t)W * std::max(1, 64 / R) * 1024
+          !tops ? 0 : in.perfect ? (int64_t)W * std::max(1, 64 / R) * gb
                                  : (int64_t)W * kTopWaveBytes;
-      const int64_t lds = (int64_t)in.F * R * in.x_bytes + top_bytes_wg +
-                          (tops && !in.perfect ? 0 : (int64_t)in.K * G * R * 8);
+      const int64_t lds = tile + top_bytes_wg + ((tops && !in.perfect) || alias ? 0 : acc);
       if (lds > kLdsBytesPerCU) continue;
       const int m = (int)std::min<int64_t>(kLdsBytesPerCU / lds, kMaxWavesPerCU / W);
       if (m < 1) continue;
@@ -695,6 +715,8 @@ Plan choose_global_plan(const PlanInput &in, bool tops = false) {
       p.ilp = env_int("BRIDGER_ILP", 8) == 4 ? 4 : 8;  // L2 round trips: keep 8 in flight
       p.global_nodes = 1;
       p.tops = !tops ? 0 : in.perfect ? perfect_top_levels() : top_levels_default();
+      p.acc_alias = alias ? 1 : 0;
+      p.top_group_bytes = tops && in.perfect ? gb : 0;
       p.waves_per_cu = m * W;
       const double n = (double)std::max<int64_t>(in.n_rows, 1);
       p.hbm_bytes = n * in.F * 4 + n * in.K * 4 + in.forest_bytes;
@@ -880,15 +902,15 @@ void make_perfect_deep(const bridger_forest *h, int TL, bool binned, std::vector
 
 // The deep blocks serve the wide-row plans whose top levels come from LDS copies.
 bool deep_wanted(const bridger_forest *h) {
-  return env_int("BRIDGER_DEEP", 1) != 0 && !h->vec && h->F <= kDeepMaxFeatures &&
-         h->perfect_depth > perfect_top_levels();
+  return deep_possible(h->vec, h->F, h->perfect_depth);
 }
 
 bool same_plan(const Plan &a, const Plan &b) {
   return a.waves == b.waves && a.rows_per_wg == b.rows_per_wg && a.groups == b.groups &&
          a.chunk_bytes == b.chunk_bytes && a.trees_per_chunk == b.trees_per_chunk &&
          a.n_chunks == b.n_chunks && a.lds_bytes == b.lds_bytes && a.ilp == b.ilp &&
-         a.global_nodes == b.global_nodes && a.acc_alias == b.acc_alias && a.tops == b.tops;
+         a.global_nodes == b.global_nodes && a.acc_alias == b.acc_alias && a.tops == b.tops &&
+         a.top_group_bytes == b.top_group_bytes;
 }
 
 // PERFECT plans for the batch-size classes that differ from the large-batch plan `big`, each
@@ -1260,11 +1282,19 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
     if (h->kernel_active == kPerfect && p.global_nodes) {
       if (p.tops) {  // after the row tile and the class sums
         a.top_levels = p.tops;
+        a.top_group_bytes = p.top_group_bytes;
         a.lds_top_off = a.lds_acc_off + h->K * p.groups * p.rows_per_wg * 8;
         void *deep = binned ? h->d_perfect_bdeep : h->d_perfect_deep;
         if (deep && p.tops == h->deep_tl) {
           a.deep = (const uint8_t *)deep;
           a.deep_tree_bytes = deep_tree_bytes(h->perfect_depth, p.tops);
+        }
+        if (p.acc_alias) {  // class sums in registers, then into the row tile: no sum area
+          if (!a.deep)
+            return fail(BRIDGER_ERR_DEVICE, "plan without the deep blocks it was made for");
+          a.acc_alias = 1;
+          a.lds_acc_off = a.lds_x_off;
+          a.lds_top_off = a.lds_x_off + h->F * p.rows_per_wg * xsz;
         }
       }
       err = launch_perfect_global(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
@@ -1497,6 +1527,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
       pin.vec = vec;
       pin.depth = D;
+      pin.deep = deep_possible(vec, n_features, D);
       h->perfect_plan = pick_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
       if (h->perfect_ok) {
@@ -1529,6 +1560,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
                       h->perfect_tree_bytes, true, visits, h->bin_bytes};
         pin.vec = vec;
         pin.depth = D;
+        pin.deep = deep_possible(vec, n_features, D);
         h->perfect_bplan = pick_plan(pin);
         h->perfect_bok = h->perfect_bplan.waves > 0;
         if (h->perfect_bok) {

@@ -111,7 +111,9 @@ struct Plan {
   int32_t acc_alias;       // class sums written after the walk into the row tile's LDS
   int32_t tops;            // RAGGED global: 0, or L, the top levels read from a per-wave LDS
                            // copy (after the row tile, kTopWaveBytes per wave, which then
-                           // holds the group sums)
+                           // holds the group sums); PERFECT global: the top levels read from
+                           // per-lane-group LDS copies
+  int32_t top_group_bytes; // PERFECT global with tops: bytes of one lane group's copy (1 or 2 KB)
   double hbm_bytes, stage_bytes, lds_read_bytes, est_seconds;
 };
 
@@ -170,6 +172,7 @@ struct LaunchArgs {
   int32_t lds_top_off;         // byte offset of the per-wave top-level copies in dynamic LDS
   const uint8_t *deep;         // PERFECT deep blocks of the top_levels plan, or nullptr
   int32_t deep_tree_bytes;     // their bytes per kernel tree (deep_tree_bytes(D, top_levels))
+  int32_t top_group_bytes;     // PERFECT global: bytes of a lane group's top-level copy
 };
 
 // Vector leaves: floats per leaf in leaf_vec, K rounded up to whole 16-byte groups.

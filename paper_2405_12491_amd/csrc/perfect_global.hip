@@ -25,12 +25,17 @@ __device__ __forceinline__ uint32_t go_right(uint32_t w, uint32_t x) {
 // DEEP: below the top levels the walk reads the deep blocks (layout in internal.h): one
 // 16-byte load per pair of levels, and the last level's block carries its two leaf values.
 // DEEP holds 16 blocks of 16 bytes per lane: workgroups of at most 8 waves, so that a lane may
-// use 256 registers.
-template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0, bool DEEP = false>
+// use 256 registers.  GB: bytes of a lane group's top-level copy (one batch of U trees).  KS:
+// scalar leaves of at most KS classes with the group's class sums in registers, written only
+// after the walk into the row tile's LDS (acc_alias), which leaves the LDS to the tile and
+// the top-level copies during the walk.
+template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0, bool DEEP = false,
+          int GB = 1024, int KS = 0>
 __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(LaunchArgs a) {
-  static_assert(TL == 0 || (VK == 0 && U * (8 << TL) == 1024 && TL < D),
-                "top levels: scalar leaves, one lane group's batch in 1 KB");
+  static_assert(TL == 0 || (VK == 0 && U * (8 << TL) == GB && TL < D && GB % 1024 == 0),
+                "top levels: scalar leaves, one lane group's batch in GB bytes");
   static_assert(!DEEP || TL > 0, "deep blocks follow LDS top levels");
+  static_assert(KS == 0 || (TL > 0 && !LEAVES), "register class sums: the top-level walk");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr bool VK_REG = VK == 4 || VK == 8;  // vector leaves, class sums in registers
   constexpr int VR = VK_REG ? VK : 4;
@@ -59,6 +64,28 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
   double vacc[VR];
   if (VK_REG) vec_init_reg(a, vacc, g == 0);
   if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
+  // KS: a group's trees are contiguous and class-sorted, so each class is summed in one
+  // stretch; the running sum moves into cs[k] when the class changes
+  double cs[KS > 0 ? KS : 1];
+  if (KS) {
+#pragma unroll
+    for (int c = 0; c < KS; ++c) cs[c] = c < a.K ? class_init(a, c, g == 0) : 0.0;
+  }
+  auto advance_reg = [&](int t) {
+    if (t < ca.next_b) return;
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c == ca.k) cs[c] = ca.acc;
+    while (t >= ca.next_b) {
+      ca.k += 1;
+      ca.next_b = a.class_begin[ca.k + 1];
+    }
+    double v = 0.0;
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c == ca.k) v = cs[c];
+    ca.acc = v;
+  };
 
   auto finish = [&](auto &m, int q) {
     constexpr int N = sizeof(m) / sizeof(m[0]);
@@ -104,9 +131,9 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
     const int gpw = R < 64 ? 64 / R : 1;              // lane groups per wave
     const int gi = R < 64 ? lane / R : 0;             // this lane's group within the wave
     const int gw0 = __builtin_amdgcn_readfirstlane((wave * 64) / R);  // the wave's first group
-    const uint32_t wave_bytes = (uint32_t)gpw * U * TBT;
+    const uint32_t wave_bytes = (uint32_t)gpw * GB;
     const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * wave_bytes;
-    static_assert(U * TBT == 1024, "one lane group's batch is one 16-byte-per-lane load");
+    static_assert(U * TBT == GB, "one lane group's batch is GB / 1024 16-byte-per-lane loads");
     const int NB = ((T + G - 1) / G + U - 1) / U;     // batches of the largest group
     // the tree ranges of the wave's (at most two) lane groups
     int cb0[2], cb1[2];
@@ -116,18 +143,21 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
       cb0[i] = (int)(((int64_t)T * gc) / G);
       cb1[i] = (int)(((int64_t)T * (gc + 1)) / G);
     }
-    constexpr int LPT = (int)TBT / 16;                 // lanes per tree of the copy
-    const int cu = lane / LPT;                         // tree of the batch this lane copies
-    const uint32_t cpos = (uint32_t)(lane % LPT) * 16; // and its 16 bytes of that tree's levels
+    constexpr int LPT = (int)TBT / 16;                 // 16-byte pieces per tree of the copy
     auto copy_batch = [&](int j) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         if (i < gpw) {
-          const int t = min(cb0[i] + j * U + cu, cb1[i] - 1);
-          __builtin_amdgcn_global_load_lds(
-              (const void *)(a.nodes + (size_t)t * tb + cpos),
-              (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf + i * 1024u), 16,
-              0, 0);
+#pragma unroll
+          for (int k = 0; k < GB / 1024; ++k) {
+            const int piece = k * 64 + lane;           // this lane's piece of the batch
+            const int t = min(cb0[i] + j * U + piece / LPT, cb1[i] - 1);
+            __builtin_amdgcn_global_load_lds(
+                (const void *)(a.nodes + (size_t)t * tb + (uint32_t)(piece % LPT) * 16),
+                (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf +
+                                                           (uint32_t)i * GB + k * 1024u),
+                16, 0, 0);
+          }
         }
       }
     };
@@ -142,7 +172,7 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
         m[u] = 1u;
         base[u] = (size_t)min(q + u, t_end - 1) * tb;
       }
-      const uint32_t lbuf = buf + (uint32_t)gi * U * TBT;
+      const uint32_t lbuf = buf + (uint32_t)gi * GB;
 #pragma unroll
       for (int d = 0; d < (DEEP ? TL : D); ++d) {
         uint2 rec[U];
@@ -227,7 +257,8 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           if (q + u < t_end) {
-            class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
+            if (KS) advance_reg(q + u);
+            else class_advance(a, ca, q + u, acc_lds, slot_stride, g == 0);
             ca.acc += (double)lv[u];
           }
         }
@@ -247,7 +278,17 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
     }
   }
   if (LEAVES) return;
-  if (VK_REG) {
+  if (KS) {
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c == ca.k) cs[c] = ca.acc;
+    // the sums go into the row tile's LDS: every group must be done with the tile (no copy of
+    // top levels is in flight after the last batch)
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < KS; ++c)
+      if (c < a.K) acc_lds[c * slot_stride] = cs[c];
+  } else if (VK_REG) {
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
@@ -265,18 +306,49 @@ __global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(Launc
 }
 
 // ---------------------------------------------------------------------- launchers
+// The deep-block walk: top levels TL and group copies of GB bytes (3 levels of 16 trees in
+// 1 KB; 4 levels of 16 trees or 5 of 8 in 2 KB), class sums in registers (acc_alias) or LDS.
+template <int D, bool FIN, int XB, int TL, int GB>
+static int launch_global_deep_tg(const LaunchArgs &a, int threads, int64_t n_wg, int lds_bytes,
+                                 void *stream) {
+  constexpr int U = GB / (8 << TL);
+  if constexpr (TL < D && (U == 8 || U == 16)) {
+    if (a.out_leaf)
+      return launch_common(perfect_global_kernel<D, U, true, FIN, XB, 0, TL, true, GB>, threads,
+                           n_wg, lds_bytes, stream, a);
+    if (a.acc_alias)
+      return launch_common(perfect_global_kernel<D, U, false, FIN, XB, 0, TL, true, GB, 16>,
+                           threads, n_wg, lds_bytes, stream, a);
+    return launch_common(perfect_global_kernel<D, U, false, FIN, XB, 0, TL, true, GB>, threads,
+                         n_wg, lds_bytes, stream, a);
+  } else {
+    return (int)hipErrorInvalidValue;
+  }
+}
+
+template <int D, bool FIN, int XB>
+static int launch_global_deep(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                              void *stream) {
+  const int threads = 64 * waves;
+  const int gb = a.top_group_bytes ? a.top_group_bytes : 1024;
+  if (a.top_levels == 3 && gb == 1024)
+    return launch_global_deep_tg<D, FIN, XB, 3, 1024>(a, threads, n_wg, lds_bytes, stream);
+  if (a.top_levels == 4 && gb == 1024)
+    return launch_global_deep_tg<D, FIN, XB, 4, 1024>(a, threads, n_wg, lds_bytes, stream);
+  if (a.top_levels == 4 && gb == 2048)
+    return launch_global_deep_tg<D, FIN, XB, 4, 2048>(a, threads, n_wg, lds_bytes, stream);
+  if (a.top_levels == 5 && gb == 2048)
+    return launch_global_deep_tg<D, FIN, XB, 5, 2048>(a, threads, n_wg, lds_bytes, stream);
+  return (int)hipErrorInvalidValue;
+}
+
 template <int D, bool FIN, int XB>
 static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                              void *stream) {
   const int threads = 64 * waves;
+  if (a.top_levels && !a.vec && a.deep && waves <= 8)
+    return launch_global_deep<D, FIN, XB>(a, waves, n_wg, lds_bytes, stream);
   if constexpr (D > 4) {
-    if (a.top_levels == 4 && !a.vec && a.deep && waves <= 8) {  // 8 trees per lane, deep blocks
-      if (a.out_leaf)
-        return launch_common(perfect_global_kernel<D, 8, true, FIN, XB, 0, 4, true>, threads,
-                             n_wg, lds_bytes, stream, a);
-      return launch_common(perfect_global_kernel<D, 8, false, FIN, XB, 0, 4, true>, threads,
-                           n_wg, lds_bytes, stream, a);
-    }
     if (a.top_levels == 4 && !a.vec) {  // 8 trees per lane
       if (a.out_leaf)
         return launch_common(perfect_global_kernel<D, 8, true, FIN, XB, 0, 4>, threads, n_wg,
@@ -286,13 +358,6 @@ static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int l
     }
   }
   if constexpr (D > 3) {
-    if (a.top_levels == 3 && !a.vec && a.deep && waves <= 8) {  // 16 trees per lane, deep blocks
-      if (a.out_leaf)
-        return launch_common(perfect_global_kernel<D, 16, true, FIN, XB, 0, 3, true>, threads,
-                             n_wg, lds_bytes, stream, a);
-      return launch_common(perfect_global_kernel<D, 16, false, FIN, XB, 0, 3, true>, threads,
-                           n_wg, lds_bytes, stream, a);
-    }
     if (a.top_levels == 3 && !a.vec) {  // 16 trees per lane
       if (a.out_leaf)
         return launch_common(perfect_global_kernel<D, 16, true, FIN, XB, 0, 3>, threads, n_wg,

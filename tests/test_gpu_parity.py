@@ -168,6 +168,32 @@ def test_adversarial_values(F, grid_name, monkeypatch):
                                      f"{B.KERNEL_NAMES[k]}", forest=f)
 
 
+@pytest.mark.parametrize("deep", ["1", "0"])
+@pytest.mark.parametrize("grid_name", list(THRESHOLD_GRIDS))
+@pytest.mark.parametrize("F", [7, 28])
+def test_adversarial_values_global(F, grid_name, deep, monkeypatch):
+    """The same values through the global-node perfect kernel (top levels from LDS copies),
+    with and without the deep blocks: both level steps (finite thresholds: sign of the
+    difference; infinite ones: compare) on depths whose deep levels end in a block with leaf
+    values (4, 8) and in a leaf array (5, 7)."""
+    monkeypatch.setenv("BRIDGER_GLOBAL", "1")
+    monkeypatch.setenv("BRIDGER_DEEP", deep)
+    rng = np.random.default_rng(200 + F)
+    grid = np.array(THRESHOLD_GRIDS[grid_name], np.float32)
+    for D in (4, 5, 7, 8):
+        n_int = (1 << D) - 1
+        model = concat_trees([perfect_tree_arrays(D, rng.integers(0, F, n_int),
+                                                  grid[rng.integers(0, len(grid), n_int)],
+                                                  rng.standard_normal(1 << D).astype(np.float32))
+                              for _ in range(9)], F)
+        X = _adversarial_rows(F, grid, rng, n=700)
+        with B.Forest(model) as f:
+            print(f"[adversarial-global] F={F} D={D} {grid_name} deep={deep} "
+                  f"plan={f.plan(X.shape[0])}", flush=True)
+            check_parity(model, X, B.BRIDGER_KERNEL_PERFECT,
+                         f"adversarial global F={F} D={D} {grid_name} deep={deep}", forest=f)
+
+
 def test_unaligned_rows():
     """X starting 4 bytes past a 16-byte boundary takes the scalar row-load path."""
     import torch
@@ -375,7 +401,11 @@ def test_global_class_slots(family, env, monkeypatch):
                 assert p["rows_per_wg"] == R and p["chunk_bytes"] == 0
                 tile, slots = F * R * 4, G * K * R * 8
                 if family == "perfect":
-                    allowed = (tile + slots, tile + slots + W * max(1, 64 // R) * 1024)
+                    # class sums in LDS, or (deep blocks, at most 16 classes) in registers and
+                    # written into the tile after the walk; copies of 1 or 2 KB per lane group
+                    copies = [W * max(1, 64 // R) * kb for kb in (1024, 2048)]
+                    allowed = (tile + slots,) + tuple(tile + slots + c for c in copies) + \
+                        tuple(tile + c for c in copies)
                 else:
                     allowed = (tile + slots,) + ((tile + W * 1024,) if K == 1 and R >= 64 else ())
                 assert p["lds_bytes"] in allowed, (p["lds_bytes"], allowed)
