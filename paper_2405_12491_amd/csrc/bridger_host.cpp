@@ -1226,6 +1226,7 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
   a.K = h->K;
   a.aggregate = h->aggregate;
   a.transform = h->transform;
+  a.tile_coalesced = env_int("BRIDGER_COALESCED_TILE", 1) != 0 ? 1 : 0;
   RowNorms norms;
   if (!binned) {
     set_preprocess_args(h, a);

@@ -173,6 +173,7 @@ struct LaunchArgs {
   const uint8_t *deep;         // PERFECT deep blocks of the top_levels plan, or nullptr
   int32_t deep_tree_bytes;     // their bytes per kernel tree (deep_tree_bytes(D, top_levels))
   int32_t top_group_bytes;     // PERFECT global: bytes of a lane group's top-level copy
+  int32_t tile_coalesced;      // global-node RAGGED kernels: the row tile read 8 rows x 128 B a load
 };
 
 // Vector leaves: floats per leaf in leaf_vec, K rounded up to whole 16-byte groups.

@@ -279,6 +279,50 @@ __device__ __forceinline__ void load_tile_any(uint8_t *smem, const LaunchArgs &a
   }
 }
 
+// The row tile of a workgroup whose threads all load (the global-node RAGGED kernels), for dense
+// fp32 rows without preprocessing (16-byte aligned, F % 4 == 0): each wave instruction reads 8
+// rows x 128 consecutive bytes (8 lanes per row, one cache line each) instead of 64 rows x 16
+// bytes, and writes the values into the same feature-major tile.  In that tile a feature's row
+// spans the 32 banks once, so the 8 lanes of a row write to one bank: the L2 reads touch 8
+// lines instead of 64 and the LDS writes conflict 8-way.  That pays where two workgroups per
+// CU overlap one's tile load with the other's walk (4M x 256 rows: 15.02 -> 14.82 ms); with one
+// workgroup per CU waiting on its tile it does not (the 784-feature perfect forest: 0.538 ->
+// 0.572 ms), so the PERFECT kernels keep load_tile_any.  Other rows and element types take
+// load_tile_any.
+template <int XB, bool NAN_TO_INF>
+__device__ __forceinline__ void load_tile_all(uint8_t *smem, const LaunchArgs &a, int r,
+                                              int64_t row, bool row_ok, int g, int G) {
+  if constexpr (XB == 4) {
+    if (a.tile_coalesced && a.x_vec4 && !a.csr && a.pre_kind == 0) {
+      float *xt = reinterpret_cast<float *>(smem + a.lds_x_off);
+      const int R = a.rows_per_wg, F4 = a.F >> 2;
+      const int n_rb = R / 8, n_inst = n_rb * ((F4 + 7) / 8);
+      const int tid = threadIdx.x, lane = tid & 63, waves = (int)(blockDim.x >> 6);
+      const int64_t row0 = (int64_t)blockIdx.x * R;
+      const float4 *x4 = reinterpret_cast<const float4 *>(a.X);
+      for (int q = tid >> 6; q < n_inst; q += waves) {
+        const int rr = (q % n_rb) * 8 + (lane & 7), c = (q / n_rb) * 8 + (lane >> 3);
+        if (c < F4) {
+          const int64_t gr = row0 + rr;
+          float4 v = gr < a.n_rows ? x4[gr * F4 + c] : make_float4(0.f, 0.f, 0.f, 0.f);
+          if (NAN_TO_INF) {
+            v.x = (v.x != v.x) ? __builtin_inff() : v.x;
+            v.y = (v.y != v.y) ? __builtin_inff() : v.y;
+            v.z = (v.z != v.z) ? __builtin_inff() : v.z;
+            v.w = (v.w != v.w) ? __builtin_inff() : v.w;
+          }
+          xt[(4 * c + 0) * R + rr] = v.x;
+          xt[(4 * c + 1) * R + rr] = v.y;
+          xt[(4 * c + 2) * R + rr] = v.z;
+          xt[(4 * c + 3) * R + rr] = v.w;
+        }
+      }
+      return;
+    }
+  }
+  load_tile_any<XB, NAN_TO_INF>(smem, a, r, row, row_ok, g, G);
+}
+
 __device__ __forceinline__ double sigmoid_d(double z) {
   if (z >= 0.0) return 1.0 / (1.0 + exp(-z));
   const double e = exp(z);

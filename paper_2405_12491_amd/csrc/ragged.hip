@@ -142,7 +142,7 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
   const int shift = a.log2_row_bytes;
   const int T = a.n_trees;
 
-  load_tile_any<XB, false>(smem, a, r, row, row_ok, g, G);
+  load_tile_all<XB, false>(smem, a, r, row, row_ok, g, G);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
@@ -261,7 +261,7 @@ __global__ __launch_bounds__(1024) void ragged_top_kernel(LaunchArgs a) {
   const int T = a.n_trees;
   const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * kTopWaveBytes;
 
-  load_tile_any<XB, false>(smem, a, r, row, row_ok, g, G);
+  load_tile_all<XB, false>(smem, a, r, row, row_ok, g, G);
   __syncthreads();
 
   const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
