@@ -184,6 +184,17 @@ def calibrate(copy_bytes=512 << 20, reps=20):
     return out
 
 
+def calibrated_bound(calib, visits_per_s):
+    """The visit bound at this device's measured conflict-free gather rates: a visit issues one
+    64-bit node gather and one 32-bit feature gather, each wave-wide instruction taking
+    64 / rate clocks of the CU's LDS."""
+    rates = calib["lds_gather_lanes_per_clk_per_cu"]
+    clk_per_visit_wave = 64.0 / rates["b64"] + 64.0 / rates["b32"]
+    peak = N_CU * CLOCK_HZ * 64.0 / clk_per_visit_wave
+    return {"peak": peak / 1e9, "unit": "Gvisit/s", "frac": visits_per_s / peak,
+            "rates_lanes_per_clk": {"b64": rates["b64"], "b32": rates["b32"]}}
+
+
 def build_x(w, device):
     import torch
     from synth import BLOCK_ROWS, x_rows
@@ -507,6 +518,9 @@ def main():
             "unit": "Gvisit/s",
             "frac": visits_per_s / PEAK_VISITS_PER_S,
             "traffic": measured_traffic(w.name, n),
+            # the same bound at the gather rate measured in this run (conflict-free 64-bit node
+            # gathers and 32-bit feature gathers, one of each per visit)
+            "calibrated": calibrated_bound(calib, visits_per_s),
             "what": "internal-node visits per second against the on-chip gather bound: each "
                     "visit needs 2 data-dependent per-lane LDS gathers (node, feature value); a "
                     "CU's LDS serves 32 lanes/clk; 256 CUs x 2.4 GHz. The calibration object "
