@@ -651,12 +651,16 @@ int top_levels_default() {
   return (l == 4 || l == 5) ? l : kTopLevelsDefault;
 }
 
-// Top levels of the PERFECT global-node kernel read from LDS: 3 (16 trees per lane: 0.629 ms
-// on the 10-class 784-feature forest) or 4 (8 trees per lane: 0.685 ms; 2 levels with 32
-// trees per lane spill registers); BRIDGER_PERFECT_TOP_LEVELS overrides.
-int perfect_top_levels() {
-  const int l = env_int("BRIDGER_PERFECT_TOP_LEVELS", kPerfectTopLevels);
-  return (l >= 3 && l <= 5) ? l : kPerfectTopLevels;
+// Top levels of the PERFECT global-node kernel read from LDS (BRIDGER_PERFECT_TOP_LEVELS
+// overrides).  With the deep blocks, on the 10-class 784-feature forest: 4 levels of 8 trees per
+// lane in workgroups of 16 waves 0.489 ms (16-bit bins 0.370); 3 levels of 16 trees, whose
+// registers allow 8 waves, 0.536 (0.443); 4 levels of 16 trees in 2 KB copies 0.535; 5 of 8,
+// 0.551.  Without deep blocks: 3 levels 0.629, 4 levels 0.685; 2 levels with 32 trees per lane
+// spill registers.
+int perfect_top_levels(int depth) {
+  const int dflt = depth > kPerfectTopLevels ? kPerfectTopLevels : 3;
+  const int l = env_int("BRIDGER_PERFECT_TOP_LEVELS", dflt);
+  return (l >= 3 && l <= 5) ? l : dflt;
 }
 
 // Bytes of a lane group's copy of top levels: 1 KB (3 levels of 16 trees, 4 of 8), 2 KB (4
@@ -670,7 +674,7 @@ int perfect_top_group_bytes(int L, bool deep) {
 // Deep blocks: scalar leaves, feature indices in 10 bits, trees deeper than the top levels.
 bool deep_possible(bool vec, int F, int depth) {
   return env_int("BRIDGER_DEEP", 1) != 0 && !vec && F <= kDeepMaxFeatures &&
-         depth > perfect_top_levels();
+         depth > perfect_top_levels(depth);
 }
 
 // tops: the RAGGED variant whose top levels come from per-wave LDS copies (one class, scalar
@@ -694,8 +698,11 @@ Plan choose_global_plan(const PlanInput &in, bool tops = false) {
       // PERFECT top levels: 1 or 2 KB per lane group of each wave (a wave holds 64 / R groups
       // when R < 64), besides the class sums, which the deep-block kernel keeps in registers
       // (at most 16 classes) and writes into the row tile after the walk
-      const bool deep = tops && in.perfect && in.deep && W <= 8;
-      const int gb = perfect_top_group_bytes(perfect_top_levels(), deep);
+      const int tl = perfect_top_levels(in.depth);
+      const int gb_deep = perfect_top_group_bytes(tl, true);
+      const int u_deep = gb_deep / (8 << tl);  // trees per lane
+      const bool deep = tops && in.perfect && in.deep && W <= (u_deep > 8 ? 8 : 16);
+      const int gb = perfect_top_group_bytes(tl, deep);
       const int64_t tile = (int64_t)in.F * R * in.x_bytes;
       const int64_t acc = (int64_t)in.K * G * R * 8;
       const bool alias = deep && in.K <= 16 && acc <= tile && env_int("BRIDGER_REG_SUMS", 1) != 0;
@@ -714,7 +721,7 @@ Plan choose_global_plan(const PlanInput &in, bool tops = false) {
       p.acc_in_lds = 1;
       p.ilp = env_int("BRIDGER_ILP", 8) == 4 ? 4 : 8;  // L2 round trips: keep 8 in flight
       p.global_nodes = 1;
-      p.tops = !tops ? 0 : in.perfect ? perfect_top_levels() : top_levels_default();
+      p.tops = !tops ? 0 : in.perfect ? tl : top_levels_default();
       p.acc_alias = alias ? 1 : 0;
       p.top_group_bytes = tops && in.perfect ? gb : 0;
       p.waves_per_cu = m * W;
@@ -778,7 +785,7 @@ Plan pick_plan(const PlanInput &pin) {
   if (!pin.perfect) return g;
   // PERFECT trees deeper than the copied levels, scalar leaves, eight trees per lane: the top
   // levels from per-wave LDS copies when that keeps as many resident waves
-  if (!pin.vec && pin.depth > perfect_top_levels() && g.ilp == 8 &&
+  if (!pin.vec && pin.depth > perfect_top_levels(pin.depth) && g.ilp == 8 &&
       env_int("BRIDGER_TOPS", 1) != 0) {
     Plan t = choose_global_plan(pin, true);
     if (t.waves && t.waves_per_cu >= g.waves_per_cu) {
@@ -1535,7 +1542,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         build_perfect_trav(h);
         build_sized_plans(h, pin, h->perfect_plan, false);
         if (deep_wanted(h)) {
-          h->deep_tl = perfect_top_levels();
+          h->deep_tl = perfect_top_levels(h->perfect_depth);
           make_perfect_deep(h, h->deep_tl, false, h->perfect_deep);
         }
       }

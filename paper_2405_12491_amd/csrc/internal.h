@@ -51,7 +51,7 @@ constexpr int kTopWaveBytes = 1024;
 // PERFECT trees on the global-node kernel: the first L levels (default kPerfectTopLevels) of
 // each of the 1024 / 2^(L+3) trees a lane group walks at once are copied to the wave's LDS
 // (1 KB per lane group).
-constexpr int kPerfectTopLevels = 3;
+constexpr int kPerfectTopLevels = 4;
 constexpr int kTopLevelsDefault = 5;
 constexpr int top_bytes(int L) { return 8 << L; }
 constexpr int top_batch(int L) { return kTopWaveBytes / top_bytes(L); }

@@ -24,14 +24,14 @@ __device__ __forceinline__ uint32_t go_right(uint32_t w, uint32_t x) {
 // TL: 0, or the number of top levels read from per-wave LDS copies (scalar leaves only).
 // DEEP: below the top levels the walk reads the deep blocks (layout in internal.h): one
 // 16-byte load per pair of levels, and the last level's block carries its two leaf values.
-// DEEP holds 16 blocks of 16 bytes per lane: workgroups of at most 8 waves, so that a lane may
-// use 256 registers.  GB: bytes of a lane group's top-level copy (one batch of U trees).  KS:
+// DEEP with 16 trees per lane holds 16 blocks of 16 bytes per lane: workgroups of at most 8
+// waves, so that a lane may use 256 registers; with 8 trees per lane, 16-wave workgroups.  GB: bytes of a lane group's top-level copy (one batch of U trees).  KS:
 // scalar leaves of at most KS classes with the group's class sums in registers, written only
 // after the walk into the row tile's LDS (acc_alias), which leaves the LDS to the tile and
 // the top-level copies during the walk.
 template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0, bool DEEP = false,
           int GB = 1024, int KS = 0>
-__global__ __launch_bounds__(DEEP ? 512 : 1024) void perfect_global_kernel(LaunchArgs a) {
+__global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_kernel(LaunchArgs a) {
   static_assert(TL == 0 || (VK == 0 && U * (8 << TL) == GB && TL < D && GB % 1024 == 0),
                 "top levels: scalar leaves, one lane group's batch in GB bytes");
   static_assert(!DEEP || TL > 0, "deep blocks follow LDS top levels");
@@ -346,7 +346,9 @@ template <int D, bool FIN, int XB>
 static int launch_global_dfx(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                              void *stream) {
   const int threads = 64 * waves;
-  if (a.top_levels && !a.vec && a.deep && waves <= 8)
+  // 16 trees per lane: at most 8 waves (256 registers a lane); 8 trees: up to 16 waves
+  if (a.top_levels && !a.vec && a.deep &&
+      waves <= (a.top_group_bytes / (8 << a.top_levels) > 8 ? 8 : 16))
     return launch_global_deep<D, FIN, XB>(a, waves, n_wg, lds_bytes, stream);
   if constexpr (D > 4) {
     if (a.top_levels == 4 && !a.vec) {  // 8 trees per lane

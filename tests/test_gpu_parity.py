@@ -278,7 +278,10 @@ def test_classes_aggregates_transforms(agg, xform, K):
 VARIANT_ENVS = [
     {"BRIDGER_GLOBAL": "1"},                                   # records from global memory
     {"BRIDGER_GLOBAL": "1", "BRIDGER_NO_SIGN_STEP": "1"},      # (top 3 levels from LDS copies)
-    {"BRIDGER_GLOBAL": "1", "BRIDGER_PERFECT_TOP_LEVELS": "4"},  # top 4 levels, 8 trees a lane
+    {"BRIDGER_GLOBAL": "1", "BRIDGER_PERFECT_TOP_LEVELS": "3"},  # top 3 levels, 16 trees a lane
+    {"BRIDGER_GLOBAL": "1", "BRIDGER_PERFECT_TOP_LEVELS": "5"},  # top 5 levels, 8 trees (2 KB)
+    {"BRIDGER_GLOBAL": "1", "BRIDGER_TOP_GROUP_KB": "2"},      # top 4 levels, 16 trees (2 KB)
+    {"BRIDGER_GLOBAL": "1", "BRIDGER_REG_SUMS": "0"},          # class sums in LDS
     {"BRIDGER_GLOBAL": "1", "BRIDGER_TOPS": "0"},              # every level from global memory
     {"BRIDGER_GLOBAL": "1", "BRIDGER_DEEP": "0"},              # top levels, then one record a level
     {"BRIDGER_GLOBAL": "1", "BRIDGER_WAVES": "8", "BRIDGER_ROWS": "32"},    # 2 groups a wave
