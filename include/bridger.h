@@ -329,8 +329,14 @@ bridger_status bridger_forest_plan(bridger_forest_t h, int64_t n_rows, int32_t *
  * thresholds (9): per kernel tree, levels taken in pairs, one 16-byte block {w(m), w(2m),
  * w(2m + 1), f(m) | f(2m) << 10 | f(2m + 1) << 20} per node m of a pair's upper level, then
  * either one block {w(m), f(m), leaf value of 2m, of 2m + 1} per node of the last level or
- * the 2^D leaf values (absent with vector leaves or more than 1024 features).  *ptr stays
- * valid until destroy or set_kernel.
+ * the 2^D leaf values (absent with vector leaves or more than 1024 features), 10 the ragged
+ * trees' two-level treelets (16 bytes a slot: a 4-ary heap per tree, slot s holding a node of
+ * an even level and its two children, {w(n), v(c0), v(c1), f(n) | f(c0) << 10 | f(c1) << 20 |
+ * leaf(c0) << 30 | leaf(c1) << 31}, v the child's threshold or leaf value; the grandchild of
+ * steps b1, b2 in slot 4s + 1 + 2 b1 + b2; a leaf n as {0, v(n), v(n), 3 << 30}), 11 each
+ * kernel tree's first slot (int32 [n_trees + 1]), 12 the leaf id of each slot's two children
+ * (int32 pairs), 13 the treelets with ranks in place of thresholds (absent when the plan does
+ * not use them).  *ptr stays valid until destroy or set_kernel.
  */
 bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const void **ptr,
                                      int64_t *bytes);

@@ -143,6 +143,12 @@ struct bridger_forest {
   std::vector<uint8_t> perfect_deep, perfect_bdeep;
   int32_t deep_tl = 0;
   void *d_perfect_deep = nullptr, *d_perfect_bdeep = nullptr;
+  // RAGGED treelets (layout in internal.h): blocks (fp32 thresholds / ranks), per kernel tree
+  // the first slot, per slot the leaf ids of its two children (4 words, 4 words, 1, 2 per slot)
+  std::vector<uint32_t> treelets, btreelets;
+  std::vector<int32_t> treelet_start, treelet_leaf;
+  void *d_treelets = nullptr, *d_btreelets = nullptr, *d_treelet_start = nullptr,
+       *d_treelet_leaf = nullptr;
   std::vector<uint64_t> ragged_brec;    // RAGGED records with ranks in place of thresholds
   std::vector<uint64_t> ragged_tops, ragged_btops;  // top-level heaps (fp32 / binned records)
   std::vector<int32_t> ragged_bchunk_first, ragged_bchunk_rec;
@@ -948,6 +954,102 @@ void build_sized_plans(bridger_forest *h, PlanInput pin, const Plan &big, bool b
   }
 }
 
+// RAGGED treelets (layout in internal.h) of every kernel tree, thresholds as bits or (binned)
+// their ranks; false when a tree needs more than 2^27 slots in all (32-bit byte offsets).
+bool make_treelets(const bridger_forest *h, const int64_t *offs, const int32_t *feat,
+                   const float *thr, const int32_t *left, const int32_t *right,
+                   const float *value, bool binned, std::vector<uint32_t> &blk,
+                   std::vector<int32_t> &start, std::vector<int32_t> *leaf_ids) {
+  start.assign((size_t)h->n_trees + 1, 0);
+  int64_t total = 0;
+  std::vector<std::pair<int32_t, int32_t>> stack;
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int32_t t = h->tree_order[k];
+    const int64_t a = offs[t];
+    int32_t depth = 0;  // the tree's largest leaf depth
+    stack.assign(1, {0, 0});
+    while (!stack.empty()) {
+      const auto [nd, d] = stack.back();
+      stack.pop_back();
+      depth = std::max(depth, d);
+      if (left[a + nd] != -1) {
+        stack.push_back({left[a + nd], d + 1});
+        stack.push_back({right[a + nd], d + 1});
+      }
+    }
+    const int levels = depth / 2 + 1;  // treelet levels: nodes at tree levels 0, 2, ..., 2(levels-1)
+    if (2 * levels > 26) return false;
+    start[k] = (int32_t)total;
+    total += ((int64_t(1) << (2 * levels)) - 1) / 3;
+    if (total > (int64_t(1) << 27)) return false;
+  }
+  // the heaps are sparse (a ragged tree fills few of its deep slots): at most 8x the packed
+  // records' bytes and 512 MB, else the record walk serves (1000 trees up to depth 12: 74 MB
+  // against 11.3 MB)
+  if (total * 16 > std::min<int64_t>(8 * 8 * (int64_t)h->ragged_rec.size() + (1 << 20),
+                                     int64_t(512) << 20))
+    return false;
+  start[h->n_trees] = (int32_t)total;
+  // the LDS copy reads kTreeletCopyBytes from every tree's first slot, so the last tree is
+  // followed by that many zero bytes
+  const int64_t pad = kTreeletCopyBytes / 16;
+  blk.assign((size_t)(total + pad) * 4, 0u);
+  if (leaf_ids) leaf_ids->assign((size_t)(total + pad) * 2, -1);
+  auto w_of = [&](int64_t i) {
+    float th = thr[i];
+    if (th == 0.0f) th = 0.0f;
+    uint32_t w;
+    if (binned) w = rank_of(h, feat[i], th);
+    else std::memcpy(&w, &th, 4);
+    return w;
+  };
+  auto bits = [](float v) {
+    uint32_t w;
+    std::memcpy(&w, &v, 4);
+    return w;
+  };
+  std::vector<std::pair<int64_t, int32_t>> todo;  // (slot, node)
+  for (int32_t k = 0; k < h->n_trees; ++k) {
+    const int32_t t = h->tree_order[k];
+    const int64_t a = offs[t];
+    todo.assign(1, {0, 0});
+    while (!todo.empty()) {
+      const auto [sl, nd] = todo.back();
+      todo.pop_back();
+      uint32_t *b = &blk[(size_t)(start[k] + sl) * 4];
+      int32_t *lid = leaf_ids ? &(*leaf_ids)[(size_t)(start[k] + sl) * 2] : nullptr;
+      if (left[a + nd] == -1) {
+        b[0] = 0u;
+        b[1] = b[2] = bits(value[a + nd]);
+        b[3] = 3u << 30;
+        if (lid) lid[0] = lid[1] = nd;
+        continue;
+      }
+      const int32_t c[2] = {left[a + nd], right[a + nd]};
+      b[0] = w_of(a + nd);
+      b[3] = (uint32_t)feat[a + nd];
+      for (int j = 0; j < 2; ++j) {
+        const int64_t ci = a + c[j];
+        if (left[ci] == -1) {
+          b[1 + j] = bits(value[ci]);
+          b[3] |= 1u << (30 + j);
+          if (lid) lid[j] = c[j];
+        } else {
+          b[1 + j] = w_of(ci);
+          b[3] |= (uint32_t)feat[ci] << (10 + 10 * j);
+          todo.push_back({4 * sl + 1 + 2 * j, left[ci]});
+          todo.push_back({4 * sl + 2 + 2 * j, right[ci]});
+        }
+      }
+    }
+  }
+  return true;
+}
+
+bool treelets_wanted(const bridger_forest *h) {
+  return env_int("BRIDGER_TREELETS", 1) != 0 && !h->vec && h->F <= kDeepMaxFeatures;
+}
+
 // RAGGED records for bins: an internal record's threshold becomes its rank.
 void build_ragged_brec(bridger_forest *h) {
   h->ragged_brec = h->ragged_rec;
@@ -1032,7 +1134,8 @@ void free_all(bridger_forest *h) {
       free_dev(c.d_trav);
       free_dev(c.d_roots);
     }
-  for (void **q : {&h->d_perfect_deep, &h->d_perfect_bdeep, &h->d_ragged_tops,
+  for (void **q : {&h->d_treelets, &h->d_btreelets, &h->d_treelet_start, &h->d_treelet_leaf,
+                   &h->d_perfect_deep, &h->d_perfect_bdeep, &h->d_ragged_tops,
                    &h->d_ragged_btops, &h->d_q_values, &h->d_q_off,
                    &h->d_perfect_btrav, &h->d_ragged_brec,
                    &h->d_ragged_bchunk_first, &h->d_ragged_bchunk_rec, &h->d_pre_a, &h->d_pre_b,
@@ -1074,6 +1177,11 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_ragged.leaf_map, h->ragged_rec_node)) != BRIDGER_OK) return s;
     if (!h->ragged_tops.empty() && (s = upload(&h->d_ragged_tops, h->ragged_tops)) != BRIDGER_OK)
       return s;
+    if (!h->treelets.empty()) {
+      if ((s = upload(&h->d_treelets, h->treelets, 1024)) != BRIDGER_OK) return s;
+      if ((s = upload(&h->d_treelet_start, h->treelet_start)) != BRIDGER_OK) return s;
+      if ((s = upload(&h->d_treelet_leaf, h->treelet_leaf)) != BRIDGER_OK) return s;
+    }
   }
   if (h->bin_bytes) {
     if ((s = upload(&h->d_q_values, h->q_values)) != BRIDGER_OK) return s;
@@ -1096,6 +1204,8 @@ bridger_status upload_all(bridger_forest *h) {
     if ((s = upload(&h->d_ragged_bchunk_rec, h->ragged_bchunk_rec)) != BRIDGER_OK) return s;
     if (!h->ragged_btops.empty() &&
         (s = upload(&h->d_ragged_btops, h->ragged_btops)) != BRIDGER_OK)
+      return s;
+    if (!h->btreelets.empty() && (s = upload(&h->d_btreelets, h->btreelets, 1024)) != BRIDGER_OK)
       return s;
   }
   if ((s = upload(&h->d_direct.nodes, h->direct_rec)) != BRIDGER_OK) return s;
@@ -1311,7 +1421,14 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
       err = launch_perfect_fixed(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
     else if (h->kernel_active == kPerfect)
       err = launch_perfect(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
-    else if (p.global_nodes && p.tops) {
+    else if (p.global_nodes && p.tops && (binned ? h->d_btreelets : h->d_treelets)) {
+      a.nodes = (const uint8_t *)(binned ? h->d_btreelets : h->d_treelets);
+      a.nodes_bytes = (uint32_t)(4 * (binned ? h->btreelets.size() : h->treelets.size()));
+      a.tree_start = (const int32_t *)h->d_treelet_start;
+      a.leaf_map = (const int32_t *)h->d_treelet_leaf;
+      a.lds_top_off = h->F * p.rows_per_wg * xsz;
+      err = launch_ragged_treelet(a, p.waves, n_wg, p.lds_bytes, stream);
+    } else if (p.global_nodes && p.tops) {
       a.tops = (const uint64_t *)(binned ? h->d_ragged_btops : h->d_ragged_tops);
       a.nodes_bytes = (uint32_t)(8 * h->ragged_rec.size());
       a.top_levels = p.tops;
@@ -1557,9 +1674,14 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
       if (h->ragged_ok && !h->ragged_plan.global_nodes)
         h->ragged_plan.n_chunks = ragged_chunks(h, h->ragged_plan.chunk_bytes,
                                                 h->ragged_chunk_first, h->ragged_chunk_rec);
-      if (h->ragged_ok && h->ragged_plan.tops)
+      if (h->ragged_ok && h->ragged_plan.tops) {
         build_ragged_tops(h->ragged_rec, h->ragged_tree_start, h->n_trees, h->ragged_plan.tops,
                           h->ragged_tops);
+        if (treelets_wanted(h) &&
+            !make_treelets(h, tree_offsets, feature, threshold, left, right, value, false,
+                           h->treelets, h->treelet_start, &h->treelet_leaf))
+          h->treelets.clear();
+      }
     }
     // binned variants of the same layouts (used by bridger_forest_predict_binned)
     if (build_quantization(h, feature, threshold, left)) {
@@ -1586,9 +1708,14 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
         h->ragged_bok = h->ragged_bplan.waves > 0;
         if (h->ragged_bok) {
           build_ragged_brec(h);
-          if (h->ragged_bplan.tops)
+          if (h->ragged_bplan.tops) {
             build_ragged_tops(h->ragged_brec, h->ragged_tree_start, h->n_trees,
                               h->ragged_bplan.tops, h->ragged_btops);
+            if (!h->treelets.empty() &&
+                !make_treelets(h, tree_offsets, feature, threshold, left, right, value, true,
+                               h->btreelets, h->treelet_start, nullptr))
+              h->btreelets.clear();
+          }
           if (!h->ragged_bplan.global_nodes)
             h->ragged_bplan.n_chunks = ragged_chunks(h, h->ragged_bplan.chunk_bytes,
                                                      h->ragged_bchunk_first, h->ragged_bchunk_rec);
@@ -1948,6 +2075,14 @@ bridger_status bridger_forest_packed(bridger_forest_t h, int32_t which, const vo
       if (which == 1) return give(h->ragged_tree_start.data(), h->ragged_tree_start.size() * 4);
       if (which == 2) return give(h->ragged_rec_node.data(), h->ragged_rec_node.size() * 4);
       if (which == 4) return give(h->ragged_chunk_first.data(), h->ragged_chunk_first.size() * 4);
+      if (which == 10 && !h->treelets.empty())
+        return give(h->treelets.data(), h->treelets.size() * 4);
+      if (which == 11 && !h->treelet_start.empty())
+        return give(h->treelet_start.data(), h->treelet_start.size() * 4);
+      if (which == 12 && !h->treelet_leaf.empty())
+        return give(h->treelet_leaf.data(), h->treelet_leaf.size() * 4);
+      if (which == 13 && !h->btreelets.empty())
+        return give(h->btreelets.data(), h->btreelets.size() * 4);
       if (which == 7 && !h->ragged_tops.empty())
         return give(h->ragged_tops.data(), h->ragged_tops.size() * 8);
       break;

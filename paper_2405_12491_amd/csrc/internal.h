@@ -83,6 +83,17 @@ constexpr bool perfect_fixed_ok(int D, int CT) {
 // node m of level D - 1, {w(m), f(m), leaf value of 2m, leaf value of 2m + 1}, else the 2^D
 // leaf values.  Every block of a level is indexed by m - 2^level.
 constexpr int kDeepMaxFeatures = 1024;
+// RAGGED treelets (the global-node ragged kernel): per kernel tree a 4-ary heap of 16-byte
+// blocks, slot s holding the node n at tree level 2l of treelet level l and its two children:
+// {w(n), v(c0), v(c1), f(n) | f(c0) << 10 | f(c1) << 20 | leaf(c0) << 30 | leaf(c1) << 31},
+// v(c) = w(c) for an internal child, its leaf value for a leaf; the grandchild reached by
+// steps b1 (at n) and b2 (at c_b1) sits in slot 4s + 1 + 2 b1 + b2.  A leaf n takes {0, v(n),
+// v(n), 3 << 30}; unreachable slots are zero.  Feature indices below kDeepMaxFeatures.  The
+// first kTreeletTopSlots slots (levels 0-3) of a batch of kTreeletBatch trees are copied to the
+// wave's LDS, kTreeletCopyBytes per tree.
+constexpr int kTreeletTopSlots = 5;
+constexpr int kTreeletCopyBytes = 128;
+constexpr int kTreeletBatch = kTopWaveBytes / kTreeletCopyBytes;
 constexpr int deep_pair_off(int TL, int i) {
   int o = 0;
   for (int j = 0; j < i; ++j) o += 16 << (TL + 2 * j);
@@ -197,6 +208,8 @@ int launch_ragged(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, v
 int launch_ragged_global(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                          void *stream);
 int launch_ragged_top(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream);
+int launch_ragged_treelet(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                          void *stream);
 int launch_direct(const LaunchArgs &a, int64_t n_wg, void *stream);
 int launch_gemm(int depth, const LaunchArgs &a, int64_t n_wg, void *stream);
 

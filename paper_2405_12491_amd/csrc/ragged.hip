@@ -393,6 +393,151 @@ __global__ __launch_bounds__(1024) void ragged_top_kernel(LaunchArgs a) {
   }
 }
 
+// The lockstep global-node walk over two-level treelets (layout in internal.h): one 16-byte
+// load brings a node's threshold and feature and both children's (or their leaf values), so a
+// load covers two levels and a leaf child ends the walk without a load of its own.  Each wave
+// copies slots 0-4 (levels 0-3) of its next kTreeletBatch trees to its LDS buffer with one
+// 16-byte load per lane; deeper slots come from global memory through a buffer resource
+// (32-bit offsets; a read past the blocks returns zeros).  One class, scalar leaves; lane
+// groups of whole waves.
+template <bool LEAVES, int XB, int U>
+__global__ __launch_bounds__(1024) void ragged_treelet_kernel(LaunchArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  static_assert(U <= kTreeletBatch, "a batch's copies fit the wave's buffer");
+  constexpr uint32_t kCopy = (uint32_t)kTreeletCopyBytes;
+  const int tid = threadIdx.x;
+  const int R = a.rows_per_wg, G = a.groups;
+  const int r = tid & (R - 1);
+  const int g = __builtin_amdgcn_readfirstlane(tid / R);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int64_t row = (int64_t)blockIdx.x * R + r;
+  const bool row_ok = row < a.n_rows;
+  const uint32_t lane_off = (uint32_t)a.lds_x_off + tile_row_off<XB>(r);
+  const int shift = a.log2_row_bytes;
+  const int T = a.n_trees;
+  const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * kTopWaveBytes;
+
+  load_tile_all<XB, false>(smem, a, r, row, row_ok, g, G);
+  __syncthreads();
+
+  const int ga = (int)(((int64_t)T * g) / G), gb = (int)(((int64_t)T * (g + 1)) / G);
+  const uint8_t *blocks = a.nodes;
+  // slots 0 .. kCopy / 16 - 1 of trees q .. q + U - 1 (the last tree of the group repeated past
+  // the group's end) into this wave's buffer, tree u at buf + u * kCopy; returns this lane's
+  // tree's first slot, which lane 8u holds for tree u of the batch
+  auto copy_tops = [&](int q) {
+    const int t = min(q + lane / (int)(kCopy / 16), gb - 1);
+    const uint32_t piece = (uint32_t)(lane % (int)(kCopy / 16));
+    const int32_t first = a.tree_start[t];
+    __builtin_amdgcn_global_load_lds(
+        (const void *)(blocks + ((size_t)first + piece) * 16),
+        (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf), 16, 0, 0);
+    return first;
+  };
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)blocks, (short)0, (int)a.nodes_bytes, kBufferRsrcWord3);
+  auto load_block = [&](uint32_t slot) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, slot * 16u, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+  };
+  double acc = (!LEAVES && a.aggregate == 0 && g == 0) ? (double)a.base[0] : 0.0;
+  int32_t firsts = ga < gb ? copy_tops(ga) : 0;
+  for (int q = ga; q < gb; q += U) {
+    const int nvalid = gb - q < U ? gb - q : U;
+    wait_stage();  // this batch's slots have landed
+    uint32_t s[U], out[U];  // slot within the tree; on finishing: leaf value or leaf-id index
+    bool live[U];
+    uint4 blk[U];
+    int32_t base[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      base[u] = __builtin_amdgcn_readlane(firsts, u * (int)(kCopy / 16));
+      s[u] = 0u;
+      out[u] = 0u;
+      live[u] = true;
+    }
+    // one step of every live slot from its block: the node, then the child it chooses; a leaf
+    // child finishes the slot, an internal one moves it to the grandchild's slot
+    auto step = [&]() {
+      uint32_t x1[U], wc[U], fc[U], b1[U], x2[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        x1[u] = gather_x<false, XB>(smem, ((blk[u].w & 1023u) << shift) + lane_off);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        b1[u] = goes_right<XB>(x1[u], blk[u].x) ? 1u : 0u;
+        wc[u] = b1[u] ? blk[u].z : blk[u].y;
+        fc[u] = (blk[u].w >> (b1[u] ? 20 : 10)) & 1023u;
+        x2[u] = gather_x<false, XB>(smem, (fc[u] << shift) + lane_off);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (live[u]) {
+          if ((blk[u].w >> (30 + b1[u])) & 1u) {
+            live[u] = false;
+            out[u] = LEAVES ? ((uint32_t)base[u] + s[u]) * 2u + b1[u] : wc[u];
+          } else {
+            s[u] = 4u * s[u] + 1u + 2u * b1[u] + (goes_right<XB>(x2[u], wc[u]) ? 1u : 0u);
+          }
+        }
+      }
+    };
+    // treelet levels 0 and 1 (slots 0 .. 4) from the copy
+#pragma unroll
+    for (int lv = 0; lv < 2; ++lv) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t addr = buf + (uint32_t)u * kCopy + 16u * (s[u] < 5u ? s[u] : 0u);
+        const uint2 lo = lds_u64(smem, addr), hi = lds_u64(smem, addr + 8u);
+        blk[u] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+      step();
+    }
+    // the copy is read: the next batch's slots can land while the deeper levels run
+    if (q + U < gb) firsts = copy_tops(q + U);
+    // deeper treelets from global memory; a slot whose lanes have all finished skips its load
+    // (trees are at most 64 levels deep: 32 treelet levels; the bound keeps the loop finite)
+    for (int lv = 2; lv < 34; ++lv) {
+      bool any = false;
+#pragma unroll
+      for (int u = 0; u < U; ++u) any = any || live[u];
+      if (!any) break;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (live[u]) blk[u] = load_block((uint32_t)base[u] + s[u]);
+      step();
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u < nvalid) {
+        if (LEAVES) {
+          if (row_ok) a.out_leaf[row * (int64_t)T + a.tree_order[q + u]] = a.leaf_map[out[u]];
+        } else {
+          acc += (double)__uint_as_float(out[u]);
+        }
+      }
+    }
+  }
+  if (LEAVES) return;
+  // group sums: each thread's partial in its own wave's copy buffer (free once no copy is in
+  // flight), then group 0 adds the groups' partials of its row in group order
+  wait_stage();
+  auto slot = [&](int t) {
+    return reinterpret_cast<double *>(smem + a.lds_top_off + (t >> 6) * kTopWaveBytes +
+                                      (t & 63) * 8);
+  };
+  *slot(tid) = acc;
+  __syncthreads();
+  if (g == 0 && row_ok) {
+    double z = *slot(r);
+    for (int gg = 1; gg < G; ++gg) z += *slot(gg * R + r);
+    if (a.aggregate == 1) z = (double)a.base[0] + z / (double)a.class_count[0];
+    store_one(a, row, z);
+  }
+}
+
 // ---------------------------------------------------------------------- launchers
 template <int XB, int L>
 static int launch_ragged_top_xl(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
@@ -409,6 +554,24 @@ static int launch_ragged_top_x(const LaunchArgs &a, int waves, int64_t n_wg, int
   if (a.top_levels == 5) return launch_ragged_top_xl<XB, 5>(a, waves, n_wg, lds_bytes, stream);
   if (a.top_levels == 4) return launch_ragged_top_xl<XB, 4>(a, waves, n_wg, lds_bytes, stream);
   return (int)hipErrorInvalidValue;
+}
+
+// Four trees per batch: with eight (72 registers) one 16-wave workgroup fits a CU instead of
+// two (4M x 256 rows: 19.8 against 14.2 ms); six measured 21.3 ms.
+template <int XB>
+static int launch_ragged_treelet_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                                   void *stream) {
+  const int threads = 64 * waves;
+  if (a.out_leaf)
+    return launch_common(ragged_treelet_kernel<true, XB, 4>, threads, n_wg, lds_bytes, stream, a);
+  return launch_common(ragged_treelet_kernel<false, XB, 4>, threads, n_wg, lds_bytes, stream, a);
+}
+
+int launch_ragged_treelet(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
+                          void *stream) {
+  if (a.x_bytes == 2) return launch_ragged_treelet_x<2>(a, waves, n_wg, lds_bytes, stream);
+  if (a.x_bytes == 1) return launch_ragged_treelet_x<1>(a, waves, n_wg, lds_bytes, stream);
+  return launch_ragged_treelet_x<4>(a, waves, n_wg, lds_bytes, stream);
 }
 
 int launch_ragged_top(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes, void *stream) {

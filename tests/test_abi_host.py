@@ -566,3 +566,77 @@ def test_perfect_deep_blocks_absent():
     with host(concat_trees(trees, 1100)) as f:
         with pytest.raises(B.BridgerError):
             B.bridger_forest_packed(f.handle, 8, np.uint8)
+
+
+def walk_treelets(f: B.Forest, X, bins=None):
+    """The treelet walk (packed arrays 10-12; with bins, 13 and right iff bin > rank): slot s of
+    a tree holds a node and its two children; a leaf child ends the walk, an internal one moves
+    it to slot 4s + 1 + 2 b1 + b2."""
+    blk = B.bridger_forest_packed(f.handle, 13 if bins is not None else 10, np.uint32).reshape(-1, 4)
+    start = B.bridger_forest_packed(f.handle, 11, np.int32)
+    leaf_ids = B.bridger_forest_packed(f.handle, 12, np.int32)
+    order = B.bridger_forest_packed(f.handle, 3, np.int32)
+    T = f.n_trees
+    n = X.shape[0]
+    rows = np.arange(n)
+    V = bins if bins is not None else X
+
+    def right(w, x):
+        if bins is not None:
+            return (x > w.astype(np.int64)).astype(np.int64)
+        return np.where(x <= w.view(np.float32), 0, 1)
+
+    leaves = np.empty((n, T), np.int32)
+    vals = np.empty((n, T), np.float32)
+    for k in range(T):
+        s = np.zeros(n, np.int64)
+        done = np.zeros(n, bool)
+        lid = np.zeros(n, np.int64)
+        val = np.zeros(n, np.uint32)
+        for _ in range(40):
+            if done.all():
+                break
+            q = blk[start[k] + s]
+            b1 = right(q[:, 0].copy(), V[rows, q[:, 3] & 1023])
+            wc = np.where(b1 == 1, q[:, 2], q[:, 1]).astype(np.uint32)
+            fc = (q[:, 3] >> np.where(b1 == 1, 20, 10).astype(np.uint32)) & 1023
+            leaf = ((q[:, 3] >> (30 + b1).astype(np.uint32)) & 1) == 1
+            fin = ~done & leaf
+            lid[fin] = (start[k] + s[fin]) * 2 + b1[fin]
+            val[fin] = wc[fin]
+            go = ~done & ~leaf
+            b2 = right(wc, V[rows, fc])
+            s = np.where(go, 4 * s + 1 + 2 * b1 + b2, s)
+            done |= fin
+        assert done.all()
+        leaves[:, order[k]] = leaf_ids[lid]
+        vals[:, order[k]] = val.view(np.float32)
+    return leaves, vals
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_ragged_treelets(seed):
+    """Random one-class ragged forests (single-leaf trees, leaves at every level, depths up to
+    11, ties, NaN and infinite inputs) packed as two-level treelets: walking them reproduces
+    the oracle's leaf ids and leaf values, on fp32 rows and on bins."""
+    rng = np.random.default_rng(300 + seed)
+    F = int(rng.integers(1, 12))
+    model = random_tiny_forest(rng, int(rng.integers(1, 30)), F, max_depth=int(rng.integers(0, 12)),
+                               p_split=float(rng.uniform(0.3, 0.95)), thr_grid=[-1.0, -0.0, 0.0, 0.5, 1.0])
+    model = permute_nodes(model, rng)
+    X = rng.choice(np.array([-1.0, -0.0, 0.0, 0.5, 1.0, 2.0, np.nan, np.inf, -np.inf], np.float32), (96, F))
+    _, ref_lv, _ = oracle.predict(model, X, want_leaves=True)
+    ref_val = model.value[model.tree_offsets[:-1][None, :] + ref_lv].astype(np.float32)
+    with host(model) as f:
+        if f.kernel != B.BRIDGER_KERNEL_RAGGED:
+            f.kernel = B.BRIDGER_KERNEL_RAGGED
+        if not has_tops(f):
+            pytest.skip("plan without top levels")
+        lv, vals = walk_treelets(f, X)
+        assert np.array_equal(lv, ref_lv)
+        assert np.array_equal(vals, ref_val)
+        from oracle import binning
+        bins = binning.bin_rows(binning.tables(model), X)
+        lv, vals = walk_treelets(f, X, bins=bins)
+        assert np.array_equal(lv, ref_lv)
+        assert np.array_equal(vals, ref_val)

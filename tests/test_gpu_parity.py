@@ -318,15 +318,18 @@ def _variant_models():
 
 @pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1"}, {"BRIDGER_GLOBAL": "1", "BRIDGER_ILP": "2"},
                                  {"BRIDGER_GLOBAL": "1", "BRIDGER_ILP": "4"}, {"BRIDGER_GLOBAL": "0"},
-                                 {"BRIDGER_TOPS": "0"}, {"BRIDGER_TOP_LEVELS": "4"},
-                                 {"BRIDGER_TOP_LEVELS": "4", "BRIDGER_ROWS": "128"},
+                                 {"BRIDGER_TOPS": "0"}, {"BRIDGER_TREELETS": "0"},
+                                 {"BRIDGER_TREELETS": "0", "BRIDGER_TOP_LEVELS": "4"},
+                                 {"BRIDGER_TREELETS": "0", "BRIDGER_TOP_LEVELS": "4", "BRIDGER_ROWS": "128"},
                                  {"BRIDGER_ROWS": "256", "BRIDGER_WAVES": "8"},
+                                 {"BRIDGER_TREELETS": "0", "BRIDGER_ROWS": "256", "BRIDGER_WAVES": "8"},
                                  {"BRIDGER_COALESCED_TILE": "0"}],
                          ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
 def test_ragged_kernel_variants(env, monkeypatch):
     """The ragged kernel with records in LDS chunks and read from global memory (one or two
-    runs per lane; the top levels from per-wave LDS copies of 4 or 5 levels, with lane groups of
-    one, two or four waves, or without them), on ragged, multiclass and leaf-id cases."""
+    runs per lane; two-level treelets, or the top levels from per-wave LDS copies of 4 or 5
+    levels, with lane groups of one, two or four waves, or without them), on ragged,
+    multiclass and leaf-id cases."""
     for k, v in env.items():
         monkeypatch.setenv(k, v)
     rng = np.random.default_rng(91)
