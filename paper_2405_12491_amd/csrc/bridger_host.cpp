@@ -677,10 +677,12 @@ int perfect_top_group_bytes(int L, bool deep) {
   return env_int("BRIDGER_TOP_GROUP_KB", 1) == 2 ? 2048 : 1024;
 }
 
-// Deep blocks: scalar leaves, feature indices in 10 bits, trees deeper than the top levels.
-bool deep_possible(bool vec, int F, int depth) {
-  return env_int("BRIDGER_DEEP", 1) != 0 && !vec && F <= kDeepMaxFeatures &&
-         depth > perfect_top_levels(depth);
+// Deep blocks: scalar leaves, feature indices in 10 bits, trees deeper than the top levels,
+// all of them addressed by 32-bit byte offsets.
+bool deep_possible(bool vec, int F, int depth, int64_t n_trees) {
+  const int tl = perfect_top_levels(depth);
+  return env_int("BRIDGER_DEEP", 1) != 0 && !vec && F <= kDeepMaxFeatures && depth > tl &&
+         n_trees * deep_tree_bytes(depth, tl) < (int64_t(1) << 31);
 }
 
 // tops: the RAGGED variant whose top levels come from per-wave LDS copies (one class, scalar
@@ -915,7 +917,22 @@ void make_perfect_deep(const bridger_forest *h, int TL, bool binned, std::vector
 
 // The deep blocks serve the wide-row plans whose top levels come from LDS copies.
 bool deep_wanted(const bridger_forest *h) {
-  return deep_possible(h->vec, h->F, h->perfect_depth);
+  return deep_possible(h->vec, h->F, h->perfect_depth, h->n_trees);
+}
+
+// The most classes the trees of one lane group span when G groups split the kernel trees
+// (class-sorted) into contiguous ranges.
+int class_span(const bridger_forest *h, int G) {
+  auto class_of = [&](int t) {
+    return (int)(std::upper_bound(h->class_begin.begin(), h->class_begin.end(), t) -
+                 h->class_begin.begin()) - 1;
+  };
+  int span = 1;
+  for (int g = 0; g < G; ++g) {
+    const int t0 = (int)((int64_t)h->n_trees * g / G), t1 = (int)((int64_t)h->n_trees * (g + 1) / G);
+    if (t0 < t1) span = std::max(span, class_of(t1 - 1) - class_of(t0) + 1);
+  }
+  return span;
 }
 
 bool same_plan(const Plan &a, const Plan &b) {
@@ -1413,6 +1430,7 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
           a.acc_alias = 1;
           a.lds_acc_off = a.lds_x_off;
           a.lds_top_off = a.lds_x_off + h->F * p.rows_per_wg * xsz;
+          a.class_span = class_span(h, p.groups);
         }
       }
       err = launch_perfect_global(h->perfect_depth, a, p.waves, n_wg, p.lds_bytes, stream);
@@ -1652,7 +1670,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
                     (double)h->perfect_blob.size(), h->perfect_tree_bytes, true, visits};
       pin.vec = vec;
       pin.depth = D;
-      pin.deep = deep_possible(vec, n_features, D);
+      pin.deep = deep_possible(vec, n_features, D, n_trees);
       h->perfect_plan = pick_plan(pin);
       h->perfect_ok = h->perfect_plan.waves > 0;
       if (h->perfect_ok) {
@@ -1690,7 +1708,7 @@ bridger_status bridger_forest_create_ex(int32_t n_trees, const int64_t *tree_off
                       h->perfect_tree_bytes, true, visits, h->bin_bytes};
         pin.vec = vec;
         pin.depth = D;
-        pin.deep = deep_possible(vec, n_features, D);
+        pin.deep = deep_possible(vec, n_features, D, n_trees);
         h->perfect_bplan = pick_plan(pin);
         h->perfect_bok = h->perfect_bplan.waves > 0;
         if (h->perfect_bok) {

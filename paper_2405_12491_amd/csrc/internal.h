@@ -161,6 +161,7 @@ struct LaunchArgs {
   int32_t lds_x_off;           // byte offset of the feature tile in dynamic LDS
   int32_t lds_acc_off;         // byte offset of the partial-sum area (acc_in_lds)
   int32_t acc_alias;           // that area is the row tile's, written only after the walk
+  int32_t class_span;          // acc_alias: the most classes one lane group's trees span
   int32_t acc_in_lds;
   int32_t ilp;                 // trees walked at once per lane (the plan's ilp)
   int32_t finite_thresholds;   // PERFECT: every threshold is finite (sign-of-difference step)

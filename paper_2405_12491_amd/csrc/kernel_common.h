@@ -373,6 +373,54 @@ __device__ void finalize_store(const LaunchArgs &a, double *z, int stride, int64
   }
 }
 
+// Tile epilogue of the kernels whose G lane groups hold partial class sums: slot (k, g, r) at
+// z0[k * stride + g * R + r].  Each (row, class) sum is added in group order by one of the R * G
+// compute threads (threads 0 .. R * G - 1 of a tile of rows blockIdx.x * R + r, R a power of
+// two; every one of them calls this after a barrier) into slot (k, 0, r); then the first
+// group's lanes (tid < R) finish and store their rows.
+__device__ void groups_finalize_store(const LaunchArgs &a, double *z0, int R, int G, int stride,
+                                      int tid, int64_t row, bool row_ok) {
+  if (G > 1) {
+    for (int i = tid; i < R * a.K; i += R * G) {
+      const int k = i / R;
+      double *z = z0 + k * stride + (i - k * R);
+      double s = z[0];
+      for (int gg = 1; gg < G; ++gg) s += z[gg * R];
+      z[0] = s;
+    }
+    __syncthreads();
+    if (a.transform == 2 && !a.out_label && a.K > 1) {
+      // softmax, one (row, class) per thread as well: each thread finishes its row's K values
+      // as finalize_store does (same operations, same order) and writes its exponential into
+      // the second group's slot, free now; then each divides by the row's sum
+      const int K = a.K;
+      const int64_t row0 = (int64_t)blockIdx.x * R;  // the tile's first row
+      for (int i = tid; i < R * K; i += R * G) {
+        const int k = i / R, rr = i - k * R;
+        const double *z = z0 + rr;
+        auto v = [&](int j) {
+          const double x = z[j * stride];
+          return a.aggregate == 1 ? (double)a.base[j] + x / (double)a.class_count[j] : x;
+        };
+        double m = v(0);
+        for (int j = 1; j < K; ++j) m = v(j) > m ? v(j) : m;
+        z0[k * stride + R + rr] = exp(v(k) - m);
+      }
+      __syncthreads();
+      for (int i = tid; i < R * K; i += R * G) {
+        const int k = i / R, rr = i - k * R;
+        if (row0 + rr >= a.n_rows) continue;
+        const double *e = z0 + R + rr;
+        double sum = 0.0;
+        for (int j = 0; j < K; ++j) sum += e[j * stride];
+        a.out[(row0 + rr) * (int64_t)K + k] = (float)(e[k * stride] / sum);
+      }
+      return;
+    }
+  }
+  if (tid < R && row_ok) finalize_store(a, z0 + tid, stride, row);
+}
+
 // Per-lane class bookkeeping for forests with several classes or several tree groups.
 struct ClassAcc {
   double acc;

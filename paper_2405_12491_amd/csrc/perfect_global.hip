@@ -23,12 +23,15 @@ __device__ __forceinline__ uint32_t go_right(uint32_t w, uint32_t x) {
 // VK: 0 scalar leaves; 4 or 8 (K <= VK) or 64 vector leaves (class sums in registers / LDS).
 // TL: 0, or the number of top levels read from per-wave LDS copies (scalar leaves only).
 // DEEP: below the top levels the walk reads the deep blocks (layout in internal.h): one
-// 16-byte load per pair of levels, and the last level's block carries its two leaf values.
-// DEEP with 16 trees per lane holds 16 blocks of 16 bytes per lane: workgroups of at most 8
-// waves, so that a lane may use 256 registers; with 8 trees per lane, 16-wave workgroups.  GB: bytes of a lane group's top-level copy (one batch of U trees).  KS:
-// scalar leaves of at most KS classes with the group's class sums in registers, written only
-// after the walk into the row tile's LDS (acc_alias), which leaves the LDS to the tile and
-// the top-level copies during the walk.
+// 16-byte load per pair of levels; the last level's block carries its two leaf values, or
+// (an even number of deep levels) the last pair's load goes out together with that of the
+// four leaves under its node, so no load waits for the last pair.  DEEP with 16 trees per
+// lane holds 16 blocks of 16 bytes per lane: workgroups of at most 8 waves, so that a lane
+// may use 256 registers; with 8 trees per lane, 16-wave workgroups.  GB: bytes of a lane
+// group's top-level copy (one batch of U trees).  KS: scalar leaves, and the class sums of
+// the (at most KS) classes of a group's trees in registers, written only after the walk into
+// the row tile's LDS (acc_alias), which leaves the LDS to the tile and the top-level copies
+// during the walk.
 template <int D, int U, bool LEAVES, bool FIN, int XB, int VK = 0, int TL = 0, bool DEEP = false,
           int GB = 1024, int KS = 0>
 __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_kernel(LaunchArgs a) {
@@ -51,40 +54,79 @@ __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_ker
   constexpr uint32_t kLeafOff = 4u << D;
   constexpr uint32_t kFirstLeaf = 1u << D;
 
+  // Top levels from LDS (TL > 0): the wave's copies of its lane groups' first batch are issued
+  // before the row tile, so their latency overlaps the tile's.
+  constexpr uint32_t TBT = 8u << TL;  // bytes of one tree's top levels
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int gpw = R < 64 ? 64 / R : 1;              // lane groups per wave
+  const int gi = R < 64 ? lane / R : 0;             // this lane's group within the wave
+  const int gw0 = __builtin_amdgcn_readfirstlane((wave * 64) / R);  // the wave's first group
+  const uint32_t wave_bytes = (uint32_t)gpw * GB;
+  const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * wave_bytes;
+  static_assert(TL == 0 || U * TBT == GB,
+                "one lane group's batch is GB / 1024 16-byte-per-lane loads");
+  const int NB = ((T + G - 1) / G + U - 1) / U;     // batches of the largest group
+  // the tree ranges of the wave's (at most two) lane groups
+  int cb0[2], cb1[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int gc = gw0 + (i < gpw ? i : 0);
+    cb0[i] = (int)(((int64_t)T * gc) / G);
+    cb1[i] = (int)(((int64_t)T * (gc + 1)) / G);
+  }
+  constexpr int LPT = (int)TBT / 16;                 // 16-byte pieces per tree of the copy
+  auto copy_batch = [&](int j) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (i < gpw) {
+#pragma unroll
+        for (int k = 0; k < GB / 1024; ++k) {
+          const int piece = k * 64 + lane;           // this lane's piece of the batch
+          const int t = min(cb0[i] + j * U + piece / LPT, cb1[i] - 1);
+          __builtin_amdgcn_global_load_lds(
+              (const void *)(a.nodes + (size_t)t * tb + (uint32_t)(piece % LPT) * 16),
+              (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf +
+                                                         (uint32_t)i * GB + k * 1024u),
+              16, 0, 0);
+        }
+      }
+    }
+  };
+  if constexpr (TL > 0) copy_batch(0);
   load_tile_any<XB, FIN>(smem, a, r, row, row_ok, g, G);
   __syncthreads();
 
   double *acc_lds = reinterpret_cast<double *>(smem + a.lds_acc_off) + g * R + r;
   const int slot_stride = G * R;
   const int t_begin = (int)(((int64_t)T * g) / G), t_end = (int)(((int64_t)T * (g + 1)) / G);
+  // KS: the class of the group's first tree (register class slot 0)
+  int k0 = 0;
+  if (KS)
+    while (k0 + 1 < a.K && t_begin >= a.class_begin[k0 + 1]) ++k0;
   ClassAcc ca;
-  ca.k = 0;
-  ca.acc = class_init(a, 0, g == 0);
-  ca.next_b = a.class_begin[1];
+  ca.k = k0;
+  ca.acc = class_init(a, k0, g == 0);
+  ca.next_b = a.class_begin[k0 + 1];
   double vacc[VR];
   if (VK_REG) vec_init_reg(a, vacc, g == 0);
   if (VK == 64) vec_init(a, acc_lds, slot_stride, g == 0);
   // KS: a group's trees are contiguous and class-sorted, so each class is summed in one
-  // stretch; the running sum moves into cs[k] when the class changes
+  // stretch; when the class changes its finished sum is shifted into cs (cs[j] then holds class
+  // ca.k - 1 - j), so that no register is indexed at run time (the host takes this kernel only
+  // when every group's trees span at most KS classes)
   double cs[KS > 0 ? KS : 1];
-  if (KS) {
 #pragma unroll
-    for (int c = 0; c < KS; ++c) cs[c] = c < a.K ? class_init(a, c, g == 0) : 0.0;
-  }
+  for (int j = 0; j < (KS > 0 ? KS : 1); ++j) cs[j] = 0.0;
   auto advance_reg = [&](int t) {
-    if (t < ca.next_b) return;
-#pragma unroll
-    for (int c = 0; c < KS; ++c)
-      if (c == ca.k) cs[c] = ca.acc;
     while (t >= ca.next_b) {
+#pragma unroll
+      for (int j = KS - 1; j > 0; --j) cs[j] = cs[j - 1];
+      cs[0] = ca.acc;
       ca.k += 1;
+      ca.acc = class_init(a, ca.k, g == 0);
       ca.next_b = a.class_begin[ca.k + 1];
     }
-    double v = 0.0;
-#pragma unroll
-    for (int c = 0; c < KS; ++c)
-      if (c == ca.k) v = cs[c];
-    ca.acc = v;
   };
 
   auto finish = [&](auto &m, int q) {
@@ -125,43 +167,11 @@ __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_ker
     // instruction), issued as soon as the current batch has left its top levels.  The batch
     // loop is wave-uniform: batch j covers trees t_begin + jU .. + U - 1 of every group, slots
     // past a group's last tree walk that tree again and are not added.
-    constexpr uint32_t TBT = 8u << TL;  // bytes of one tree's top levels
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int gpw = R < 64 ? 64 / R : 1;              // lane groups per wave
-    const int gi = R < 64 ? lane / R : 0;             // this lane's group within the wave
-    const int gw0 = __builtin_amdgcn_readfirstlane((wave * 64) / R);  // the wave's first group
-    const uint32_t wave_bytes = (uint32_t)gpw * GB;
-    const uint32_t buf = (uint32_t)a.lds_top_off + (uint32_t)wave * wave_bytes;
-    static_assert(U * TBT == GB, "one lane group's batch is GB / 1024 16-byte-per-lane loads");
-    const int NB = ((T + G - 1) / G + U - 1) / U;     // batches of the largest group
-    // the tree ranges of the wave's (at most two) lane groups
-    int cb0[2], cb1[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int gc = gw0 + (i < gpw ? i : 0);
-      cb0[i] = (int)(((int64_t)T * gc) / G);
-      cb1[i] = (int)(((int64_t)T * (gc + 1)) / G);
-    }
-    constexpr int LPT = (int)TBT / 16;                 // 16-byte pieces per tree of the copy
-    auto copy_batch = [&](int j) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        if (i < gpw) {
-#pragma unroll
-          for (int k = 0; k < GB / 1024; ++k) {
-            const int piece = k * 64 + lane;           // this lane's piece of the batch
-            const int t = min(cb0[i] + j * U + piece / LPT, cb1[i] - 1);
-            __builtin_amdgcn_global_load_lds(
-                (const void *)(a.nodes + (size_t)t * tb + (uint32_t)(piece % LPT) * 16),
-                (__attribute__((address_space(3))) void *)((lds_byte *)smem + buf +
-                                                           (uint32_t)i * GB + k * 1024u),
-                16, 0, 0);
-          }
-        }
-      }
-    };
-    copy_batch(0);
+    // deep blocks through a buffer resource: 32-bit byte offsets, and a read outside the blocks
+    // returns zeros instead of faulting
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const __amdgpu_buffer_rsrc_t drs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.deep, (short)0, T * a.deep_tree_bytes, kBufferRsrcWord3);
     for (int j = 0; j < NB; ++j) {
       const int q = t_begin + j * U;
       wait_stage();  // this batch's top levels have landed
@@ -190,21 +200,36 @@ __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_ker
       float lv[U];
       if constexpr (DEEP) {
         constexpr int ND = D - TL, NP = ND / 2;
+        // D - TL even: the last pair's node m has the four leaves of its grandchildren, 16
+        // contiguous bytes of the leaf array, loaded with its block (not with 16 register class
+        // sums in a 1024-thread workgroup: no registers left for them)
+        constexpr bool QUAD = !(ND & 1) && !LEAVES && !(KS > 4 && U <= 8);
         const uint32_t l2rb = (uint32_t)a.log2_row_bytes;
-        const uint8_t *dbase[U];
+        uint32_t doff[U];  // byte offsets of the trees' blocks (below 2^31, checked on the host)
 #pragma unroll
         for (int u = 0; u < U; ++u)
-          dbase[u] = a.deep + (size_t)min(q + u, t_end - 1) * (uint32_t)a.deep_tree_bytes;
+          doff[u] = (uint32_t)min(q + u, t_end - 1) * (uint32_t)a.deep_tree_bytes;
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
           // levels d and d + 1: node m's block holds both children's thresholds and features
           const int d = TL + 2 * i;
-          const int off = deep_pair_off(TL, i) - (16 << d);
+          const uint32_t off = (uint32_t)(deep_pair_off(TL, i) - (16 << d));
           uint4 blk[U];
+          uint4 quad[QUAD ? U : 1];
           uint32_t xv[U], b[U];
 #pragma unroll
-          for (int u = 0; u < U; ++u)
-            blk[u] = *reinterpret_cast<const uint4 *>(dbase[u] + off + (m[u] << 4));
+          for (int u = 0; u < U; ++u) {
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(drs, doff[u] + off + (m[u] << 4), 0, 0);
+            blk[u] = make_uint4(v.x, v.y, v.z, v.w);
+          }
+          if (QUAD && i == NP - 1) {
+            constexpr uint32_t qoff = (uint32_t)(deep_pair_off(TL, NP) - (16 << (D - 2)));
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+              const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(drs, doff[u] + qoff + (m[u] << 4), 0, 0);
+              quad[QUAD ? u : 0] = make_uint4(v.x, v.y, v.z, v.w);
+            }
+          }
 #pragma unroll
           for (int u = 0; u < U; ++u)
             xv[u] = gather_x<FIN, XB>(smem, ((blk[u].w & 1023u) << l2rb) + lane_off);
@@ -216,17 +241,27 @@ __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_ker
             xv[u] = gather_x<FIN, XB>(smem, (f2 << l2rb) + lane_off);
           }
 #pragma unroll
-          for (int u = 0; u < U; ++u)
-            m[u] = 4u * m[u] + 2u * b[u] + go_right<FIN, XB>(blk[u].x, xv[u]);
+          for (int u = 0; u < U; ++u) {
+            const uint32_t b2 = go_right<FIN, XB>(blk[u].x, xv[u]);
+            if (QUAD && i == NP - 1) {
+              const uint4 qv = quad[QUAD ? u : 0];
+              const uint32_t lo = b2 ? qv.y : qv.x, hi = b2 ? qv.w : qv.z;
+              lv[u] = __uint_as_float(b[u] ? hi : lo);
+            }
+            m[u] = 4u * m[u] + 2u * b[u] + b2;
+          }
         }
         if constexpr (ND & 1) {
           // level D - 1 with its two leaf values
-          constexpr int off = deep_pair_off(TL, NP) - (16 << (D - 1));
+          constexpr uint32_t off = (uint32_t)(deep_pair_off(TL, NP) - (16 << (D - 1)));
           uint4 blk[U];
           uint32_t xv[U];
 #pragma unroll
           for (int u = 0; u < U; ++u)
-            blk[u] = *reinterpret_cast<const uint4 *>(dbase[u] + off + (m[u] << 4));
+          {
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(drs, doff[u] + off + (m[u] << 4), 0, 0);
+            blk[u] = make_uint4(v.x, v.y, v.z, v.w);
+          }
 #pragma unroll
           for (int u = 0; u < U; ++u) xv[u] = gather_x<FIN, XB>(smem, (blk[u].y << l2rb) + lane_off);
 #pragma unroll
@@ -235,11 +270,6 @@ __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_ker
             lv[u] = __uint_as_float(bb ? blk[u].w : blk[u].z);
             m[u] = 2u * m[u] + bb;
           }
-        } else if (!LEAVES) {
-          constexpr int off = deep_pair_off(TL, NP) - (4 << D);
-#pragma unroll
-          for (int u = 0; u < U; ++u)
-            lv[u] = *reinterpret_cast<const float *>(dbase[u] + off + (m[u] << 2));
         }
       } else if (!LEAVES) {
 #pragma unroll
@@ -279,30 +309,26 @@ __global__ __launch_bounds__(DEEP && U > 8 ? 512 : 1024) void perfect_global_ker
   }
   if (LEAVES) return;
   if (KS) {
-#pragma unroll
-    for (int c = 0; c < KS; ++c)
-      if (c == ca.k) cs[c] = ca.acc;
     // the sums go into the row tile's LDS: every group must be done with the tile (no copy of
-    // top levels is in flight after the last batch)
+    // top levels is in flight after the last batch); classes outside the group's span get
+    // their initial value (the base score in the first group)
     __syncthreads();
+    for (int c = 0; c < a.K; ++c) {
+      const int d = ca.k - c;  // class c's sum: ca.acc (d = 0) or cs[d - 1] (k0 <= c < ca.k)
+      double v = d == 0 ? ca.acc : class_init(a, c, g == 0);
 #pragma unroll
-    for (int c = 0; c < KS; ++c)
-      if (c < a.K) acc_lds[c * slot_stride] = cs[c];
+      for (int j = 0; j < KS; ++j)
+        if (c >= k0 && d == j + 1) v = cs[j];
+      acc_lds[c * slot_stride] = v;
+    }
   } else if (VK_REG) {
     vec_store_reg(a, vacc, acc_lds, slot_stride);
   } else if (!VK) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
-  if (g == 0) {
-    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
-    for (int k = 0; k < a.K; ++k) {
-      double s = z[k * slot_stride];
-      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
-      z[k * slot_stride] = s;
-    }
-    if (row_ok) finalize_store(a, z, slot_stride, row);
-  }
+  groups_finalize_store(a, reinterpret_cast<double *>(smem + a.lds_acc_off), R, G, slot_stride,
+                        tid, row, row_ok);
 }
 
 // ---------------------------------------------------------------------- launchers
@@ -316,6 +342,9 @@ static int launch_global_deep_tg(const LaunchArgs &a, int threads, int64_t n_wg,
     if (a.out_leaf)
       return launch_common(perfect_global_kernel<D, U, true, FIN, XB, 0, TL, true, GB>, threads,
                            n_wg, lds_bytes, stream, a);
+    if (a.acc_alias && a.class_span <= 4)
+      return launch_common(perfect_global_kernel<D, U, false, FIN, XB, 0, TL, true, GB, 4>,
+                           threads, n_wg, lds_bytes, stream, a);
     if (a.acc_alias)
       return launch_common(perfect_global_kernel<D, U, false, FIN, XB, 0, TL, true, GB, 16>,
                            threads, n_wg, lds_bytes, stream, a);

@@ -159,15 +159,8 @@ __global__ __launch_bounds__(1024) void perfect_kernel(LaunchArgs a) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
-  if (g == 0) {
-    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
-    for (int k = 0; k < a.K; ++k) {
-      double s = z[k * slot_stride];
-      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
-      z[k * slot_stride] = s;
-    }
-    if (row_ok) finalize_store(a, z, slot_stride, row);
-  }
+  groups_finalize_store(a, reinterpret_cast<double *>(smem + a.lds_acc_off), R, G, slot_stride,
+                        tid, row, row_ok);
 }
 
 // Launch for one depth and element size; U is chosen from the plan (lane-group plans pick it

@@ -109,15 +109,8 @@ __global__ __launch_bounds__(1024) void ragged_kernel(LaunchArgs a) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
-  if (g == 0) {
-    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
-    for (int k = 0; k < a.K; ++k) {
-      double s = z[k * slot_stride];
-      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
-      z[k * slot_stride] = s;
-    }
-    if (row_ok) finalize_store(a, z, slot_stride, row);
-  }
+  groups_finalize_store(a, reinterpret_cast<double *>(smem + a.lds_acc_off), R, G, slot_stride,
+                        tid, row, row_ok);
 }
 
 // Records read from global memory instead of LDS chunks (big forests on wide rows, where a
@@ -221,15 +214,8 @@ __global__ __launch_bounds__(1024) void ragged_global_kernel(LaunchArgs a) {
     class_flush_all(a, ca, acc_lds, slot_stride, g == 0);
   }
   __syncthreads();
-  if (g == 0) {
-    double *z = reinterpret_cast<double *>(smem + a.lds_acc_off) + r;
-    for (int k = 0; k < a.K; ++k) {
-      double s = z[k * slot_stride];
-      for (int gg = 1; gg < G; ++gg) s += z[k * slot_stride + gg * R];
-      z[k * slot_stride] = s;
-    }
-    if (row_ok) finalize_store(a, z, slot_stride, row);
-  }
+  groups_finalize_store(a, reinterpret_cast<double *>(smem + a.lds_acc_off), R, G, slot_stride,
+                        tid, row, row_ok);
 }
 
 // The same lockstep walk for one output class with scalar leaves (or leaf ids), when every

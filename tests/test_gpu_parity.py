@@ -353,14 +353,17 @@ def test_ragged_kernel_variants(env, monkeypatch):
 def _class_layouts(T, rng):
     """Class assignments that stress the global kernels' class slots (a lane group's tree
     range is contiguous in class order): empty classes, one-tree classes next to classes
-    spread over several groups, and classes given in shuffled tree order."""
+    spread over several groups, classes given in shuffled tree order, and groups whose trees
+    span more classes (empty ones between) than the kernels' small register class slots hold."""
     K1 = 7
     tc1 = np.array([0] * 20 + [1] + [3] * 2 + [4] * 30 + [6] * (T - 53))  # 2 and 5 empty
     K2 = 12
     tc2 = np.arange(T) % K2                                                # interleaved
     K3 = 3
     tc3 = np.r_[np.zeros(T - 2, int), [1, 2]]                              # one huge class
-    return [(K1, rng.permutation(tc1)), (K2, tc2), (K3, tc3)]
+    K4 = 16
+    tc4 = np.repeat([0, 5, 10, 15], [14, 18, 15, T - 47])                  # spans of 6 classes
+    return [(K1, rng.permutation(tc1)), (K2, tc2), (K3, tc3), (K4, tc4)]
 
 
 @pytest.mark.parametrize("family", ["perfect", "ragged"])
