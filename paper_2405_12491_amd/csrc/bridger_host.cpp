@@ -1007,9 +1007,9 @@ bool make_treelets(const bridger_forest *h, const int64_t *offs, const int32_t *
                                      int64_t(512) << 20))
     return false;
   start[h->n_trees] = (int32_t)total;
-  // the LDS copy reads kTreeletCopyBytes from every tree's first slot, so the last tree is
-  // followed by that many zero bytes
-  const int64_t pad = kTreeletCopyBytes / 16;
+  // an LDS copy reads up to 21 slots (treelet levels 0-2) from every tree's first slot, so the
+  // last tree is followed by that many zero slots
+  const int64_t pad = 21;
   blk.assign((size_t)(total + pad) * 4, 0u);
   if (leaf_ids) leaf_ids->assign((size_t)(total + pad) * 2, -1);
   auto w_of = [&](int64_t i) {
@@ -1445,6 +1445,9 @@ bridger_status launch_rows(bridger_forest *h, const void *X, int64_t n_rows, flo
       a.tree_start = (const int32_t *)h->d_treelet_start;
       a.leaf_map = (const int32_t *)h->d_treelet_leaf;
       a.lds_top_off = h->F * p.rows_per_wg * xsz;
+      // treelet levels from the LDS copy: 3 (three trees a batch; 4M x 256 rows 14.15 ms,
+      // 1M x 28 rows 0.362 ms) or 2 (four trees: 14.22 and 0.374 ms)
+      a.top_levels = env_int("BRIDGER_TREELET_LDS_LEVELS", 3) == 2 ? 2 : 3;
       err = launch_ragged_treelet(a, p.waves, n_wg, p.lds_bytes, stream);
     } else if (p.global_nodes && p.tops) {
       a.tops = (const uint64_t *)(binned ? h->d_ragged_btops : h->d_ragged_tops);

@@ -89,8 +89,9 @@ constexpr int kDeepMaxFeatures = 1024;
 // v(c) = w(c) for an internal child, its leaf value for a leaf; the grandchild reached by
 // steps b1 (at n) and b2 (at c_b1) sits in slot 4s + 1 + 2 b1 + b2.  A leaf n takes {0, v(n),
 // v(n), 3 << 30}; unreachable slots are zero.  Feature indices below kDeepMaxFeatures.  The
-// first kTreeletTopSlots slots (levels 0-3) of a batch of kTreeletBatch trees are copied to the
-// wave's LDS, kTreeletCopyBytes per tree.
+// first kTreeletTopSlots slots (levels 0-3) of each tree of a batch are copied to the wave's
+// LDS, kTreeletCopyBytes per tree (or the first 21 slots, levels 0-5, 336 bytes per tree);
+// the last tree is followed by 21 zero slots.
 constexpr int kTreeletTopSlots = 5;
 constexpr int kTreeletCopyBytes = 128;
 constexpr int kTreeletBatch = kTopWaveBytes / kTreeletCopyBytes;

@@ -382,15 +382,19 @@ __global__ __launch_bounds__(1024) void ragged_top_kernel(LaunchArgs a) {
 // The lockstep global-node walk over two-level treelets (layout in internal.h): one 16-byte
 // load brings a node's threshold and feature and both children's (or their leaf values), so a
 // load covers two levels and a leaf child ends the walk without a load of its own.  Each wave
-// copies slots 0-4 (levels 0-3) of its next kTreeletBatch trees to its LDS buffer with one
-// 16-byte load per lane; deeper slots come from global memory through a buffer resource
-// (32-bit offsets; a read past the blocks returns zeros).  One class, scalar leaves; lane
-// groups of whole waves.
-template <bool LEAVES, int XB, int U>
+// copies the first slots of its next U trees to its LDS buffer with one 16-byte load per lane
+// (slots 0-20, tree levels 0-5, of three trees; or slots 0-4 of four); deeper slots come from
+// global memory through a buffer resource (32-bit offsets; a read past the blocks returns
+// zeros).  One class, scalar leaves; lane groups of whole waves.
+// LT: treelet levels read from the copy, 2 (slots 0-4, kTreeletCopyBytes per tree) or 3
+// (slots 0-20, 336 bytes per tree: three trees per buffer).
+template <bool LEAVES, int XB, int U, int LT = 2>
 __global__ __launch_bounds__(1024) void ragged_treelet_kernel(LaunchArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  static_assert(U <= kTreeletBatch, "a batch's copies fit the wave's buffer");
-  constexpr uint32_t kCopy = (uint32_t)kTreeletCopyBytes;
+  static_assert(LT == 2 || LT == 3, "two or three treelet levels from the copy");
+  constexpr uint32_t kSlots = LT == 2 ? (uint32_t)kTreeletTopSlots : 21u;
+  constexpr uint32_t kCopy = LT == 2 ? (uint32_t)kTreeletCopyBytes : 16u * kSlots;
+  static_assert(U * kCopy <= (uint32_t)kTopWaveBytes, "a batch's copies fit the wave's buffer");
   const int tid = threadIdx.x;
   const int R = a.rows_per_wg, G = a.groups;
   const int r = tid & (R - 1);
@@ -470,12 +474,12 @@ __global__ __launch_bounds__(1024) void ragged_treelet_kernel(LaunchArgs a) {
         }
       }
     };
-    // treelet levels 0 and 1 (slots 0 .. 4) from the copy
+    // treelet levels 0 .. LT - 1 (slots 0 .. kSlots - 1) from the copy
 #pragma unroll
-    for (int lv = 0; lv < 2; ++lv) {
+    for (int lv = 0; lv < LT; ++lv) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const uint32_t addr = buf + (uint32_t)u * kCopy + 16u * (s[u] < 5u ? s[u] : 0u);
+        const uint32_t addr = buf + (uint32_t)u * kCopy + 16u * (s[u] < kSlots ? s[u] : 0u);
         const uint2 lo = lds_u64(smem, addr), hi = lds_u64(smem, addr + 8u);
         blk[u] = make_uint4(lo.x, lo.y, hi.x, hi.y);
       }
@@ -485,7 +489,7 @@ __global__ __launch_bounds__(1024) void ragged_treelet_kernel(LaunchArgs a) {
     if (q + U < gb) firsts = copy_tops(q + U);
     // deeper treelets from global memory; a slot whose lanes have all finished skips its load
     // (trees are at most 64 levels deep: 32 treelet levels; the bound keeps the loop finite)
-    for (int lv = 2; lv < 34; ++lv) {
+    for (int lv = LT; lv < 34; ++lv) {
       bool any = false;
 #pragma unroll
       for (int u = 0; u < U; ++u) any = any || live[u];
@@ -542,12 +546,18 @@ static int launch_ragged_top_x(const LaunchArgs &a, int waves, int64_t n_wg, int
   return (int)hipErrorInvalidValue;
 }
 
-// Four trees per batch: with eight (72 registers) one 16-wave workgroup fits a CU instead of
-// two (4M x 256 rows: 19.8 against 14.2 ms); six measured 21.3 ms.
+// Two treelet levels from the copy: four trees per batch; with eight (72 registers) one
+// 16-wave workgroup fits a CU instead of two (4M x 256 rows: 19.8 against 14.2 ms); six
+// measured 21.3 ms.  Three levels from the copy: three trees per batch.
 template <int XB>
 static int launch_ragged_treelet_x(const LaunchArgs &a, int waves, int64_t n_wg, int lds_bytes,
                                    void *stream) {
   const int threads = 64 * waves;
+  if (a.top_levels == 3) {  // three treelet levels from the copy, three trees per batch
+    if (a.out_leaf)
+      return launch_common(ragged_treelet_kernel<true, XB, 3, 3>, threads, n_wg, lds_bytes, stream, a);
+    return launch_common(ragged_treelet_kernel<false, XB, 3, 3>, threads, n_wg, lds_bytes, stream, a);
+  }
   if (a.out_leaf)
     return launch_common(ragged_treelet_kernel<true, XB, 4>, threads, n_wg, lds_bytes, stream, a);
   return launch_common(ragged_treelet_kernel<false, XB, 4>, threads, n_wg, lds_bytes, stream, a);

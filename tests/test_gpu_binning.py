@@ -82,7 +82,7 @@ def test_binned_adversarial(F):
 
 @pytest.mark.parametrize("env", [{"BRIDGER_GLOBAL": "1"}, {"BRIDGER_GLOBAL": "0"},
                                  {"BRIDGER_GLOBAL": "1", "BRIDGER_DEEP": "0"},
-                                 {"BRIDGER_TREELETS": "0"},
+                                 {"BRIDGER_TREELETS": "0"}, {"BRIDGER_TREELET_LDS_LEVELS": "2"},
                                  {"BRIDGER_GLOBAL": "1", "BRIDGER_PERFECT_TOP_LEVELS": "3"},
                                  {"BRIDGER_ILP": "1", "BRIDGER_WAVES": "4", "BRIDGER_ROWS": "128"},
                                  # the binning pass: row kernel, stream kernel, small LDS buffers

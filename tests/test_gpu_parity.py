@@ -323,7 +323,9 @@ def _variant_models():
                                  {"BRIDGER_TREELETS": "0", "BRIDGER_TOP_LEVELS": "4", "BRIDGER_ROWS": "128"},
                                  {"BRIDGER_ROWS": "256", "BRIDGER_WAVES": "8"},
                                  {"BRIDGER_TREELETS": "0", "BRIDGER_ROWS": "256", "BRIDGER_WAVES": "8"},
-                                 {"BRIDGER_COALESCED_TILE": "0"}],
+                                 {"BRIDGER_COALESCED_TILE": "0"},
+                                 {"BRIDGER_TREELET_LDS_LEVELS": "2"},
+                                 {"BRIDGER_TREELET_LDS_LEVELS": "2", "BRIDGER_ROWS": "256", "BRIDGER_WAVES": "8"}],
                          ids=lambda e: ",".join(f"{k[8:]}={v}" for k, v in e.items()))
 def test_ragged_kernel_variants(env, monkeypatch):
     """The ragged kernel with records in LDS chunks and read from global memory (one or two
