@@ -365,7 +365,13 @@ def _class_layouts(T, rng):
     tc3 = np.r_[np.zeros(T - 2, int), [1, 2]]                              # one huge class
     K4 = 16
     tc4 = np.repeat([0, 5, 10, 15], [14, 18, 15, T - 47])                  # spans of 6 classes
-    return [(K1, rng.permutation(tc1)), (K2, tc2), (K3, tc3), (K4, tc4)]
+    # with 16 groups of 4 trees: the widest group spans exactly 4 classes (the small slot
+    # count), or exactly 5, with an empty class inside (the large one)
+    K5 = 5
+    tc5 = np.array([0] * 4 + [1, 2, 3, 4] + [4] * (T - 8))
+    K6 = 9
+    tc6 = np.array([0] * 4 + [1, 2, 3, 4] + [4] * 4 + [4, 6, 7, 8] + [8] * (T - 16))
+    return [(K1, rng.permutation(tc1)), (K2, tc2), (K3, tc3), (K4, tc4), (K5, tc5), (K6, tc6)]
 
 
 @pytest.mark.parametrize("family", ["perfect", "ragged"])
